@@ -1,0 +1,63 @@
+"""Plant plausible mistakes in copies of oracle.c and require the pins to catch
+each one (CPU only).  Nothing here touches the real oracle build."""
+import os
+import shutil
+import tempfile
+
+import pytest
+
+import oracle
+from oracle import build as obuild
+from oracle_pins import ALL_PINS
+
+SRC = os.path.join(os.path.dirname(obuild.__file__), "oracle.c")
+
+# (name, text in oracle.c, replacement)
+MUTANTS = [
+    ("scale dropped", "score[j] = a->scale * dot;", "score[j] = dot;"),
+    ("window one short", "j >= p - a->window + 1", "j >= p - a->window + 2"),
+    ("window one long", "j >= p - a->window + 1", "j >= p - a->window"),
+    ("causal excludes own token", "if (j > p) return 0;", "if (j >= p) return 0;"),
+    ("no causal mask", "if (j > p) return 0;", "if (j > p + 1000000) return 0;"),
+    ("top-left alignment", "int p = S - a->q_len + i;", "int p = i;"),
+    ("sinks one too many", "return j < a->n_sink ||", "return j <= a->n_sink ||"),
+    ("GQA heads interleaved", "int hk = h / G;", "int hk = h % a->Hkv;"),
+    ("K and V swapped in scores", "load_elem(a->k, a->dtype, k_off + c);",
+     "load_elem(a->v, a->dtype, k_off + c);"),
+    ("lse without max", "m + log(Z) : -INFINITY", "log(Z) : -INFINITY"),
+    ("lse in log2", "m + log(Z) : -INFINITY", "m + log2(Z) : -INFINITY"),
+    ("row order transposed", "int h = (int)(row % a->Hq);\n    int i = (int)((row / a->Hq) % a->q_len);",
+     "int i = (int)(row % a->q_len);\n    int h = (int)((row / a->q_len) % a->Hq);"),
+    ("page slot wrong", "tok = j % a->page_size;", "tok = (j + 1) % a->page_size;"),
+    ("bf16 widened wrongly", "[idx]) << 16;", "[idx]) << 15;"),
+    ("merge without max shift", "total += exp(l - mx);", "total += exp(l);"),
+    ("merge weight unnormalised", "double w = exp(l - lse_r);", "double w = exp(l - mx);"),
+    ("merge keeps empty parts", "if (l == -INFINITY) continue;\n      double w",
+     "if (0) continue;\n      double w"),
+]
+
+
+@pytest.fixture(scope="module")
+def tmpdir_mod():
+    d = tempfile.mkdtemp(prefix="oracle_mutants_")
+    yield d
+    shutil.rmtree(d, ignore_errors=True)
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(name, old, new, tmpdir_mod):
+    text = open(SRC).read()
+    assert text.count(old) >= 1, f"mutation anchor not found: {old!r}"
+    mutated = text.replace(old, new)
+    tag = "".join(ch if ch.isalnum() else "_" for ch in name)
+    src = os.path.join(tmpdir_mod, f"{tag}.c")
+    with open(src, "w") as f:
+        f.write(mutated)
+    lib = oracle.open_library(obuild.build(src=src, out=os.path.join(tmpdir_mod, f"{tag}.so")))
+    caught = []
+    for pin in ALL_PINS:
+        try:
+            pin(lib=lib)
+        except (AssertionError, ValueError):
+            caught.append(pin.__name__)
+    assert caught, f"no pin catches the planted mistake '{name}'"
