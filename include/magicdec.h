@@ -1,0 +1,171 @@
+/*
+ * magicdec.h -- C ABI of libmagicdec.so: batched GQA decode attention for
+ * speculative decoding with a sparse-KV self-speculative draft (MagicDec,
+ * arXiv 2408.11049), on AMD Instinct MI355X (gfx950).
+ *
+ * The paper's hot path at large batch and long context is attention over the
+ * KV cache: its loading cost grows with both batch size and sequence length
+ * and dominates the decode step (Sec. 1 insight 1; Sec. 3.2), and verification
+ * of gamma+1 speculated tokens shares that loading cost with plain decoding
+ * (Sec. 3.2), while the draft reads only a fixed-budget compressed cache
+ * (Sec. 4.1, Eq. 3; StreamingLLM-style drafting, Sec. 5.1).
+ *
+ * Conventions shared by every entry point
+ *   - All pointers in md_attn_args are DEVICE pointers except where noted.
+ *     The caller owns every buffer; the library allocates nothing per call
+ *     and keeps no pointer after it returns.
+ *   - Calls are asynchronous on `stream` (a hipStream_t passed as void*;
+ *     NULL is the null stream).  Buffers must stay alive and unmodified until
+ *     the stream reaches the call.  Nothing synchronises with the host.
+ *   - Calls are thread-safe and re-entrant.  The only global state is a
+ *     per-device cache of the compute-unit count.
+ *   - Errors are return codes (md_status).  Argument errors are detected on
+ *     the host before any HIP call, so a failed call has launched nothing.
+ *   - Device-side contract violations are not detected: kv_lens[b] < q_len
+ *     yields rows with an empty key set (O = 0, lse = -inf); kv_lens[b] is
+ *     clamped to max_kv_len; page ids outside [0, num_pages) are never
+ *     dereferenced (those tokens read as zero).  Results are then meaningless
+ *     but memory stays in bounds.
+ */
+#ifndef MAGICDEC_H_
+#define MAGICDEC_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MD_OK = 0,
+  MD_ERR_INVALID_ARG = 1, /* a malformed argument (see each entry point) */
+  MD_ERR_UNSUPPORTED = 2, /* valid, but this shape or dtype is not built */
+  MD_ERR_WORKSPACE = 3,   /* workspace missing, too small or misaligned */
+  MD_ERR_HIP = 4          /* the HIP runtime reported an error on launch */
+} md_status;
+
+typedef enum { MD_F32 = 0, MD_BF16 = 1 } md_dtype;
+
+typedef enum { MD_MODE_VERIFY = 0, MD_MODE_DRAFT = 1 } md_mode;
+
+/*
+ * One attention call over a batch of B sequences for one layer.
+ *
+ * Shapes (B = num_seqs, L = q_len = gamma + 1, Hq = num_q_heads,
+ * Hkv = num_kv_heads, d = head_dim, G = Hq / Hkv):
+ *   q   [B, L, Hq, d]          row-major, contiguous, 16-byte aligned
+ *   o   [B, L, Hq, d]          row-major, contiguous, 16-byte aligned, dtype of q
+ *   lse [B, L, Hq]             fp32, natural log of the softmax denominator
+ *                              (including the max), or NULL
+ *   k, v                       element (blk, tok, hk, c) lives at
+ *                              blk*kv_stride_blk + tok*kv_stride_tok +
+ *                              hk*kv_stride_head + c   (element strides; c unit
+ *                              stride; strides multiples of 16 bytes)
+ *     contiguous (page_size == 0): blk = sequence b, tok = token j;
+ *                              each sequence holds >= max_kv_len tokens.
+ *     paged (page_size > 0, a power of two): blk = page_table[b*max_pages_per_seq
+ *                              + j/page_size], tok = j % page_size; the pool
+ *                              holds num_pages pages.
+ *   kv_lens [B] int32          S_b, the number of cached tokens of sequence b,
+ *                              INCLUDING the L speculated tokens, whose K/V are
+ *                              already written at positions S_b-L .. S_b-1.
+ *
+ * Query row i of sequence b sits at position p = S_b - L + i and sees
+ *   verify: keys j with 0 <= j <= p                   (Sec. 3.1, T_V)
+ *   draft : keys j <= p with j < n_sink or j >= p - window + 1
+ *           (sink tokens plus the query's own last `window` positions:
+ *            a StreamingLLM-style cache of budget n_sink + window, Sec. 5.1)
+ * Query head h reads kv head h / G.  Scores are scaled by sm_scale
+ * (sm_scale <= 0 selects 1/sqrt(d)); softmax and accumulation are fp32.
+ */
+typedef struct {
+  int32_t num_seqs;     /* B >= 0 (0 is a no-op) */
+  int32_t q_len;        /* L in [1, 16] */
+  int32_t num_q_heads;  /* Hq >= 1, a multiple of num_kv_heads */
+  int32_t num_kv_heads; /* Hkv >= 1; G * L <= 64 */
+  int32_t head_dim;     /* d in {64, 128} */
+  int32_t dtype;        /* md_dtype of q, k, v, o */
+  float sm_scale;       /* <= 0: 1/sqrt(d) */
+  const void* q;
+  const void* k;
+  const void* v;
+  int64_t kv_stride_blk;
+  int64_t kv_stride_tok;
+  int64_t kv_stride_head;
+  int32_t page_size;          /* 0 = contiguous, else tokens per page (power of two) */
+  int32_t max_pages_per_seq;  /* columns of page_table (paged only) */
+  int64_t num_pages;          /* pages in the pool (paged only) */
+  const int32_t* page_table;  /* [B, max_pages_per_seq] or NULL when contiguous */
+  const int32_t* kv_lens;     /* [B] */
+  int32_t max_kv_len;         /* HOST bound on every kv_lens[b]; sizes the grid */
+  void* o;
+  float* lse;
+  void* workspace;            /* device scratch, >= md_workspace_bytes(), 256-byte aligned */
+  size_t workspace_bytes;
+} md_attn_args;
+
+/*
+ * Verification attention: all L = gamma+1 speculated tokens of every sequence
+ * against the full KV cache, causal among themselves (Sec. 3.1-3.2).
+ * Errors: MD_ERR_INVALID_ARG for a NULL args/q/k/v/o/kv_lens, a NULL or
+ * superfluous page_table, bad sizes, a non power-of-two page size, a table too
+ * narrow for max_kv_len, max_kv_len < q_len, misaligned pointers or strides;
+ * MD_ERR_UNSUPPORTED for head_dim not in {64,128} or G*L > 64;
+ * MD_ERR_WORKSPACE; MD_ERR_HIP.
+ */
+int md_verify_attn(const md_attn_args* a, void* stream);
+
+/*
+ * Draft attention with a StreamingLLM-style sparse cache read in place: the
+ * same queries see only the first n_sink tokens and their last `window`
+ * positions (budget K = n_sink + window; Sec. 4.1 Eq. 3, Sec. 5.1).
+ * n_sink >= 0 and window >= 1, else MD_ERR_INVALID_ARG; other errors as
+ * md_verify_attn.
+ */
+int md_draft_attn(const md_attn_args* a, int32_t n_sink, int32_t window, void* stream);
+
+/*
+ * Log-sum-exp merge of attention computed over disjoint key sets (the
+ * split-KV identity of Flash-Decoding, Sec. 2).  Per row r:
+ *   lse[r] = ln sum_k exp(lse_parts[k][r]),
+ *   o[r]   = sum_k exp(lse_parts[k][r] - lse[r]) * o_parts[k][r]
+ * Parts whose lse is -inf are skipped (their o is never read); a row with
+ * every part empty gets o = 0, lse = -inf.
+ *   o_parts   [n_parts][n_rows][head_dim] fp32 (each part already normalised)
+ *   lse_parts [n_parts][n_rows] fp32
+ *   o         [n_rows][head_dim] in out_dtype (md_dtype)
+ *   lse       [n_rows] fp32 or NULL
+ * All device pointers, 16-byte aligned.  Errors: MD_ERR_INVALID_ARG for
+ * n_parts < 1, n_rows < 0, NULL or misaligned pointers, a bad dtype;
+ * MD_ERR_UNSUPPORTED for head_dim not in {64,128}; MD_ERR_HIP.
+ */
+int md_merge_lse(int32_t n_parts, int64_t n_rows, int32_t head_dim, int32_t out_dtype,
+                 const float* o_parts, const float* lse_parts, void* o, float* lse,
+                 void* stream);
+
+/*
+ * Workspace bytes an attention call with these arguments needs (0 when the
+ * call runs as a single pass).  mode is md_mode; n_sink and window are used
+ * for MD_MODE_DRAFT only.  Pure host arithmetic on the sizes plus the
+ * current device's compute-unit count (256 if no device is visible);
+ * pointers in `a` are not read.  Returns 0 for malformed arguments too:
+ * the attention call itself reports those.
+ */
+size_t md_workspace_bytes(const md_attn_args* a, int32_t mode, int32_t n_sink, int32_t window);
+
+/* Static description of a status code; never NULL. */
+const char* md_status_str(int status);
+
+/* Text of the last MD_ERR_HIP on the calling thread ("" if none). */
+const char* md_last_hip_error(void);
+
+/* sizeof(md_attn_args) as compiled into the library, so bindings can check
+ * their copy of the struct layout. */
+size_t md_attn_args_size(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MAGICDEC_H_ */

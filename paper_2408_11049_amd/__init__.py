@@ -1,1 +1,235 @@
-"""placeholder"""
+"""MI355X (gfx950) verify/draft decode attention for MagicDec-style speculative decoding.
+
+A thin ctypes binding over ``libmagicdec.so`` (C ABI in ``include/magicdec.h``):
+argument marshalling only.  Every step of the attention runs in the library's
+HIP kernels; PyTorch only supplies device memory and the stream.  There is no
+CPU fallback: if the library is missing, every call raises.
+
+    md_verify_attn(q, k, v, kv_lens, ...)          -> (o, lse)
+    md_draft_attn(q, k, v, kv_lens, n_sink, window, ...) -> (o, lse)
+    md_merge_lse(o_parts, lse_parts, ...)         -> (o, lse)
+    md_workspace_bytes(...)                       -> int
+
+Shapes: q/o [B, L, Hq, d] (L = gamma + 1); k/v contiguous [B, S_alloc, Hkv, d]
+or, with ``page_table`` [B, max_pages] int32, paged [P, page_size, Hkv, d];
+kv_lens [B] int32 counting the L speculated tokens; lse [B, L, Hq] fp32.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmagicdec.so")
+
+MD_OK, MD_ERR_INVALID_ARG, MD_ERR_UNSUPPORTED, MD_ERR_WORKSPACE, MD_ERR_HIP = range(5)
+MD_F32, MD_BF16 = 0, 1
+MD_MODE_VERIFY, MD_MODE_DRAFT = 0, 1
+
+EXPORTED = ["md_verify_attn", "md_draft_attn", "md_merge_lse", "md_workspace_bytes",
+            "md_status_str", "md_last_hip_error", "md_attn_args_size",
+            "md_bench_stream_read", "md_bench_copy", "md_bench_fill"]
+
+
+class MdAttnArgs(ctypes.Structure):
+    """Mirror of ``md_attn_args`` (checked against md_attn_args_size())."""
+    _fields_ = [
+        ("num_seqs", ctypes.c_int32), ("q_len", ctypes.c_int32),
+        ("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32), ("sm_scale", ctypes.c_float),
+        ("q", ctypes.c_void_p), ("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
+        ("kv_stride_blk", ctypes.c_int64), ("kv_stride_tok", ctypes.c_int64),
+        ("kv_stride_head", ctypes.c_int64),
+        ("page_size", ctypes.c_int32), ("max_pages_per_seq", ctypes.c_int32),
+        ("num_pages", ctypes.c_int64), ("page_table", ctypes.c_void_p),
+        ("kv_lens", ctypes.c_void_p), ("max_kv_len", ctypes.c_int32),
+        ("o", ctypes.c_void_p), ("lse", ctypes.c_void_p),
+        ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
+    ]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libmagicdec.so.  torch is imported first so the library binds to the
+    HIP runtime torch already loaded (same soname), not a second copy."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    import torch  # noqa: F401  (shares its HIP runtime with the library)
+    if not os.path.exists(path):
+        raise RuntimeError(
+            f"{path} is missing: build it with __graft_entry__.build() "
+            "(python -m paper_2408_11049_amd.build); there is no fallback path")
+    lib = ctypes.CDLL(path)
+    vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    args_p = ctypes.POINTER(MdAttnArgs)
+    lib.md_verify_attn.argtypes = [args_p, vp]
+    lib.md_verify_attn.restype = ctypes.c_int
+    lib.md_draft_attn.argtypes = [args_p, i32, i32, vp]
+    lib.md_draft_attn.restype = ctypes.c_int
+    lib.md_merge_lse.argtypes = [i32, i64, i32, i32, vp, vp, vp, vp, vp]
+    lib.md_merge_lse.restype = ctypes.c_int
+    lib.md_workspace_bytes.argtypes = [args_p, i32, i32, i32]
+    lib.md_workspace_bytes.restype = sz
+    lib.md_status_str.argtypes = [ctypes.c_int]
+    lib.md_status_str.restype = ctypes.c_char_p
+    lib.md_last_hip_error.argtypes = []
+    lib.md_last_hip_error.restype = ctypes.c_char_p
+    lib.md_attn_args_size.argtypes = []
+    lib.md_attn_args_size.restype = sz
+    lib.md_bench_stream_read.argtypes = [vp, sz, vp, vp]
+    lib.md_bench_stream_read.restype = ctypes.c_int
+    lib.md_bench_copy.argtypes = [vp, vp, sz, vp]
+    lib.md_bench_copy.restype = ctypes.c_int
+    lib.md_bench_fill.argtypes = [vp, sz, ctypes.c_uint32, vp]
+    lib.md_bench_fill.restype = ctypes.c_int
+    if lib.md_attn_args_size() != ctypes.sizeof(MdAttnArgs):
+        raise RuntimeError("md_attn_args layout mismatch between the binding and the library")
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status == MD_OK:
+        return
+    lib = load_library()
+    msg = lib.md_status_str(status).decode()
+    if status == MD_ERR_HIP:
+        raise RuntimeError(f"magicdec: {msg}: {lib.md_last_hip_error().decode()}")
+    raise ValueError(f"magicdec: {msg} (status {status})")
+
+
+def _stream_handle(t, stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream(t.device)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dtype_code(t):
+    import torch
+    if t.dtype == torch.float32:
+        return MD_F32
+    if t.dtype == torch.bfloat16:
+        return MD_BF16
+    raise ValueError(f"unsupported dtype {t.dtype}; q/k/v must be float32 or bfloat16")
+
+
+def make_args(q, k, v, kv_lens, *, max_kv_len: Optional[int] = None, page_table=None,
+              sm_scale: float = 0.0, out=None, lse=None, workspace=None) -> MdAttnArgs:
+    """Fill md_attn_args from tensors (no data is read or moved)."""
+    if q.dim() != 4 or k.dim() != 4 or v.dim() != 4:
+        raise ValueError("q, k, v must be 4-D")
+    B, L, Hq, d = q.shape
+    paged = page_table is not None
+    if k.shape != v.shape or k.stride() != v.stride():
+        raise ValueError("k and v must share shape and strides")
+    if k.stride(3) != 1:
+        raise ValueError("the head_dim axis of k/v must be unit-stride")
+    if not q.is_contiguous() or (out is not None and not out.is_contiguous()):
+        raise ValueError("q and o must be contiguous [B, L, Hq, d]")
+    if max_kv_len is None:  # a bound that needs no device sync
+        max_kv_len = page_table.shape[1] * k.shape[1] if paged else k.shape[1]
+    if B > 0 and not paged and k.shape[1] < max_kv_len:
+        raise ValueError("contiguous k/v must hold max_kv_len tokens per sequence")
+    if B > 0 and not paged and k.shape[0] < B:
+        raise ValueError("contiguous k/v must hold B sequences")
+    a = MdAttnArgs()
+    a.num_seqs, a.q_len, a.num_q_heads, a.num_kv_heads, a.head_dim = B, L, Hq, k.shape[2], d
+    a.dtype = _dtype_code(q)
+    if _dtype_code(k) != a.dtype or _dtype_code(v) != a.dtype:
+        raise ValueError("q, k, v must share a dtype")
+    a.sm_scale = float(sm_scale)
+    a.q, a.k, a.v = q.data_ptr(), k.data_ptr(), v.data_ptr()
+    a.kv_stride_blk, a.kv_stride_tok, a.kv_stride_head = k.stride(0), k.stride(1), k.stride(2)
+    if paged:
+        import torch
+        if page_table.dtype != torch.int32 or not page_table.is_contiguous():
+            raise ValueError("page_table must be contiguous int32 [B, max_pages]")
+        a.page_size, a.max_pages_per_seq = k.shape[1], page_table.shape[1]
+        a.num_pages = k.shape[0]
+        a.page_table = page_table.data_ptr()
+    a.kv_lens = kv_lens.data_ptr()
+    a.max_kv_len = int(max_kv_len)
+    a.o = out.data_ptr() if out is not None else None
+    a.lse = lse.data_ptr() if lse is not None else None
+    if workspace is not None:
+        a.workspace, a.workspace_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
+    return a
+
+
+def md_workspace_bytes(q, k, v, kv_lens, *, mode=MD_MODE_VERIFY, n_sink=0, window=1, **kw) -> int:
+    lib = load_library()
+    a = make_args(q, k, v, kv_lens, **kw)
+    return int(lib.md_workspace_bytes(ctypes.byref(a), mode, n_sink, window))
+
+
+def _attention(mode, q, k, v, kv_lens, n_sink, window, *, max_kv_len=None, page_table=None,
+               sm_scale=0.0, out=None, lse=None, return_lse=True, workspace=None, stream=None):
+    import torch
+    lib = load_library()
+    if kv_lens.dtype != torch.int32:
+        raise ValueError("kv_lens must be int32")
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None and return_lse:
+        lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
+    a = make_args(q, k, v, kv_lens, max_kv_len=max_kv_len, page_table=page_table,
+                  sm_scale=sm_scale, out=out, lse=lse)
+    need = int(lib.md_workspace_bytes(ctypes.byref(a), mode, n_sink, window))
+    if need and workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    if workspace is not None:
+        a.workspace = workspace.data_ptr()
+        a.workspace_bytes = workspace.numel() * workspace.element_size()
+    s = _stream_handle(q, stream)
+    if mode == MD_MODE_VERIFY:
+        st = lib.md_verify_attn(ctypes.byref(a), s)
+    else:
+        st = lib.md_draft_attn(ctypes.byref(a), int(n_sink), int(window), s)
+    _check(st)
+    return out, lse
+
+
+def md_verify_attn(q, k, v, kv_lens, **kw):
+    """Verification attention over the full cache (see include/magicdec.h)."""
+    return _attention(MD_MODE_VERIFY, q, k, v, kv_lens, 0, 1, **kw)
+
+
+def md_draft_attn(q, k, v, kv_lens, n_sink, window, **kw):
+    """StreamingLLM-style sparse draft attention (see include/magicdec.h)."""
+    return _attention(MD_MODE_DRAFT, q, k, v, kv_lens, n_sink, window, **kw)
+
+
+def md_merge_lse(o_parts, lse_parts, *, out_dtype=None, out=None, lse=None, stream=None):
+    """o_parts [n_parts, n_rows, d] fp32, lse_parts [n_parts, n_rows] fp32 -> (o, lse)."""
+    import torch
+    lib = load_library()
+    n_parts, n_rows, d = o_parts.shape
+    if o_parts.dtype != torch.float32 or lse_parts.dtype != torch.float32:
+        raise ValueError("o_parts and lse_parts must be float32")
+    if not o_parts.is_contiguous() or not lse_parts.is_contiguous():
+        raise ValueError("o_parts and lse_parts must be contiguous")
+    if out is None:
+        out = torch.empty((n_rows, d), dtype=out_dtype or torch.float32, device=o_parts.device)
+    if lse is None:
+        lse = torch.empty((n_rows,), dtype=torch.float32, device=o_parts.device)
+    code = _dtype_code(out)
+    st = lib.md_merge_lse(n_parts, n_rows, d, code, _ptr(o_parts), _ptr(lse_parts), _ptr(out),
+                          _ptr(lse), _stream_handle(o_parts, stream))
+    _check(st)
+    return out, lse
+
+
+# Short aliases.
+verify_attn = md_verify_attn
+draft_attn = md_draft_attn
+merge_lse = md_merge_lse
+workspace_bytes = md_workspace_bytes

@@ -1,0 +1,176 @@
+// api.cpp -- the C ABI of libmagicdec.so: argument checks, the split-KV plan,
+// and the launches on the caller's stream.  No allocation, no host sync.
+#include <hip/hip_runtime.h>
+#include <math.h>
+
+#include <atomic>
+#include <string>
+
+#include "internal.h"
+#include "kernels.h"
+#include "magicdec.h"
+#include "magicdec_bench.h"
+
+namespace md {
+
+namespace {
+
+thread_local std::string g_last_hip_error;
+
+int hip_fail(hipError_t e) {
+  g_last_hip_error = hipGetErrorString(e);
+  return MD_ERR_HIP;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void* stream) {
+  int st = validate_attn(a, mode, n_sink, window);
+  if (st != MD_OK) return st;
+  if (a->num_seqs == 0) return MD_OK;
+  const Plan pl = make_plan(a, mode, n_sink, window, device_cu_count());
+  const bool bf16 = a->dtype == MD_BF16;
+  const bool paged = a->page_size != 0;
+
+  AttnParams p{};
+  p.q = a->q;
+  p.k = a->k;
+  p.v = a->v;
+  p.s_blk = a->kv_stride_blk;
+  p.s_tok = a->kv_stride_tok;
+  p.s_head = a->kv_stride_head;
+  p.page_table = a->page_table;
+  p.page_shift = 0;
+  if (paged)
+    while ((1 << p.page_shift) < a->page_size) ++p.page_shift;
+  p.max_pages = a->max_pages_per_seq;
+  p.num_pages = a->num_pages;
+  p.kv_lens = a->kv_lens;
+  p.max_kv_len = a->max_kv_len;
+  p.L = a->q_len;
+  p.Hq = a->num_q_heads;
+  p.Hkv = a->num_kv_heads;
+  p.G = pl.G;
+  p.R = pl.R;
+  const float scale = a->sm_scale > 0.f ? a->sm_scale : 1.0f / sqrtf(static_cast<float>(a->head_dim));
+  p.scale_log2 = scale * 1.44269504088896340736f;
+  p.mode = mode;
+  p.n_sink = mode == MD_MODE_DRAFT ? n_sink : 0;
+  p.window = mode == MD_MODE_DRAFT ? window : 1;
+  p.n_chunks = pl.n_chunks;
+  p.chunk_len = pl.chunk_len;
+  p.o = a->o;
+  p.lse = a->lse;
+  p.n_rows = pl.n_rows;
+  if (pl.n_chunks > 1) {
+    p.part_o = static_cast<float*>(a->workspace);
+    p.part_lse = reinterpret_cast<float*>(static_cast<unsigned char*>(a->workspace) + pl.part_o_bytes);
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = launch_attn_partial(p, a->head_dim, bf16, pl.NT, paged,
+                                     pl.n_units * pl.n_chunks, s);
+  if (e != hipSuccess) return hip_fail(e);
+  if (pl.n_chunks > 1) {
+    e = launch_merge_lse(pl.n_chunks, pl.n_rows, a->head_dim, bf16, p.part_o, p.part_lse, a->o,
+                         a->lse, s);
+    if (e != hipSuccess) return hip_fail(e);
+  }
+  return MD_OK;
+}
+
+}  // namespace
+
+int device_cu_count() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+    (void)hipGetLastError();
+    return 256;
+  }
+  int c = cache[dev].load(std::memory_order_relaxed);
+  if (c > 0) return c;
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      n <= 0) {
+    (void)hipGetLastError();
+    return 256;
+  }
+  cache[dev].store(n, std::memory_order_relaxed);
+  return n;
+}
+
+}  // namespace md
+
+extern "C" {
+
+int md_verify_attn(const md_attn_args* a, void* stream) {
+  return md::run_attention(a, MD_MODE_VERIFY, 0, 1, stream);
+}
+
+int md_draft_attn(const md_attn_args* a, int32_t n_sink, int32_t window, void* stream) {
+  return md::run_attention(a, MD_MODE_DRAFT, n_sink, window, stream);
+}
+
+int md_merge_lse(int32_t n_parts, int64_t n_rows, int32_t head_dim, int32_t out_dtype,
+                 const float* o_parts, const float* lse_parts, void* o, float* lse,
+                 void* stream) {
+  if (n_parts < 1 || n_rows < 0) return MD_ERR_INVALID_ARG;
+  if (out_dtype != MD_F32 && out_dtype != MD_BF16) return MD_ERR_INVALID_ARG;
+  if (head_dim != 64 && head_dim != 128) return MD_ERR_UNSUPPORTED;
+  if (n_rows == 0) return MD_OK;
+  if (!o_parts || !lse_parts || !o) return MD_ERR_INVALID_ARG;
+  if (!md::aligned16(o_parts) || !md::aligned16(lse_parts) || !md::aligned16(o) || (lse && !md::aligned16(lse)))
+    return MD_ERR_INVALID_ARG;
+  hipError_t e = md::launch_merge_lse(n_parts, n_rows, head_dim, out_dtype == MD_BF16, o_parts,
+                                      lse_parts, o, lse, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? MD_OK : md::hip_fail(e);
+}
+
+size_t md_workspace_bytes(const md_attn_args* a, int32_t mode, int32_t n_sink, int32_t window) {
+  if (!a) return 0;
+  if (mode != MD_MODE_VERIFY && mode != MD_MODE_DRAFT) return 0;
+  if (mode == MD_MODE_DRAFT && (n_sink < 0 || window < 1)) return 0;
+  if (a->num_seqs < 0 || a->q_len < 1 || a->num_q_heads < 1 || a->num_kv_heads < 1 ||
+      a->num_q_heads % a->num_kv_heads || a->max_kv_len < a->q_len ||
+      (a->head_dim != 64 && a->head_dim != 128))
+    return 0;
+  return md::make_plan(a, mode, n_sink, window, md::device_cu_count()).workspace_bytes;
+}
+
+const char* md_status_str(int status) {
+  switch (status) {
+    case MD_OK: return "ok";
+    case MD_ERR_INVALID_ARG: return "invalid argument";
+    case MD_ERR_UNSUPPORTED: return "unsupported shape or dtype";
+    case MD_ERR_WORKSPACE: return "workspace missing, too small or misaligned";
+    case MD_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char* md_last_hip_error(void) { return md::g_last_hip_error.c_str(); }
+
+size_t md_attn_args_size(void) { return sizeof(md_attn_args); }
+
+int md_bench_stream_read(const void* buf, size_t bytes, float* sink, void* stream) {
+  if (!buf || !sink || !md::aligned16(buf) || bytes % 16) return MD_ERR_INVALID_ARG;
+  hipError_t e = md::launch_bench_read(buf, bytes, sink, md::device_cu_count() * 8,
+                                       static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? MD_OK : md::hip_fail(e);
+}
+
+int md_bench_copy(void* dst, const void* src, size_t bytes, void* stream) {
+  if (!dst || !src || !md::aligned16(dst) || !md::aligned16(src) || bytes % 16) return MD_ERR_INVALID_ARG;
+  hipError_t e = md::launch_bench_copy(dst, src, bytes, md::device_cu_count() * 8,
+                                       static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? MD_OK : md::hip_fail(e);
+}
+
+int md_bench_fill(void* buf, size_t bytes, uint32_t value, void* stream) {
+  if (!buf || !md::aligned16(buf) || bytes % 16) return MD_ERR_INVALID_ARG;
+  hipError_t e = md::launch_bench_fill(buf, bytes, value, md::device_cu_count() * 8,
+                                       static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? MD_OK : md::hip_fail(e);
+}
+
+}  // extern "C"

@@ -1,0 +1,55 @@
+// internal.h -- host-side types shared by the entry points, the planner and
+// the kernel launchers of libmagicdec.so.  No HIP types appear here, so the
+// validation and planning code compiles and runs without a GPU.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "magicdec.h"
+
+namespace md {
+
+// Work decomposition of one attention call.
+//
+// A "unit" is one (sequence b, kv head hk) pair: the G*L query rows that share
+// that kv head are packed into 16-row MFMA tiles and stream the unit's K/V
+// once.  The unit's visible key range (the whole causal prefix for verify;
+// sinks followed by the window for draft, read as one virtual range) is cut
+// into n_chunks chunks of chunk_len tokens; each chunk is one workgroup of
+// kWaves waves, which interleave kTile-token tiles.  With n_chunks > 1 the
+// chunks write normalised partial results and a merge pass combines them
+// by log-sum-exp (the split-KV decomposition named in the paper's Sec. 2).
+constexpr int kWaves = 4;
+constexpr int kTile = 32;            // tokens per wave iteration
+constexpr int kMinChunkTokens = 1024;  // every wave gets >= 8 tiles of a chunk
+constexpr int kMaxRows = 64;         // G*L bound: at most four 16-row tiles
+
+struct Plan {
+  int32_t G = 0;         // Hq / Hkv
+  int32_t R = 0;         // G * L query rows per unit
+  int32_t NT = 0;        // 16-row tiles per unit
+  int32_t U_max = 0;     // bound on any unit's visible range, in tokens
+  int32_t n_chunks = 0;
+  int32_t chunk_len = 0;
+  int64_t n_rows = 0;    // B * L * Hq
+  int64_t n_units = 0;   // B * Hkv
+  size_t part_o_bytes = 0;   // workspace: [n_chunks][n_rows][d] fp32 partial O
+  size_t part_lse_bytes = 0; // workspace: [n_chunks][n_rows] fp32 partial lse
+  size_t workspace_bytes = 0;
+};
+
+// Checks every argument the host can see.  Returns MD_OK or an md_status.
+int validate_attn(const md_attn_args* a, int mode, int n_sink, int window);
+
+// The decomposition for these sizes on a device with num_cus compute units.
+// Only sizes are read from `a`.  Call after validate_attn succeeded.
+Plan make_plan(const md_attn_args* a, int mode, int n_sink, int window, int num_cus);
+
+// Compute units of the current device (cached per device); 256 when no
+// device is visible, so sizes stay defined on a host without a GPU.
+int device_cu_count();
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+}  // namespace md

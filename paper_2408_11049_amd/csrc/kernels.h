@@ -1,0 +1,48 @@
+// kernels.h -- device-side parameter blocks and the launchers of the HIP
+// kernels behind the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace md {
+
+// Everything one attention launch needs, passed by value as the kernel
+// argument.  Strides are in elements; pointers are device pointers.
+struct AttnParams {
+  const void* q;
+  const void* k;
+  const void* v;
+  int64_t s_blk, s_tok, s_head;
+  const int32_t* page_table;  // [B, max_pages] (paged instances only)
+  int32_t page_shift;         // log2(page_size)
+  int32_t max_pages;
+  int64_t num_pages;
+  const int32_t* kv_lens;
+  int32_t max_kv_len;
+  int32_t L, Hq, Hkv, G, R;
+  float scale_log2;           // softmax scale * log2(e)
+  int32_t mode, n_sink, window;
+  int32_t n_chunks, chunk_len;
+  void* o;                    // final O (single chunk)
+  float* lse;                 // final lse or nullptr (single chunk)
+  float* part_o;              // [n_chunks][n_rows][d] (several chunks)
+  float* part_lse;            // [n_chunks][n_rows]
+  int64_t n_rows;
+};
+
+hipError_t launch_attn_partial(const AttnParams& p, int head_dim, bool bf16, int NT, bool paged,
+                               int64_t n_blocks, hipStream_t s);
+
+hipError_t launch_merge_lse(int n_parts, int64_t n_rows, int head_dim, bool out_bf16,
+                            const float* o_parts, const float* lse_parts, void* o, float* lse,
+                            hipStream_t s);
+
+hipError_t launch_bench_read(const void* buf, size_t bytes, float* sink, int n_blocks,
+                             hipStream_t s);
+hipError_t launch_bench_copy(void* dst, const void* src, size_t bytes, int n_blocks,
+                             hipStream_t s);
+hipError_t launch_bench_fill(void* buf, size_t bytes, uint32_t value, int n_blocks,
+                             hipStream_t s);
+
+}  // namespace md

@@ -1,0 +1,115 @@
+// plan.cpp -- argument validation and the split-KV work decomposition.
+// Pure host arithmetic: no HIP call is made here, so every error path can be
+// exercised on a machine without a GPU.
+#include <limits.h>
+
+#include "internal.h"
+
+namespace md {
+
+namespace {
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Largest visible range of any unit, in tokens.  Verify: the whole cache.
+// Draft: sinks plus the union of the L queries' windows, which is
+// [S - L - W + 1, S) -- or the whole prefix when that reaches the sinks.
+int64_t visible_bound(int64_t max_kv_len, int L, int mode, int64_t n_sink, int64_t window) {
+  if (mode == MD_MODE_VERIFY) return max_kv_len;
+  int64_t lo = max_kv_len - L - window + 1;
+  if (lo <= n_sink) return max_kv_len;
+  return n_sink + (max_kv_len - lo);
+}
+
+}  // namespace
+
+int validate_attn(const md_attn_args* a, int mode, int n_sink, int window) {
+  if (!a) return MD_ERR_INVALID_ARG;
+  if (mode != MD_MODE_VERIFY && mode != MD_MODE_DRAFT) return MD_ERR_INVALID_ARG;
+  if (mode == MD_MODE_DRAFT && (n_sink < 0 || window < 1)) return MD_ERR_INVALID_ARG;
+  if (a->num_seqs < 0) return MD_ERR_INVALID_ARG;
+  if (a->q_len < 1 || a->q_len > 16) return MD_ERR_INVALID_ARG;
+  if (a->num_q_heads < 1 || a->num_kv_heads < 1) return MD_ERR_INVALID_ARG;
+  if (a->num_q_heads % a->num_kv_heads != 0) return MD_ERR_INVALID_ARG;
+  if (a->dtype != MD_F32 && a->dtype != MD_BF16) return MD_ERR_INVALID_ARG;
+  if (a->head_dim < 1) return MD_ERR_INVALID_ARG;
+  if (a->max_kv_len < a->q_len) return MD_ERR_INVALID_ARG;
+  const bool paged = a->page_size != 0;
+  if (a->page_size < 0) return MD_ERR_INVALID_ARG;
+  if (paged) {
+    if (!is_pow2(a->page_size) || a->max_pages_per_seq < 1 || a->num_pages < 1)
+      return MD_ERR_INVALID_ARG;
+    if (ceil_div(a->max_kv_len, a->page_size) > a->max_pages_per_seq) return MD_ERR_INVALID_ARG;
+    if (a->num_pages > INT32_MAX) return MD_ERR_INVALID_ARG;  // page ids are int32
+  }
+  if (a->kv_stride_blk < 0 || a->kv_stride_tok < 0 || a->kv_stride_head < 0)
+    return MD_ERR_INVALID_ARG;
+  if (a->head_dim != 64 && a->head_dim != 128) return MD_ERR_UNSUPPORTED;
+  const int64_t G = a->num_q_heads / a->num_kv_heads;
+  if (G * a->q_len > kMaxRows) return MD_ERR_UNSUPPORTED;
+  if (a->num_seqs == 0) return MD_OK;  // nothing will be read or written
+
+  if (!a->q || !a->k || !a->v || !a->o || !a->kv_lens) return MD_ERR_INVALID_ARG;
+  if (paged != (a->page_table != nullptr)) return MD_ERR_INVALID_ARG;
+  if (!aligned16(a->q) || !aligned16(a->k) || !aligned16(a->v) || !aligned16(a->o))
+    return MD_ERR_INVALID_ARG;
+  if ((reinterpret_cast<uintptr_t>(a->kv_lens) & 3u) ||
+      (a->lse && (reinterpret_cast<uintptr_t>(a->lse) & 3u)) ||
+      (paged && (reinterpret_cast<uintptr_t>(a->page_table) & 3u)))
+    return MD_ERR_INVALID_ARG;
+  // Every token row must start on a 16-byte boundary for the 128-bit loads.
+  const int64_t per16 = a->dtype == MD_BF16 ? 8 : 4;
+  if (a->kv_stride_blk % per16 || a->kv_stride_tok % per16 || a->kv_stride_head % per16)
+    return MD_ERR_INVALID_ARG;
+  // A token row must not overlap the next head's row.
+  if (a->num_kv_heads > 1 && a->kv_stride_head < a->head_dim) return MD_ERR_INVALID_ARG;
+
+  const int num_cus = device_cu_count();
+  Plan p = make_plan(a, mode, n_sink, window, num_cus);
+  if (p.workspace_bytes) {
+    if (!a->workspace || a->workspace_bytes < p.workspace_bytes) return MD_ERR_WORKSPACE;
+    if (reinterpret_cast<uintptr_t>(a->workspace) & 255u) return MD_ERR_WORKSPACE;
+  }
+  return MD_OK;
+}
+
+Plan make_plan(const md_attn_args* a, int mode, int n_sink, int window, int num_cus) {
+  Plan p;
+  const int L = a->q_len;
+  p.G = a->num_q_heads / a->num_kv_heads;
+  p.R = p.G * L;
+  p.NT = (p.R + 15) / 16;
+  const int64_t U = visible_bound(a->max_kv_len, L, mode, n_sink, window);
+  p.U_max = static_cast<int32_t>(U);
+  p.n_rows = static_cast<int64_t>(a->num_seqs) * L * a->num_q_heads;
+  p.n_units = static_cast<int64_t>(a->num_seqs) * a->num_kv_heads;
+
+  // Resident workgroups: two of kWaves waves per compute unit.  When the units
+  // alone cover every slot, one chunk per unit avoids the merge pass; else
+  // split each unit's range until about two workgroups wait per slot, but
+  // never below kMinChunkTokens tokens per chunk.
+  const int64_t slots = static_cast<int64_t>(num_cus > 0 ? num_cus : 256) * 2;
+  int64_t n_chunks = 1;
+  if (p.n_units > 0 && p.n_units < slots) {
+    n_chunks = ceil_div(2 * slots, p.n_units);
+    int64_t cap = ceil_div(U, kMinChunkTokens);
+    if (n_chunks > cap) n_chunks = cap;
+    if (n_chunks < 1) n_chunks = 1;
+  }
+  int64_t chunk_len = ceil_div(ceil_div(U, n_chunks), kTile) * kTile;
+  if (chunk_len < kTile) chunk_len = kTile;
+  n_chunks = ceil_div(U, chunk_len);
+  if (n_chunks < 1) n_chunks = 1;
+  p.n_chunks = static_cast<int32_t>(n_chunks);
+  p.chunk_len = static_cast<int32_t>(chunk_len);
+  if (p.n_chunks > 1) {
+    p.part_o_bytes = align_up(static_cast<size_t>(n_chunks) * p.n_rows * a->head_dim * 4, 256);
+    p.part_lse_bytes = align_up(static_cast<size_t>(n_chunks) * p.n_rows * 4, 256);
+    p.workspace_bytes = p.part_o_bytes + p.part_lse_bytes;
+  }
+  return p;
+}
+
+}  // namespace md

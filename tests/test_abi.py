@@ -1,0 +1,195 @@
+"""C ABI checks that need no GPU: the library loads, exports every symbol the
+headers declare, agrees with the binding on the struct layout, and rejects
+every malformed argument on the host before any launch.  No compute call is
+made here (only calls that return an error before reaching a kernel)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2408_11049_amd as md
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("magicdec.h", "magicdec_bench.h")]
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(md.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    return md.load_library()
+
+
+def declared_functions():
+    names = []
+    for h in HEADERS:
+        text = open(h).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names += re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*(md_[a-z_0-9]+)\s*\(", text, re.M)
+    return sorted(set(names))
+
+
+def test_headers_declare_the_entry_points():
+    names = declared_functions()
+    for n in ["md_verify_attn", "md_draft_attn", "md_merge_lse", "md_workspace_bytes",
+              "md_status_str"]:
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", md.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (md_[a-z_0-9]+)$", out, re.M))
+    declared = set(declared_functions())
+    assert declared <= exported, f"declared but not exported: {sorted(declared - exported)}"
+    assert set(md.EXPORTED) <= exported
+    for n in declared:
+        assert hasattr(lib, n)
+
+
+def test_no_oracle_in_the_product_library():
+    out = subprocess.run(["nm", "-D", md.LIB_PATH], capture_output=True, text=True).stdout
+    assert "oracle" not in out
+    deps = subprocess.run(["readelf", "-d", md.LIB_PATH], capture_output=True, text=True).stdout
+    assert "liboracle" not in deps
+
+
+def test_struct_layout_matches(lib):
+    assert lib.md_attn_args_size() == ctypes.sizeof(md.MdAttnArgs)
+
+
+def test_status_strings(lib):
+    for s in range(5):
+        assert lib.md_status_str(s)
+    assert lib.md_status_str(99) == b"unknown status"
+
+
+FAKE = 0x10000  # aligned, never dereferenced: validation rejects before any launch
+
+
+def good_args(**over):
+    a = md.MdAttnArgs()
+    a.num_seqs, a.q_len, a.num_q_heads, a.num_kv_heads, a.head_dim = 4, 4, 8, 2, 128
+    a.dtype = md.MD_BF16
+    a.q = a.k = a.v = a.o = a.kv_lens = FAKE
+    a.kv_stride_head = 128
+    a.kv_stride_tok = 2 * 128
+    a.kv_stride_blk = 64 * 2 * 128
+    a.max_kv_len = 64
+    for k, v in over.items():
+        setattr(a, k, v)
+    return a
+
+
+BAD = [
+    ("q_len 0", dict(q_len=0), md.MD_ERR_INVALID_ARG),
+    ("q_len 17", dict(q_len=17), md.MD_ERR_INVALID_ARG),
+    ("negative batch", dict(num_seqs=-1), md.MD_ERR_INVALID_ARG),
+    ("Hq not multiple of Hkv", dict(num_q_heads=7), md.MD_ERR_INVALID_ARG),
+    ("zero kv heads", dict(num_kv_heads=0), md.MD_ERR_INVALID_ARG),
+    ("bad dtype", dict(dtype=7), md.MD_ERR_INVALID_ARG),
+    ("max_kv_len < q_len", dict(max_kv_len=3), md.MD_ERR_INVALID_ARG),
+    ("null q", dict(q=None), md.MD_ERR_INVALID_ARG),
+    ("null k", dict(k=None), md.MD_ERR_INVALID_ARG),
+    ("null v", dict(v=None), md.MD_ERR_INVALID_ARG),
+    ("null o", dict(o=None), md.MD_ERR_INVALID_ARG),
+    ("null kv_lens", dict(kv_lens=None), md.MD_ERR_INVALID_ARG),
+    ("misaligned q", dict(q=FAKE + 8), md.MD_ERR_INVALID_ARG),
+    ("misaligned k", dict(k=FAKE + 2), md.MD_ERR_INVALID_ARG),
+    ("misaligned o", dict(o=FAKE + 4), md.MD_ERR_INVALID_ARG),
+    ("token stride not 16 B", dict(kv_stride_tok=2 * 128 + 4), md.MD_ERR_INVALID_ARG),
+    ("head stride overlaps", dict(kv_stride_head=64), md.MD_ERR_INVALID_ARG),
+    ("negative stride", dict(kv_stride_blk=-8), md.MD_ERR_INVALID_ARG),
+    ("page table without page size", dict(page_table=FAKE), md.MD_ERR_INVALID_ARG),
+    ("page size without table", dict(page_size=16, max_pages_per_seq=4, num_pages=8),
+     md.MD_ERR_INVALID_ARG),
+    ("page size not power of two", dict(page_size=12, max_pages_per_seq=8, num_pages=8,
+                                        page_table=FAKE), md.MD_ERR_INVALID_ARG),
+    ("page table too narrow", dict(page_size=16, max_pages_per_seq=3, num_pages=8,
+                                   page_table=FAKE), md.MD_ERR_INVALID_ARG),
+    ("head_dim 96", dict(head_dim=96), md.MD_ERR_UNSUPPORTED),
+    ("G*L > 64", dict(num_q_heads=34, num_kv_heads=2), md.MD_ERR_UNSUPPORTED),
+]
+
+
+@pytest.mark.parametrize("name,over,want", BAD, ids=[b[0] for b in BAD])
+def test_verify_rejects(lib, name, over, want):
+    assert lib.md_verify_attn(ctypes.byref(good_args(**over)), None) == want
+    assert lib.md_draft_attn(ctypes.byref(good_args(**over)), 4, 16, None) == want
+
+
+def test_null_args(lib):
+    assert lib.md_verify_attn(None, None) == md.MD_ERR_INVALID_ARG
+    assert lib.md_draft_attn(None, 1, 1, None) == md.MD_ERR_INVALID_ARG
+    assert lib.md_workspace_bytes(None, 0, 0, 1) == 0
+
+
+@pytest.mark.parametrize("n_sink,window", [(-1, 8), (4, 0), (0, -3)])
+def test_draft_rejects_budget(lib, n_sink, window):
+    assert lib.md_draft_attn(ctypes.byref(good_args()), n_sink, window, None) == md.MD_ERR_INVALID_ARG
+
+
+def test_empty_batch_is_a_noop(lib):
+    a = good_args(num_seqs=0, q=None, k=None, v=None, o=None, kv_lens=None)
+    assert lib.md_verify_attn(ctypes.byref(a), None) == md.MD_OK
+    assert lib.md_draft_attn(ctypes.byref(a), 4, 8, None) == md.MD_OK
+
+
+def test_workspace_required_and_checked(lib):
+    # Few units and a long cache: the planner splits the range, needing workspace.
+    a = good_args(num_seqs=1, num_kv_heads=1, num_q_heads=4, max_kv_len=1 << 16,
+                  kv_stride_tok=128, kv_stride_blk=(1 << 16) * 128)
+    need = lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1)
+    assert need > 0
+    assert lib.md_verify_attn(ctypes.byref(a), None) == md.MD_ERR_WORKSPACE
+    a.workspace, a.workspace_bytes = FAKE, need - 1
+    assert lib.md_verify_attn(ctypes.byref(a), None) == md.MD_ERR_WORKSPACE
+    a.workspace, a.workspace_bytes = FAKE + 16, need
+    assert lib.md_verify_attn(ctypes.byref(a), None) == md.MD_ERR_WORKSPACE  # not 256-aligned
+
+
+def test_workspace_zero_when_units_fill_the_device(lib):
+    # 64 sequences x 8 kv heads = 512 units >= two per compute unit: one pass.
+    a = good_args(num_seqs=64, num_kv_heads=8, num_q_heads=32, q_len=5, max_kv_len=32768)
+    assert lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1) == 0
+
+
+def test_workspace_draft_smaller_than_verify(lib):
+    a = good_args(num_seqs=2, num_kv_heads=1, num_q_heads=8, q_len=4, max_kv_len=1 << 17,
+                  kv_stride_tok=128, kv_stride_blk=(1 << 17) * 128)
+    wv = lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1)
+    wd = lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_DRAFT, 64, 1984)
+    assert 0 <= wd < wv
+
+
+MERGE_BAD = [
+    ("no parts", dict(n_parts=0), md.MD_ERR_INVALID_ARG),
+    ("negative rows", dict(n_rows=-1), md.MD_ERR_INVALID_ARG),
+    ("bad dtype", dict(dt=3), md.MD_ERR_INVALID_ARG),
+    ("head_dim 32", dict(d=32), md.MD_ERR_UNSUPPORTED),
+    ("null o_parts", dict(op=None), md.MD_ERR_INVALID_ARG),
+    ("null o", dict(o=None), md.MD_ERR_INVALID_ARG),
+    ("misaligned lse", dict(lse=FAKE + 4), md.MD_ERR_INVALID_ARG),
+]
+
+
+@pytest.mark.parametrize("name,over,want", MERGE_BAD, ids=[m[0] for m in MERGE_BAD])
+def test_merge_rejects(lib, name, over, want):
+    kw = dict(n_parts=2, n_rows=8, d=128, dt=0, op=FAKE, lp=FAKE, o=FAKE, lse=FAKE)
+    kw.update(over)
+    assert lib.md_merge_lse(kw["n_parts"], kw["n_rows"], kw["d"], kw["dt"], kw["op"], kw["lp"],
+                            kw["o"], kw["lse"], None) == want
+
+
+def test_merge_zero_rows_is_a_noop(lib):
+    assert lib.md_merge_lse(3, 0, 64, 0, None, None, None, None, None) == md.MD_OK
+
+
+def test_bench_helpers_reject_bad_args(lib):
+    assert lib.md_bench_stream_read(None, 16, FAKE, None) == md.MD_ERR_INVALID_ARG
+    assert lib.md_bench_stream_read(FAKE, 17, FAKE, None) == md.MD_ERR_INVALID_ARG
+    assert lib.md_bench_copy(FAKE, FAKE + 4, 32, None) == md.MD_ERR_INVALID_ARG
+    assert lib.md_bench_fill(FAKE + 8, 32, 0, None) == md.MD_ERR_INVALID_ARG

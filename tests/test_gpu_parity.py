@@ -1,0 +1,101 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle on the
+same seeded inputs.
+
+Small cases are compared element by element over the whole output; they span
+several 32-token tiles with ragged tails, every row-tile count (G*L from 4 to
+64), both head dims and dtypes, contiguous and paged caches (page sizes 1 to
+64), single-pass and split-KV (merged) launches, and the degenerate cases
+(S = q_len, S = 1, q_len = 1, a window covering the cache, more sinks than
+tokens).  The full-size workloads run in the launch configuration the bench
+times and are checked on sampled (sequence, kv head) units the oracle
+computes one by one, plus properties that hold at any size.
+"""
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import TOL, compare, run_gpu, run_oracle, sample_units, say, unit_rows
+from paper_2408_11049_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+# name, B, q_len, Hq, Hkv, d, kv_lens, dtype, page_size, n_sink, window
+SMALL = [
+    ("cfg_tiny_f32", 2, 4, 4, 1, 64, [256, 256], "f32", 0, 4, 32),
+    ("bf16_d128_g4_ragged", 3, 4, 8, 2, 128, [300, 77, 1030], "bf16", 0, 4, 64),
+    ("bf16_d64_paged16", 4, 3, 6, 3, 64, [129, 16, 17, 500], "bf16", 16, 2, 30),
+    ("f32_d128", 2, 2, 4, 2, 128, [95, 160], "f32", 0, 1, 7),
+    ("f32_d64_paged8", 2, 5, 8, 2, 64, [70, 33], "f32", 8, 3, 10),
+    ("bf16_rows40", 2, 5, 16, 2, 128, [700, 450], "bf16", 0, 64, 200),
+    ("bf16_rows64", 1, 16, 4, 1, 64, [300], "bf16", 0, 8, 40),
+    ("bf16_rows12", 3, 3, 8, 2, 128, [64, 65, 63], "bf16", 0, 16, 20),
+    ("bf16_q1_mha", 3, 1, 8, 8, 128, [1, 50, 33], "bf16", 0, 4, 8),
+    ("f32_min_len", 2, 4, 4, 2, 64, [4, 5], "f32", 0, 1, 1),
+    ("bf16_split_kv", 2, 4, 8, 1, 128, [5000, 3100], "bf16", 0, 16, 496),
+    ("f32_split_kv_paged", 1, 3, 4, 1, 64, [4500], "f32", 16, 4, 100),
+    ("bf16_window_covers", 2, 4, 4, 2, 128, [40, 60], "bf16", 0, 10, 100),
+    ("bf16_sinks_exceed", 2, 2, 4, 2, 64, [30, 50], "bf16", 0, 64, 8),
+    ("bf16_page1", 2, 3, 4, 2, 64, [37, 20], "bf16", 1, 2, 9),
+    ("bf16_page64", 2, 3, 4, 2, 128, [300, 129], "bf16", 64, 2, 40),
+    ("f32_rows40_split", 1, 5, 8, 1, 128, [2600], "f32", 0, 16, 100),
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[s[0] for s in SMALL])
+@pytest.mark.parametrize("mode", [oracle.VERIFY, oracle.DRAFT], ids=["verify", "draft"])
+def test_small_against_oracle(case, mode):
+    name, B, L, Hq, Hkv, d, lens, dtype, ps, n_sink, window = case
+    say(f"[parity] {name} mode={mode} B={B} L={L} Hq={Hq} Hkv={Hkv} d={d} lens={lens} "
+        f"{dtype} page={ps} sink={n_sink} window={window}")
+    c = wl.make_case(B=B, q_len=L, Hq=Hq, Hkv=Hkv, d=d, kv_lens=lens, dtype=dtype, page_size=ps,
+                     seed=zlib.crc32(name.encode()) % 1000, device=DEV,
+                     S_alloc=None if ps else max(lens) + 5)  # NaN padding after every sequence
+    go, gl = run_gpu(mode, c, n_sink, window)
+    ro, rl = run_oracle(mode, c, n_sink, window)
+    compare(go, gl, ro, rl, dtype, f"{name}/{'verify' if mode == 0 else 'draft'}")
+
+
+def test_empty_batch():
+    c = wl.make_case(B=0, q_len=4, Hq=8, Hkv=2, d=128, kv_lens=[], dtype="bf16", device=DEV)
+    import paper_2408_11049_amd as md
+    o, l = md.md_verify_attn(c["q"], c["k"], c["v"], c["kv_lens"], max_kv_len=4)
+    o, l = md.md_draft_attn(c["q"], c["k"], c["v"], c["kv_lens"], 4, 8, max_kv_len=4)
+    torch.cuda.synchronize()
+    assert o.shape == (0, 4, 8, 128)
+
+
+FULL = ["tiny_f32", "llama8b_b32_s8k", "llama8b_b64_ragged_paged", "llama8b_b64_s32k_paged",
+        "llama8b_b256_s8k_koutlier", "llama70b_b16_s128k"]
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_full_size_sampled(name):
+    w = wl.WORKLOADS[name]
+    say(f"[full] {name}: B={w.B} Hq={w.Hq} Hkv={w.Hkv} d={w.d} S={w.S or (w.S_lo, w.S_hi)} "
+        f"L={w.q_len} sinks={w.n_sink} window={w.window} page={w.page_size}")
+    c = wl.make_workload(w, device=DEV)
+    G = w.Hq // w.Hkv
+    units = sample_units(c, 6, seed=w.seed_base)
+    try:
+        for mode, L in [(oracle.VERIFY, w.q_len), (oracle.DRAFT, w.q_len), (oracle.DRAFT, 1)]:
+            cc = c
+            if L != w.q_len:  # the real one-token draft step
+                cc = dict(c)
+                cc["q"] = c["q"][:, :1].contiguous()
+                cc["q_len"] = 1
+            go, gl = run_gpu(mode, cc, w.n_sink, w.window)
+            assert not np.isnan(go).any() and not np.isnan(gl).any(), "NaN in a full-size output"
+            assert np.isfinite(gl).all()
+            for b, hk in units:
+                q, k, v, lens = wl.gather_unit(cc, b, hk)
+                ro, rl = oracle.attention(mode, q, k, v, lens, n_sink=w.n_sink, window=w.window)
+                compare(unit_rows(go, b, hk, G)[None], unit_rows(gl[..., None], b, hk, G)[None, ..., 0],
+                        ro, rl, w.dtype, f"{name}/{['verify', 'draft'][mode]}/L={L}/unit({b},{hk})")
+    finally:
+        del c
+        torch.cuda.empty_cache()
