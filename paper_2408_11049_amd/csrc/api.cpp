@@ -2,6 +2,7 @@
 // and the launches on the caller's stream.  No allocation, no host sync.
 #include <hip/hip_runtime.h>
 #include <math.h>
+#include <stdlib.h>
 
 #include <atomic>
 #include <string>
@@ -23,6 +24,22 @@ int hip_fail(hipError_t e) {
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// K/V tiles in flight per wave.  MD_PREFETCH_DEPTH (1..3) overrides the
+// default, for tuning sweeps.
+int prefetch_depth(int NT, int mode) {
+  static const int forced = [] {
+    const char* e = getenv("MD_PREFETCH_DEPTH");
+    int v = e ? atoi(e) : 0;
+    return (v >= 1 && v <= 3) ? v : 0;
+  }();
+  if (forced) return forced;
+  // Measured on MI355X: two tiles in flight pay off only for the long
+  // verify streams with two row tiles; elsewhere one tile is as fast and
+  // keeps more registers for occupancy.
+  if (mode == MD_MODE_VERIFY && NT == 2) return 2;
+  return 1;
+}
 
 int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void* stream) {
   int st = validate_attn(a, mode, n_sink, window);
@@ -67,7 +84,7 @@ int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void*
     p.part_lse = reinterpret_cast<float*>(static_cast<unsigned char*>(a->workspace) + pl.part_o_bytes);
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
-  hipError_t e = launch_attn_partial(p, a->head_dim, bf16, pl.NT, paged,
+  hipError_t e = launch_attn_partial(p, a->head_dim, bf16, pl.NT, paged, prefetch_depth(pl.NT, mode),
                                      pl.n_units * pl.n_chunks, s);
   if (e != hipSuccess) return hip_fail(e);
   if (pl.n_chunks > 1) {

@@ -34,15 +34,14 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
-__device__ __forceinline__ float bf16_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
-
-// fp32 -> bf16, round to nearest even (NaN stays NaN).
-__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return u >> 16;
+// Two fp32 -> packed bf16, round to nearest even (one v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -58,7 +57,9 @@ struct Shape {
   static constexpr int TPI = 64 / LPT;             // V tokens per load instruction
   static constexpr int NV = kTile / TPI;           // V loads per lane per tile
   static constexpr int CB16 = D / 16;              // 16-channel blocks of O
-  static constexpr int VROW = D * ES + (BF16 ? 8 : 16);  // padded LDS row (bytes)
+  // Padded LDS row (bytes): an odd multiple of 32 B keeps the 16-row
+  // transposed reads of one channel block spread over all banks.
+  static constexpr int VROW = D * ES + (BF16 ? 32 : 16);
   static constexpr int VTILE = kTile * VROW;       // one wave's LDS V tile
 };
 
@@ -74,7 +75,7 @@ __device__ __forceinline__ int real_token(const UnitGeom& u, int v) {
   return v < u.seg0 ? v : v - u.seg0 + u.seg1_start;
 }
 
-template <int D, bool BF16, int NT, bool PAGED>
+template <int D, bool BF16, int NT, bool PAGED, int P>
 __global__ void __launch_bounds__(kWaves * 64)
 attn_partial_kernel(const AttnParams p) {
   using SH = Shape<D, BF16>;
@@ -143,28 +144,43 @@ attn_partial_kernel(const AttnParams p) {
   const int32_t* ptab = PAGED ? p.page_table + static_cast<int64_t>(b) * p.max_pages : nullptr;
   const int pmask = (1 << p.page_shift) - 1;
 
-  // Element offset of real token t given its page id (paged) -- or -1 if the
-  // page id is outside the pool, so the token is never dereferenced.
-  auto tok_offset = [&](int t, int pid) -> int64_t {
+  // Element offset of real token t given its page id (paged).  A token that
+  // must not be read (past the chunk, or a page id outside the pool) is
+  // redirected to element 0 of the tensor -- always in bounds -- and its
+  // value is discarded: scores are masked, V rows are zeroed.  Loads are
+  // therefore never under divergent control flow, which lets the compiler
+  // keep every prefetched tile in flight across loop iterations.
+  auto tok_offset = [&](int t, int pid, bool& ok) -> int64_t {
     if (PAGED) {
-      if (pid < 0 || pid >= p.num_pages) return -1;
-      return static_cast<int64_t>(pid) * p.s_blk + static_cast<int64_t>(t & pmask) * p.s_tok +
-             head_off;
+      ok = ok && pid >= 0 && pid < p.num_pages;
+      return ok ? static_cast<int64_t>(pid) * p.s_blk +
+                      static_cast<int64_t>(t & pmask) * p.s_tok + head_off
+                : 0;
     }
-    return static_cast<int64_t>(b) * p.s_blk + static_cast<int64_t>(t) * p.s_tok + head_off;
+    return ok ? static_cast<int64_t>(b) * p.s_blk + static_cast<int64_t>(t) * p.s_tok + head_off
+              : 0;
   };
 
-  // Page id of the token this lane stands for (lane & 31 of tile `tile`).
+  // Page id of the token this lane stands for (lane & 31 of tile `tile`);
+  // -1 past the chunk.  The table row of sequence b always has an entry 0.
   auto load_pid = [&](int tile) -> int {
     if (!PAGED) return 0;
-    int v = u.v_begin + tile * kTile + (lane & 31);
-    if (tile >= n_tiles || v >= u.v_end) return -1;
-    return ptab[real_token(u, v) >> p.page_shift];
+    const int v = u.v_begin + tile * kTile + (lane & 31);
+    const bool ok = tile < n_tiles && v < u.v_end;
+    const int pid = ptab[ok ? (real_token(u, v) >> p.page_shift) : 0];
+    return ok ? pid : -1;
   };
 
   struct TileRegs {
     u32x4 k[SH::KL];
     u32x4 v[SH::NV];
+    uint32_t vok;  // bit n: V row of load n is real (else written to LDS as zeros)
+  };
+
+  // 16-byte streaming load: every K/V byte is read exactly once, so the
+  // loads carry the nontemporal hint and do not displace reusable lines.
+  auto ld16 = [](const unsigned char* ptr) -> u32x4 {
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(ptr));
   };
 
   // Issue the loads of one tile.  tpid: this lane's page id for token lane&31.
@@ -173,27 +189,23 @@ attn_partial_kernel(const AttnParams p) {
     const bool live = tile < n_tiles;
     // K: lane = token (l16) of block tb, channel group grp of block cb.
     for (int tb = 0; tb < 2; ++tb) {
-      int vt = v0 + tb * 16 + l16;
-      int pid = PAGED ? __shfl(tpid, tb * 16 + l16) : 0;
+      const int vt = v0 + tb * 16 + l16;
+      const int pid = PAGED ? __shfl(tpid, tb * 16 + l16) : 0;
       bool ok = live && vt < u.v_end;
-      int64_t off = ok ? tok_offset(real_token(u, vt), pid) : -1;
-      for (int cb = 0; cb < SH::KCB; ++cb) {
-        u32x4 x = u32x4{0, 0, 0, 0};
-        if (off >= 0) x = *reinterpret_cast<const u32x4*>(kbase + off * SH::ES + cb * 64 + grp * 16);
-        T.k[tb * SH::KCB + cb] = x;
-      }
+      const int64_t off = tok_offset(real_token(u, vt), pid, ok);
+      for (int cb = 0; cb < SH::KCB; ++cb)
+        T.k[tb * SH::KCB + cb] = ld16(kbase + off * SH::ES + cb * 64 + grp * 16);
     }
     // V: whole token rows, LPT lanes per token.
+    T.vok = 0;
     for (int n = 0; n < SH::NV; ++n) {
-      int tt = n * SH::TPI + lane / SH::LPT;
-      int vt = v0 + tt;
-      int pid = PAGED ? __shfl(tpid, tt) : 0;
+      const int tt = n * SH::TPI + lane / SH::LPT;
+      const int vt = v0 + tt;
+      const int pid = PAGED ? __shfl(tpid, tt) : 0;
       bool ok = live && vt < u.v_end;
-      int64_t off = ok ? tok_offset(real_token(u, vt), pid) : -1;
-      u32x4 x = u32x4{0, 0, 0, 0};
-      if (off >= 0)
-        x = *reinterpret_cast<const u32x4*>(vbase + off * SH::ES + (lane % SH::LPT) * 16);
-      T.v[n] = x;
+      const int64_t off = tok_offset(real_token(u, vt), pid, ok);
+      T.v[n] = ld16(vbase + off * SH::ES + (lane % SH::LPT) * 16);
+      T.vok |= static_cast<uint32_t>(ok) << n;
     }
   };
 
@@ -208,98 +220,127 @@ attn_partial_kernel(const AttnParams p) {
 
   unsigned char* vt_lds = lds + wave * SH::VTILE;
 
-  TileRegs cur, nxt;
-  int tile = wave;
-  int pid_cur = load_pid(tile);
-  int pid_nxt = load_pid(tile + kWaves);
-  if (tile < n_tiles) load_tile(cur, tile, pid_cur);
+  // One tile: V to LDS and S^T = K Q^T from the tile's registers, which are
+  // then refilled with tile `tile + P*kWaves` (so P tiles stay in flight
+  // through the softmax and PV below), then the online softmax and O^T += V^T P^T.
+  // Per-unit facts for the mask fast path: the smallest and largest query
+  // positions of the unit's real rows.
+  const int pos_min = u.S - L;
+  const int pos_max = u.S - 1;
+  constexpr float kLazy = 8.f;  // log2 headroom before the running max must move
 
-  for (; tile < n_tiles; tile += kWaves) {
-    // Prefetch: page ids two tiles ahead, K/V one tile ahead.
-    int pid_nn = load_pid(tile + 2 * kWaves);
-    load_tile(nxt, tile + kWaves, pid_nxt);
-
+  auto process = [&](TileRegs& T, int tile, int& pid_slot) {
     const int v0 = u.v_begin + tile * kTile;
-
-    // Stage V rows in this wave's LDS tile (row tt, channels (lane%LPT)*E16..).
-    for (int n = 0; n < SH::NV; ++n) {
-      int tt = n * SH::TPI + lane / SH::LPT;
-      unsigned char* dst = vt_lds + tt * SH::VROW + (lane % SH::LPT) * 16;
-      reinterpret_cast<u32x2*>(dst)[0] = u32x2{cur.v[n].x, cur.v[n].y};
-      reinterpret_cast<u32x2*>(dst)[1] = u32x2{cur.v[n].z, cur.v[n].w};
+    // Does any key of this tile need masking for any real row?  (Uniform.)
+    const bool full = v0 + kTile <= u.v_end;
+    bool needs_mask = true;
+    if (full && !(v0 < u.seg0 && v0 + kTile > u.seg0)) {
+      const int t0 = real_token(u, v0), t1 = t0 + kTile - 1;
+      needs_mask = t1 > pos_min;
+      if (p.mode == MD_MODE_DRAFT)
+        needs_mask = needs_mask || !(t1 < p.n_sink || t0 >= pos_max - p.window + 1);
     }
 
-    // Real token index and validity of this lane's 8 score slots.
-    int tok[2][4];
-    bool tvalid[2][4];
-    for (int tb = 0; tb < 2; ++tb)
-      for (int e = 0; e < 4; ++e) {
-        int vt = v0 + tb * 16 + grp * 4 + e;
-        tvalid[tb][e] = vt < u.v_end;
-        tok[tb][e] = real_token(u, vt);
-      }
+    // Stage V rows in this wave's LDS tile (row tt, 16 B chunk lane%LPT);
+    // rows of tokens that are not real are written as zeros.
+    for (int n = 0; n < SH::NV; ++n) {
+      const int tt = n * SH::TPI + lane / SH::LPT;
+      u32x4 x = T.v[n];
+      if (!full) x = ((T.vok >> n) & 1u) ? x : u32x4{0, 0, 0, 0};
+      *reinterpret_cast<u32x4*>(vt_lds + tt * SH::VROW + (lane % SH::LPT) * 16) = x;
+    }
 
-    // S^T = K Q^T, masked, scaled into the log2 domain.
-    float x[NT][2][4];
+    // S^T = K Q^T.
+    f32x4 sacc[NT][2];
     for (int tb = 0; tb < 2; ++tb) {
       for (int rt = 0; rt < NT; ++rt) {
-        f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+        f32x4 sv = f32x4{0.f, 0.f, 0.f, 0.f};
         for (int cb = 0; cb < SH::KCB; ++cb) {
-          const u32x4 kk = cur.k[tb * SH::KCB + cb];
+          const u32x4 kk = T.k[tb * SH::KCB + cb];
           const u32x4 qq = qreg[rt][cb];
           if constexpr (BF16) {
-            s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kk),
-                                                        __builtin_bit_cast(bf16x8, qq), s, 0, 0, 0);
+            sv = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kk),
+                                                         __builtin_bit_cast(bf16x8, qq), sv, 0, 0, 0);
           } else {
             for (int j = 0; j < 4; ++j)
-              s = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kk[j]),
-                                                        __uint_as_float(qq[j]), s, 0, 0, 0);
+              sv = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kk[j]),
+                                                         __uint_as_float(qq[j]), sv, 0, 0, 0);
           }
         }
-        for (int e = 0; e < 4; ++e) {
-          const int t = tok[tb][e];
-          const int pos = row_pos[rt];
-          bool vis = tvalid[tb][e] && t <= pos;
-          if (p.mode == MD_MODE_DRAFT) vis = vis && (t < p.n_sink || t >= pos - p.window + 1);
-          x[rt][tb][e] = vis ? s[e] * p.scale_log2 : -INFINITY;
-        }
+        sacc[rt][tb] = sv;
       }
     }
 
-    // Online softmax per row: tile max over this lane's 8 slots and the 3
-    // other lanes holding the same row (lanes l16 + 16*grp).
-    u32x4 pb[NT];    // bf16 P^T B operand (8 slots)
-    float pf[NT][2][4];  // fp32 P for the fp32 path
-    for (int rt = 0; rt < NT; ++rt) {
-      float mx = -INFINITY;
-      for (int tb = 0; tb < 2; ++tb)
-        for (int e = 0; e < 4; ++e) mx = fmaxf(mx, x[rt][tb][e]);
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run[rt], mx);
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = fast_exp2(m_run[rt] - m_use);
-      m_run[rt] = m_new;
-      float psum = 0.f;
-      uint32_t h[8];
+    // The tile's registers are free: refill them P tiles ahead.  Page ids
+    // run P tiles further ahead still, so waiting for one never waits on a
+    // K/V load that is not already needed.
+    {
+      const int ahead = tile + P * kWaves;
+      const int pid_far = load_pid(ahead + P * kWaves);
+      load_tile(T, ahead, pid_slot);
+      pid_slot = pid_far;
+    }
+
+    // Scale into the log2 domain; mask only where some key is not visible.
+    float x[NT][2][4];
+    if (!needs_mask) {
+      for (int rt = 0; rt < NT; ++rt)
+        for (int tb = 0; tb < 2; ++tb)
+          for (int e = 0; e < 4; ++e) x[rt][tb][e] = sacc[rt][tb][e] * p.scale_log2;
+    } else {
       for (int tb = 0; tb < 2; ++tb)
         for (int e = 0; e < 4; ++e) {
-          float pv = fast_exp2(x[rt][tb][e] - m_use);
-          if constexpr (BF16) {
-            uint32_t hb = f32_to_bf16(pv);
-            h[tb * 4 + e] = hb;
-            psum += bf16_to_f32(hb);  // normalise by exactly what multiplies V
-          } else {
-            pf[rt][tb][e] = pv;
-            psum += pv;
+          const int vt = v0 + tb * 16 + grp * 4 + e;
+          const int t = real_token(u, vt);
+          const bool tv = vt < u.v_end;
+          for (int rt = 0; rt < NT; ++rt) {
+            const int pos = row_pos[rt];
+            bool vis = tv && t <= pos;
+            if (p.mode == MD_MODE_DRAFT) vis = vis && (t < p.n_sink || t >= pos - p.window + 1);
+            x[rt][tb][e] = vis ? sacc[rt][tb][e] * p.scale_log2 : -INFINITY;
           }
         }
-      if constexpr (BF16) {
-        pb[rt] = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
-                       h[6] | (h[7] << 16)};
+    }
+
+    // Online softmax per row (lane l16 + 16*grp all hold row l16).  The
+    // running max is moved only when some row's tile max exceeds it by more
+    // than kLazy, so most tiles skip the rescale; until then P <= 2^kLazy.
+    u32x4 pb[NT];        // bf16 P^T B operand (8 slots)
+    float pf[NT][2][4];  // fp32 P for the fp32 path
+    for (int rt = 0; rt < NT; ++rt) {
+      float mx = fmaxf(fmaxf(fmaxf(x[rt][0][0], x[rt][0][1]), fmaxf(x[rt][0][2], x[rt][0][3])),
+                       fmaxf(fmaxf(x[rt][1][0], x[rt][1][1]), fmaxf(x[rt][1][2], x[rt][1][3])));
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      if (__any(mx > m_run[rt] + kLazy)) {
+        const float m_new = fmaxf(m_run[rt], mx);
+        const float alpha = m_new == -INFINITY ? 1.f : fast_exp2(m_run[rt] - m_new);
+        m_run[rt] = m_new;
+        l_run[rt] *= alpha;
+        for (int c = 0; c < SH::CB16; ++c) acc[rt][c] *= alpha;
       }
-      l_run[rt] = l_run[rt] * alpha + psum;
-      for (int c = 0; c < SH::CB16; ++c) acc[rt][c] *= alpha;
+      const float m_use = m_run[rt] == -INFINITY ? 0.f : m_run[rt];
+      float pv[8];
+      for (int tb = 0; tb < 2; ++tb)
+        for (int e = 0; e < 4; ++e) pv[tb * 4 + e] = fast_exp2(x[rt][tb][e] - m_use);
+      if constexpr (BF16) {
+        const u32x4 h = u32x4{pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]),
+                              pack_bf16x2(pv[4], pv[5]), pack_bf16x2(pv[6], pv[7])};
+        pb[rt] = h;
+        // Normalise by exactly what multiplies V (the rounded P).
+        float psum = 0.f;
+        for (int j = 0; j < 4; ++j)
+          psum += __uint_as_float(h[j] << 16) + __uint_as_float(h[j] & 0xffff0000u);
+        l_run[rt] += psum;
+      } else {
+        float psum = 0.f;
+        for (int tb = 0; tb < 2; ++tb)
+          for (int e = 0; e < 4; ++e) {
+            pf[rt][tb][e] = pv[tb * 4 + e];
+            psum += pv[tb * 4 + e];
+          }
+        l_run[rt] += psum;
+      }
     }
 
     // O^T += V^T P^T.  A operand: lane = channel (l16) of block c, slots of
@@ -308,22 +349,23 @@ attn_partial_kernel(const AttnParams p) {
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     for (int c = 0; c < SH::CB16; ++c) {
-      const int ch = c * 16 + l16;
       if constexpr (BF16) {
-        const unsigned char* src = vt_lds + ch * 2;
-        uint32_t e[8];
-        for (int j = 0; j < 8; ++j) {
-          int tt = (j < 4) ? grp * 4 + j : 16 + grp * 4 + (j - 4);
-          e[j] = *reinterpret_cast<const uint16_t*>(src + tt * SH::VROW);
-        }
-        const u32x4 va = u32x4{e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16),
-                               e[6] | (e[7] << 16)};
+        // Transposed LDS reads: in each 16-lane group, lane k supplies row
+        // (4*grp + k/4) and channels c*16 + 4*(k%4) .. +3, and lane i gets
+        // channel c*16 + i of those 4 rows -- tokens 4grp..4grp+3, then the
+        // same 16 tokens later for slots 4..7.
+        const unsigned char* src = vt_lds + (4 * grp + (l16 >> 2)) * SH::VROW +
+                                   (c * 16 + 4 * (l16 & 3)) * 2;
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(src));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(src + 16 * SH::VROW));
+        const bf16x8 va = __builtin_bit_cast(
+            bf16x8, u32x4{__builtin_bit_cast(u32x2, lo).x, __builtin_bit_cast(u32x2, lo).y,
+                          __builtin_bit_cast(u32x2, hi).x, __builtin_bit_cast(u32x2, hi).y});
         for (int rt = 0; rt < NT; ++rt)
           acc[rt][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              __builtin_bit_cast(bf16x8, va), __builtin_bit_cast(bf16x8, pb[rt]), acc[rt][c], 0,
-              0, 0);
+              va, __builtin_bit_cast(bf16x8, pb[rt]), acc[rt][c], 0, 0, 0);
       } else {
-        const unsigned char* src = vt_lds + ch * 4;
+        const unsigned char* src = vt_lds + (c * 16 + l16) * 4;
         for (int tb = 0; tb < 2; ++tb)
           for (int j = 0; j < 4; ++j) {
             float va = *reinterpret_cast<const float*>(src + (tb * 16 + grp * 4 + j) * SH::VROW);
@@ -333,13 +375,28 @@ attn_partial_kernel(const AttnParams p) {
           }
       }
     }
-    // The next iteration overwrites this wave's LDS tile: keep the reads first.
+    // The next tile overwrites this wave's LDS tile: keep the reads first.
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  };
 
-    cur = nxt;
-    pid_nxt = pid_nn;
+  // Prologue: this wave's first P tiles in flight; page ids of the P tiles
+  // after them.
+  TileRegs ring[P];
+  int pid_ring[P];
+  {
+    int pid0[P];
+    for (int s = 0; s < P; ++s) pid0[s] = load_pid(wave + s * kWaves);
+    for (int s = 0; s < P; ++s) pid_ring[s] = load_pid(wave + (s + P) * kWaves);
+    for (int s = 0; s < P; ++s) load_tile(ring[s], wave + s * kWaves, pid0[s]);
+  }
+  // Every ring slot is processed unconditionally (a tile past the chunk is
+  // fully masked: it leaves m, l and O unchanged), so no slot becomes a
+  // conditionally-updated loop-carried value that would force a full wait.
+  for (int base = wave; base < n_tiles; base += P * kWaves) {
+#pragma unroll
+    for (int s = 0; s < P; ++s) process(ring[s], base + s * kWaves, pid_ring[s]);
   }
 
   // ---- row sums: add the 4 lanes that share a row
@@ -405,11 +462,9 @@ attn_partial_kernel(const AttnParams p) {
       const float lse = (Lt > 0.f) ? (M + fast_log2(Lt)) * 0.69314718055994530942f : -INFINITY;
       if (direct) {
         if constexpr (BF16) {
-          uint32_t hb[8];
-          for (int j = 0; j < 8; ++j) hb[j] = f32_to_bf16(o8[j]);
           *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(p.o) + row_g * D + c0) =
-              u32x4{hb[0] | (hb[1] << 16), hb[2] | (hb[3] << 16), hb[4] | (hb[5] << 16),
-                    hb[6] | (hb[7] << 16)};
+              u32x4{pack_bf16x2(o8[0], o8[1]), pack_bf16x2(o8[2], o8[3]),
+                    pack_bf16x2(o8[4], o8[5]), pack_bf16x2(o8[6], o8[7])};
         } else {
           float* op = static_cast<float*>(p.o) + row_g * D + c0;
           *reinterpret_cast<f32x4*>(op) = f32x4{o8[0], o8[1], o8[2], o8[3]};
@@ -430,36 +485,49 @@ attn_partial_kernel(const AttnParams p) {
 // ---------------------------------------------------------------------------
 // Host-side dispatch over the compiled instances.
 
-template <int D, bool BF16, int NT>
-static hipError_t launch_nt(const AttnParams& p, bool paged, int64_t n_blocks, hipStream_t s) {
+template <int D, bool BF16, int NT, int P>
+static hipError_t launch_p(const AttnParams& p, bool paged, int64_t n_blocks, hipStream_t s) {
   dim3 grid(static_cast<uint32_t>(n_blocks)), block(kWaves * 64);
   if (paged)
-    hipLaunchKernelGGL((attn_partial_kernel<D, BF16, NT, true>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((attn_partial_kernel<D, BF16, NT, true, P>), grid, block, 0, s, p);
   else
-    hipLaunchKernelGGL((attn_partial_kernel<D, BF16, NT, false>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((attn_partial_kernel<D, BF16, NT, false, P>), grid, block, 0, s, p);
   return hipGetLastError();
 }
 
+template <int D, bool BF16, int NT>
+static hipError_t launch_nt(const AttnParams& p, bool paged, int depth, int64_t n_blocks,
+                            hipStream_t s) {
+  if constexpr (BF16) {
+    if (depth <= 1) return launch_p<D, BF16, NT, 1>(p, paged, n_blocks, s);
+    if (depth == 2) return launch_p<D, BF16, NT, 2>(p, paged, n_blocks, s);
+    return launch_p<D, BF16, NT, 3>(p, paged, n_blocks, s);
+  } else {
+    (void)depth;  // fp32 serves small problems: one tile in flight
+    return launch_p<D, BF16, NT, 1>(p, paged, n_blocks, s);
+  }
+}
+
 template <int D, bool BF16>
-static hipError_t launch_d(const AttnParams& p, int NT, bool paged, int64_t n_blocks,
+static hipError_t launch_d(const AttnParams& p, int NT, bool paged, int depth, int64_t n_blocks,
                            hipStream_t s) {
   switch (NT) {
-    case 1: return launch_nt<D, BF16, 1>(p, paged, n_blocks, s);
-    case 2: return launch_nt<D, BF16, 2>(p, paged, n_blocks, s);
-    case 3: return launch_nt<D, BF16, 3>(p, paged, n_blocks, s);
-    case 4: return launch_nt<D, BF16, 4>(p, paged, n_blocks, s);
+    case 1: return launch_nt<D, BF16, 1>(p, paged, depth, n_blocks, s);
+    case 2: return launch_nt<D, BF16, 2>(p, paged, depth, n_blocks, s);
+    case 3: return launch_nt<D, BF16, 3>(p, paged, depth, n_blocks, s);
+    case 4: return launch_nt<D, BF16, 4>(p, paged, depth, n_blocks, s);
   }
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_attn_partial(const AttnParams& p, int head_dim, bool bf16, int NT, bool paged,
-                               int64_t n_blocks, hipStream_t s) {
+                               int depth, int64_t n_blocks, hipStream_t s) {
   if (n_blocks <= 0) return hipSuccess;
   if (head_dim == 128)
-    return bf16 ? launch_d<128, true>(p, NT, paged, n_blocks, s)
-                : launch_d<128, false>(p, NT, paged, n_blocks, s);
-  return bf16 ? launch_d<64, true>(p, NT, paged, n_blocks, s)
-              : launch_d<64, false>(p, NT, paged, n_blocks, s);
+    return bf16 ? launch_d<128, true>(p, NT, paged, depth, n_blocks, s)
+                : launch_d<128, false>(p, NT, paged, depth, n_blocks, s);
+  return bf16 ? launch_d<64, true>(p, NT, paged, depth, n_blocks, s)
+              : launch_d<64, false>(p, NT, paged, depth, n_blocks, s);
 }
 
 }  // namespace md

@@ -31,8 +31,9 @@ struct AttnParams {
   int64_t n_rows;
 };
 
+// depth: K/V tiles each wave keeps in flight (1..3; bf16 instances).
 hipError_t launch_attn_partial(const AttnParams& p, int head_dim, bool bf16, int NT, bool paged,
-                               int64_t n_blocks, hipStream_t s);
+                               int depth, int64_t n_blocks, hipStream_t s);
 
 hipError_t launch_merge_lse(int n_parts, int64_t n_rows, int head_dim, bool out_bf16,
                             const float* o_parts, const float* lse_parts, void* o, float* lse,
