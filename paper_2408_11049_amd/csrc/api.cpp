@@ -27,18 +27,31 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 // K/V tiles in flight per wave.  MD_PREFETCH_DEPTH (1..3) overrides the
 // default, for tuning sweeps.
+int env_int(const char* name, int lo, int hi) {
+  const char* e = getenv(name);
+  int v = e ? atoi(e) : 0;
+  return (v >= lo && v <= hi) ? v : 0;
+}
+
 int prefetch_depth(int NT, int mode) {
-  static const int forced = [] {
-    const char* e = getenv("MD_PREFETCH_DEPTH");
-    int v = e ? atoi(e) : 0;
-    return (v >= 1 && v <= 3) ? v : 0;
-  }();
+  static const int forced = env_int("MD_PREFETCH_DEPTH", 1, 3);
+  (void)NT;
+  (void)mode;
+  // Measured on MI355X: with K and V both streamed as whole rows, one tile in
+  // flight per wave already saturates HBM for every shape; deeper rings
+  // only cost registers.
+  return forced ? forced : 1;
+}
+
+// Waves per SIMD targeted by the kernel instance (MD_OCCUPANCY = 1 or 2
+// overrides, for tuning sweeps).  Long verify streams with two row tiles run
+// best at one wave per SIMD (more registers, no spills); the short draft
+// calls and single-row-tile shapes at two.
+int occupancy(int NT, int depth, int mode) {
+  static const int forced = env_int("MD_OCCUPANCY", 1, 2);
   if (forced) return forced;
-  // Measured on MI355X: two tiles in flight pay off only for the long
-  // verify streams with two row tiles; elsewhere one tile is as fast and
-  // keeps more registers for occupancy.
-  if (mode == MD_MODE_VERIFY && NT == 2) return 2;
-  return 1;
+  if (depth != 1 || NT > 2) return 1;
+  return (mode == MD_MODE_VERIFY && NT == 2) ? 1 : 2;
 }
 
 int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void* stream) {
@@ -84,8 +97,9 @@ int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void*
     p.part_lse = reinterpret_cast<float*>(static_cast<unsigned char*>(a->workspace) + pl.part_o_bytes);
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
-  hipError_t e = launch_attn_partial(p, a->head_dim, bf16, pl.NT, paged, prefetch_depth(pl.NT, mode),
-                                     pl.n_units * pl.n_chunks, s);
+  const int depth = prefetch_depth(pl.NT, mode);
+  hipError_t e = launch_attn_partial(p, a->head_dim, bf16, pl.NT, paged, depth,
+                                     occupancy(pl.NT, depth, mode), pl.n_units * pl.n_chunks, s);
   if (e != hipSuccess) return hip_fail(e);
   if (pl.n_chunks > 1) {
     e = launch_merge_lse(pl.n_chunks, pl.n_rows, a->head_dim, bf16, p.part_o, p.part_lse, a->o,
@@ -171,7 +185,7 @@ size_t md_attn_args_size(void) { return sizeof(md_attn_args); }
 
 int md_bench_stream_read(const void* buf, size_t bytes, float* sink, void* stream) {
   if (!buf || !sink || !md::aligned16(buf) || bytes % 16) return MD_ERR_INVALID_ARG;
-  hipError_t e = md::launch_bench_read(buf, bytes, sink, md::device_cu_count() * 8,
+  hipError_t e = md::launch_bench_read(buf, bytes, sink, md::device_cu_count() * 2,
                                        static_cast<hipStream_t>(stream));
   return e == hipSuccess ? MD_OK : md::hip_fail(e);
 }

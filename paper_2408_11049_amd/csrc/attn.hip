@@ -51,16 +51,19 @@ template <int D, bool BF16>
 struct Shape {
   static constexpr int ES = BF16 ? 2 : 4;          // element bytes
   static constexpr int E16 = 16 / ES;              // elements per 16 B
-  static constexpr int KCB = D * ES / 64;          // 16 B K loads per lane per 16-token block
-  static constexpr int KL = 2 * KCB;               // per tile (two 16-token blocks)
-  static constexpr int LPT = D * ES / 16;          // lanes per V token row
-  static constexpr int TPI = 64 / LPT;             // V tokens per load instruction
-  static constexpr int NV = kTile / TPI;           // V loads per lane per tile
+  static constexpr int KCB = D * ES / 64;          // 16 B A-operand chunks per lane per 16-token block
+  static constexpr int LPT = D * ES / 16;          // lanes per token row (16 B each)
+  static constexpr int TPI = 64 / LPT;             // token rows per load instruction
+  static constexpr int NV = kTile / TPI;           // K (and V) loads per lane per tile
   static constexpr int CB16 = D / 16;              // 16-channel blocks of O
-  // Padded LDS row (bytes): an odd multiple of 32 B keeps the 16-row
-  // transposed reads of one channel block spread over all banks.
+  // Padded LDS rows (bytes).  K: an odd multiple of 16 B, so the 16 rows of
+  // one A-operand read hit distinct banks.  V: an odd multiple of 32 B, so
+  // the 16-row transposed reads of one channel block spread over all banks.
+  static constexpr int KROW = D * ES + 16;
   static constexpr int VROW = D * ES + (BF16 ? 32 : 16);
-  static constexpr int VTILE = kTile * VROW;       // one wave's LDS V tile
+  static constexpr int KTILE = kTile * KROW;
+  static constexpr int VTILE = kTile * VROW;
+  static constexpr int WTILE = KTILE + VTILE;      // one wave's LDS staging
 };
 
 // Where a virtual token of the unit's visible range lives.
@@ -75,15 +78,15 @@ __device__ __forceinline__ int real_token(const UnitGeom& u, int v) {
   return v < u.seg0 ? v : v - u.seg0 + u.seg1_start;
 }
 
-template <int D, bool BF16, int NT, bool PAGED, int P>
-__global__ void __launch_bounds__(kWaves * 64)
+template <int D, bool BF16, int NT, bool PAGED, int P, int OCC>
+__global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(OCC)))
 attn_partial_kernel(const AttnParams p) {
   using SH = Shape<D, BF16>;
   constexpr int ROWS = NT * 16;
   // LDS: the V tiles during the main loop, then the cross-wave merge buffers.
   constexpr int kMergeO = kWaves * 16 * D * 4;
   constexpr int kMergeStats = 2 * kWaves * ROWS * 4;
-  constexpr int kLds = (kWaves * SH::VTILE > kMergeO + kMergeStats) ? kWaves * SH::VTILE
+  constexpr int kLds = (kWaves * SH::WTILE > kMergeO + kMergeStats) ? kWaves * SH::WTILE
                                                                      : kMergeO + kMergeStats;
   __shared__ __attribute__((aligned(16))) unsigned char lds[kLds];
 
@@ -172,9 +175,9 @@ attn_partial_kernel(const AttnParams p) {
   };
 
   struct TileRegs {
-    u32x4 k[SH::KL];
+    u32x4 k[SH::NV];
     u32x4 v[SH::NV];
-    uint32_t vok;  // bit n: V row of load n is real (else written to LDS as zeros)
+    uint32_t ok;  // bit n: token row of load n is real (else V is staged as zeros)
   };
 
   // 16-byte streaming load: every K/V byte is read exactly once, so the
@@ -183,29 +186,24 @@ attn_partial_kernel(const AttnParams p) {
     return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(ptr));
   };
 
-  // Issue the loads of one tile.  tpid: this lane's page id for token lane&31.
+  // Issue the loads of one tile.  K and V are read the same way: LPT lanes
+  // cover one whole token row (256 B for bf16, d = 128), TPI rows per
+  // instruction -- full-row accesses stream markedly faster from HBM than
+  // the 64 B-per-row pattern of the MFMA operand layout.  One address per
+  // token serves both.  tpid: this lane's page id for token lane&31.
   auto load_tile = [&](TileRegs& T, int tile, int tpid) {
     const int v0 = u.v_begin + tile * kTile;
     const bool live = tile < n_tiles;
-    // K: lane = token (l16) of block tb, channel group grp of block cb.
-    for (int tb = 0; tb < 2; ++tb) {
-      const int vt = v0 + tb * 16 + l16;
-      const int pid = PAGED ? __shfl(tpid, tb * 16 + l16) : 0;
-      bool ok = live && vt < u.v_end;
-      const int64_t off = tok_offset(real_token(u, vt), pid, ok);
-      for (int cb = 0; cb < SH::KCB; ++cb)
-        T.k[tb * SH::KCB + cb] = ld16(kbase + off * SH::ES + cb * 64 + grp * 16);
-    }
-    // V: whole token rows, LPT lanes per token.
-    T.vok = 0;
+    T.ok = 0;
     for (int n = 0; n < SH::NV; ++n) {
       const int tt = n * SH::TPI + lane / SH::LPT;
       const int vt = v0 + tt;
       const int pid = PAGED ? __shfl(tpid, tt) : 0;
       bool ok = live && vt < u.v_end;
-      const int64_t off = tok_offset(real_token(u, vt), pid, ok);
-      T.v[n] = ld16(vbase + off * SH::ES + (lane % SH::LPT) * 16);
-      T.vok |= static_cast<uint32_t>(ok) << n;
+      const int64_t off = tok_offset(real_token(u, vt), pid, ok) * SH::ES + (lane % SH::LPT) * 16;
+      T.k[n] = ld16(kbase + off);
+      T.v[n] = ld16(vbase + off);
+      T.ok |= static_cast<uint32_t>(ok) << n;
     }
   };
 
@@ -218,11 +216,13 @@ attn_partial_kernel(const AttnParams p) {
     for (int c = 0; c < SH::CB16; ++c) acc[rt][c] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  unsigned char* vt_lds = lds + wave * SH::VTILE;
+  unsigned char* kt_lds = lds + wave * SH::WTILE;
+  unsigned char* vt_lds = kt_lds + SH::KTILE;
 
-  // One tile: V to LDS and S^T = K Q^T from the tile's registers, which are
-  // then refilled with tile `tile + P*kWaves` (so P tiles stay in flight
-  // through the softmax and PV below), then the online softmax and O^T += V^T P^T.
+  // One tile: K and V rows to LDS, after which the tile's registers are
+  // refilled with tile `tile + P*kWaves` (so P tiles stay in flight through
+  // the compute below); then S^T = K Q^T, the online softmax and
+  // O^T += V^T P^T, all operands read back from LDS.
   // Per-unit facts for the mask fast path: the smallest and largest query
   // positions of the unit's real rows.
   const int pos_min = u.S - L;
@@ -241,34 +241,14 @@ attn_partial_kernel(const AttnParams p) {
         needs_mask = needs_mask || !(t1 < p.n_sink || t0 >= pos_max - p.window + 1);
     }
 
-    // Stage V rows in this wave's LDS tile (row tt, 16 B chunk lane%LPT);
-    // rows of tokens that are not real are written as zeros.
+    // Stage the K and V rows in this wave's LDS tiles (row tt, 16 B chunk
+    // lane%LPT); V rows of tokens that are not real are written as zeros.
     for (int n = 0; n < SH::NV; ++n) {
       const int tt = n * SH::TPI + lane / SH::LPT;
       u32x4 x = T.v[n];
-      if (!full) x = ((T.vok >> n) & 1u) ? x : u32x4{0, 0, 0, 0};
+      if (!full) x = ((T.ok >> n) & 1u) ? x : u32x4{0, 0, 0, 0};
+      *reinterpret_cast<u32x4*>(kt_lds + tt * SH::KROW + (lane % SH::LPT) * 16) = T.k[n];
       *reinterpret_cast<u32x4*>(vt_lds + tt * SH::VROW + (lane % SH::LPT) * 16) = x;
-    }
-
-    // S^T = K Q^T.
-    f32x4 sacc[NT][2];
-    for (int tb = 0; tb < 2; ++tb) {
-      for (int rt = 0; rt < NT; ++rt) {
-        f32x4 sv = f32x4{0.f, 0.f, 0.f, 0.f};
-        for (int cb = 0; cb < SH::KCB; ++cb) {
-          const u32x4 kk = T.k[tb * SH::KCB + cb];
-          const u32x4 qq = qreg[rt][cb];
-          if constexpr (BF16) {
-            sv = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kk),
-                                                         __builtin_bit_cast(bf16x8, qq), sv, 0, 0, 0);
-          } else {
-            for (int j = 0; j < 4; ++j)
-              sv = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kk[j]),
-                                                         __uint_as_float(qq[j]), sv, 0, 0, 0);
-          }
-        }
-        sacc[rt][tb] = sv;
-      }
     }
 
     // The tile's registers are free: refill them P tiles ahead.  Page ids
@@ -279,6 +259,31 @@ attn_partial_kernel(const AttnParams p) {
       const int pid_far = load_pid(ahead + P * kWaves);
       load_tile(T, ahead, pid_slot);
       pid_slot = pid_far;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+    // S^T = K Q^T.  A operand from LDS: lane = token (l16) of block tb,
+    // channel chunk grp of block cb.
+    f32x4 sacc[NT][2];
+    for (int tb = 0; tb < 2; ++tb) {
+      for (int rt = 0; rt < NT; ++rt) sacc[rt][tb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const unsigned char* krow = kt_lds + (tb * 16 + l16) * SH::KROW + grp * 16;
+      for (int cb = 0; cb < SH::KCB; ++cb) {
+        const u32x4 kk = *reinterpret_cast<const u32x4*>(krow + cb * 64);
+        for (int rt = 0; rt < NT; ++rt) {
+          const u32x4 qq = qreg[rt][cb];
+          if constexpr (BF16) {
+            sacc[rt][tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, kk), __builtin_bit_cast(bf16x8, qq), sacc[rt][tb], 0, 0, 0);
+          } else {
+            for (int j = 0; j < 4; ++j)
+              sacc[rt][tb] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                  __uint_as_float(kk[j]), __uint_as_float(qq[j]), sacc[rt][tb], 0, 0, 0);
+          }
+        }
+      }
     }
 
     // Scale into the log2 domain; mask only where some key is not visible.
@@ -485,49 +490,57 @@ attn_partial_kernel(const AttnParams p) {
 // ---------------------------------------------------------------------------
 // Host-side dispatch over the compiled instances.
 
-template <int D, bool BF16, int NT, int P>
+template <int D, bool BF16, int NT, int P, int OCC>
 static hipError_t launch_p(const AttnParams& p, bool paged, int64_t n_blocks, hipStream_t s) {
   dim3 grid(static_cast<uint32_t>(n_blocks)), block(kWaves * 64);
   if (paged)
-    hipLaunchKernelGGL((attn_partial_kernel<D, BF16, NT, true, P>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((attn_partial_kernel<D, BF16, NT, true, P, OCC>), grid, block, 0, s, p);
   else
-    hipLaunchKernelGGL((attn_partial_kernel<D, BF16, NT, false, P>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((attn_partial_kernel<D, BF16, NT, false, P, OCC>), grid, block, 0, s, p);
   return hipGetLastError();
 }
 
+// Instances: tiles in flight per wave (depth) x waves per SIMD (occupancy).
+// Two waves per SIMD fit the register file with one tile in flight and up to
+// two row tiles; deeper rings and more row tiles run one wave per SIMD.
 template <int D, bool BF16, int NT>
-static hipError_t launch_nt(const AttnParams& p, bool paged, int depth, int64_t n_blocks,
-                            hipStream_t s) {
+static hipError_t launch_nt(const AttnParams& p, bool paged, int depth, int occ,
+                            int64_t n_blocks, hipStream_t s) {
   if constexpr (BF16) {
-    if (depth <= 1) return launch_p<D, BF16, NT, 1>(p, paged, n_blocks, s);
-    if (depth == 2) return launch_p<D, BF16, NT, 2>(p, paged, n_blocks, s);
-    return launch_p<D, BF16, NT, 3>(p, paged, n_blocks, s);
+    if (depth <= 1) {
+      if constexpr (NT <= 2)
+        if (occ >= 2) return launch_p<D, BF16, NT, 1, 2>(p, paged, n_blocks, s);
+      return launch_p<D, BF16, NT, 1, 1>(p, paged, n_blocks, s);
+    }
+    if (depth == 2) return launch_p<D, BF16, NT, 2, 1>(p, paged, n_blocks, s);
+    return launch_p<D, BF16, NT, 3, 1>(p, paged, n_blocks, s);
   } else {
     (void)depth;  // fp32 serves small problems: one tile in flight
-    return launch_p<D, BF16, NT, 1>(p, paged, n_blocks, s);
+    (void)occ;
+    return launch_p<D, BF16, NT, 1, 1>(p, paged, n_blocks, s);
   }
 }
 
 template <int D, bool BF16>
-static hipError_t launch_d(const AttnParams& p, int NT, bool paged, int depth, int64_t n_blocks,
-                           hipStream_t s) {
+static hipError_t launch_d(const AttnParams& p, int NT, bool paged, int depth, int occ,
+                           int64_t n_blocks, hipStream_t s) {
   switch (NT) {
-    case 1: return launch_nt<D, BF16, 1>(p, paged, depth, n_blocks, s);
-    case 2: return launch_nt<D, BF16, 2>(p, paged, depth, n_blocks, s);
-    case 3: return launch_nt<D, BF16, 3>(p, paged, depth, n_blocks, s);
-    case 4: return launch_nt<D, BF16, 4>(p, paged, depth, n_blocks, s);
+    case 1: return launch_nt<D, BF16, 1>(p, paged, depth, occ, n_blocks, s);
+    case 2: return launch_nt<D, BF16, 2>(p, paged, depth, occ, n_blocks, s);
+    case 3: return launch_nt<D, BF16, 3>(p, paged, depth, occ, n_blocks, s);
+    case 4: return launch_nt<D, BF16, 4>(p, paged, depth, occ, n_blocks, s);
   }
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_attn_partial(const AttnParams& p, int head_dim, bool bf16, int NT, bool paged,
-                               int depth, int64_t n_blocks, hipStream_t s) {
+                               int depth, int occ, int64_t n_blocks, hipStream_t s) {
   if (n_blocks <= 0) return hipSuccess;
   if (head_dim == 128)
-    return bf16 ? launch_d<128, true>(p, NT, paged, depth, n_blocks, s)
-                : launch_d<128, false>(p, NT, paged, depth, n_blocks, s);
-  return bf16 ? launch_d<64, true>(p, NT, paged, depth, n_blocks, s)
-              : launch_d<64, false>(p, NT, paged, depth, n_blocks, s);
+    return bf16 ? launch_d<128, true>(p, NT, paged, depth, occ, n_blocks, s)
+                : launch_d<128, false>(p, NT, paged, depth, occ, n_blocks, s);
+  return bf16 ? launch_d<64, true>(p, NT, paged, depth, occ, n_blocks, s)
+              : launch_d<64, false>(p, NT, paged, depth, occ, n_blocks, s);
 }
 
 }  // namespace md

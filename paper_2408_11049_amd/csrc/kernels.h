@@ -32,8 +32,10 @@ struct AttnParams {
 };
 
 // depth: K/V tiles each wave keeps in flight (1..3; bf16 instances).
+// occ: waves per SIMD the instance is compiled for (2 only with depth 1 and
+// NT <= 2; otherwise 1).
 hipError_t launch_attn_partial(const AttnParams& p, int head_dim, bool bf16, int NT, bool paged,
-                               int depth, int64_t n_blocks, hipStream_t s);
+                               int depth, int occ, int64_t n_blocks, hipStream_t s);
 
 hipError_t launch_merge_lse(int n_parts, int64_t n_rows, int head_dim, bool out_bf16,
                             const float* o_parts, const float* lse_parts, void* o, float* lse,
