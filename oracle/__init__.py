@@ -17,7 +17,7 @@ import numpy as np
 from . import build as _build
 
 F32, BF16 = 0, 1
-VERIFY, DRAFT = 0, 1
+VERIFY, DRAFT, INDEXED = 0, 1, 2
 
 _lib = None
 
@@ -32,6 +32,10 @@ def open_library(path):
                                      i32, i32, vp, vp, vp, i32, i32]
     lib.oracle_merge_lse.restype = i32
     lib.oracle_merge_lse.argtypes = [i32, i64, i32, vp, vp, vp, vp]
+    lib.oracle_attention_indexed.restype = i32
+    lib.oracle_attention_indexed.argtypes = [i32, i32, i32, i32, i32, i32, dbl, vp, vp, vp, i64,
+                                             i64, i64, i32, vp, i32, vp, vp, vp, i32, vp, vp,
+                                             vp, i32, i32]
     return lib
 
 
@@ -97,6 +101,52 @@ def attention(mode, q, k, v, kv_lens, *, n_sink=0, window=1, scale=None, page_ta
                               int(probs_len or 0), int(nthreads))
     if rc != 0:
         raise ValueError("oracle_attention rejected its arguments")
+    return (o, lse, probs) if want_probs else (o, lse)
+
+
+def indexed(q, k, v, kv_lens, idx, idx_len, *, scale=None, page_table=None, want_probs=False,
+            probs_len=None, nthreads=None, lib=None):
+    """Draft attention over a listed static cache (fp64).
+
+    idx [B, Hkv, idx_stride] int32 prompt positions (any order, unique); only
+    the first idx_len[b] entries of sequence b count and only positions in
+    [0, S_b - q_len); the q_len speculated positions are always included,
+    causally.  Other arguments as attention()."""
+    lib = lib or _load()
+    q, dt = _raw(q)
+    k, dtk = _raw(k)
+    v, dtv = _raw(v)
+    if not (dt == dtk == dtv):
+        raise TypeError("q, k and v must share a dtype")
+    B, q_len, Hq, d = q.shape
+    Hkv = k.shape[2]
+    kv_lens = np.ascontiguousarray(kv_lens, dtype=np.int32)
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    idx_len = np.ascontiguousarray(idx_len, dtype=np.int32)
+    if idx.ndim != 3 or idx.shape[:2] != (B, Hkv) or idx_len.shape != (B,):
+        raise ValueError("idx must be [B, Hkv, stride] and idx_len [B]")
+    page_size, max_pages, pt = 0, 0, None
+    if page_table is not None:
+        pt = np.ascontiguousarray(page_table, dtype=np.int32)
+        page_size, max_pages = k.shape[1], pt.shape[1]
+    s_blk, s_tok, s_head = k.shape[1] * Hkv * d, Hkv * d, d
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    o = np.zeros((B, q_len, Hq, d), dtype=np.float64)
+    lse = np.zeros((B, q_len, Hq), dtype=np.float64)
+    probs = None
+    if want_probs:
+        probs_len = int(probs_len if probs_len is not None else (kv_lens.max() if B else 0))
+        probs = np.zeros((B, q_len, Hq, probs_len), dtype=np.float64)
+    if nthreads is None:
+        nthreads = os.cpu_count() or 1
+    rc = lib.oracle_attention_indexed(B, q_len, Hq, Hkv, d, dt, float(scale), _ptr(q), _ptr(k),
+                                      _ptr(v), s_blk, s_tok, s_head, page_size, _ptr(pt),
+                                      max_pages, _ptr(kv_lens), _ptr(idx), _ptr(idx_len),
+                                      idx.shape[2], _ptr(o), _ptr(lse), _ptr(probs),
+                                      int(probs_len or 0), int(nthreads))
+    if rc != 0:
+        raise ValueError("oracle_attention_indexed rejected its arguments")
     return (o, lse, probs) if want_probs else (o, lse)
 
 

@@ -13,6 +13,10 @@
  *   - Drafting with a StreamingLLM-style sparse KV (Sec. 4.1, Eq. 3 budget K;
  *     Sec. 5.1 setup, StreamingLLM-style draft cache): each query attends to
  *     the sink tokens plus a window of its most recent tokens.
+ *   - Drafting with a static compressed cache given as token positions
+ *     (SnapKV-style selection made at prefill; Sec. 4.4, Sec. 5.2): each
+ *     query attends to the listed prompt positions plus the speculated
+ *     tokens, causally.
  *   - The log-sum-exp merge of attention computed over disjoint key sets
  *     (the Flash-Decoding split-KV identity named in Sec. 2).
  *
@@ -22,6 +26,9 @@
  *     sits at position p = kv_lens[b] - q_len + i (bottom-right alignment).
  *   - Draft key set for the query at position p:
  *       { j <= p : j < n_sink  or  j >= p - window + 1 }.
+ *   - Indexed draft key set of sequence b, kv head hk: the listed positions
+ *     idx[b][hk][0 .. idx_len[b]) that lie in [0, S - q_len), taken as a set,
+ *     plus the speculated positions S - q_len .. p.
  *   - GQA: query head h reads kv head h / (Hq / Hkv).
  *   - Scale: the caller's scale (default 1/sqrt(d)); lse in natural log.
  *
@@ -42,6 +49,7 @@
 #define ORACLE_BF16 1
 #define ORACLE_VERIFY 0
 #define ORACLE_DRAFT 1
+#define ORACLE_INDEXED 2
 
 /* A bf16 value is the upper 16 bits of the fp32 with the same sign,
  * exponent and leading 7 mantissa bits, so widening is exact. */
@@ -67,6 +75,9 @@ typedef struct {
   double* lse;
   double* probs;
   int probs_len;
+  const int32_t* idx;     /* indexed mode: [B][Hkv][idx_stride] positions */
+  const int32_t* idx_len; /* indexed mode: [B] list lengths */
+  int idx_stride;
   int nthreads, tid;
   int status;
 } job_t;
@@ -84,10 +95,12 @@ static int64_t kv_offset(const job_t* a, int b, int j, int hk) {
   return blk * a->s_blk + tok * a->s_tok + (int64_t)hk * a->s_head;
 }
 
-/* Is key j visible to the query at position p? */
-static int visible(const job_t* a, int j, int p) {
+/* Is key j visible to the query at position p?  member: indexed mode only,
+ * member[j] != 0 iff j is a listed prompt position of this (b, kv head). */
+static int visible(const job_t* a, int j, int p, int S, const unsigned char* member) {
   if (j > p) return 0;
   if (a->mode == ORACLE_VERIFY) return 1;
+  if (a->mode == ORACLE_INDEXED) return j >= S - a->q_len || member[j];
   return j < a->n_sink || j >= p - a->window + 1;
 }
 
@@ -100,10 +113,12 @@ static void* run_rows(void* arg) {
     if (a->kv_lens[b] > S_cap) S_cap = a->kv_lens[b];
   double* score = (double*)malloc(sizeof(double) * (size_t)(S_cap > 0 ? S_cap : 1));
   double* acc = (double*)malloc(sizeof(double) * (size_t)a->d);
-  if (!score || !acc) {
+  unsigned char* member = (unsigned char*)malloc((size_t)(S_cap > 0 ? S_cap : 1));
+  if (!score || !acc || !member) {
     a->status = -1;
     free(score);
     free(acc);
+    free(member);
     return NULL;
   }
   for (int64_t row = a->tid; row < n_rows; row += a->nthreads) {
@@ -115,11 +130,19 @@ static void* run_rows(void* arg) {
     int S = a->kv_lens[b];
     int p = S - a->q_len + i;
     const int64_t q_off = row * a->d;
+    if (a->mode == ORACLE_INDEXED) {
+      /* The list as a set of prompt positions; anything outside [0, S - q_len) is ignored. */
+      memset(member, 0, (size_t)(S > 0 ? S : 1));
+      const int32_t* list = a->idx + ((int64_t)b * a->Hkv + hk) * a->idx_stride;
+      int n = a->idx_len[b] < a->idx_stride ? a->idx_len[b] : a->idx_stride;
+      for (int t = 0; t < n; ++t)
+        if (list[t] >= 0 && list[t] < S - a->q_len) member[list[t]] = 1;
+    }
 
     /* Pass 1: scores of every visible key, and their maximum. */
     double m = -INFINITY;
     for (int j = 0; j < S; ++j) {
-      if (!visible(a, j, p)) continue;
+      if (!visible(a, j, p, S, member)) continue;
       int64_t k_off = kv_offset(a, b, j, hk);
       double dot = 0.0;
       for (int c = 0; c < a->d; ++c)
@@ -131,7 +154,7 @@ static void* run_rows(void* arg) {
     double Z = 0.0;
     for (int c = 0; c < a->d; ++c) acc[c] = 0.0;
     for (int j = 0; j < S; ++j) {
-      if (!visible(a, j, p)) continue;
+      if (!visible(a, j, p, S, member)) continue;
       double e = exp(score[j] - m);
       Z += e;
       int64_t v_off = kv_offset(a, b, j, hk);
@@ -143,11 +166,12 @@ static void* run_rows(void* arg) {
       double* pr = a->probs + row * a->probs_len;
       for (int j = 0; j < a->probs_len; ++j) pr[j] = 0.0;
       for (int j = 0; j < S && j < a->probs_len; ++j)
-        if (visible(a, j, p)) pr[j] = exp(score[j] - m) / Z;
+        if (visible(a, j, p, S, member)) pr[j] = exp(score[j] - m) / Z;
     }
   }
   free(score);
   free(acc);
+  free(member);
   return NULL;
 }
 
@@ -162,22 +186,50 @@ static void* run_rows(void* arg) {
  *   probs    NULL, or [B, q_len, Hq, probs_len] explicit softmax rows
  * Returns 0 on success, -1 on a bad argument or allocation failure.
  */
+static int run_all(job_t base);
+
 int oracle_attention(int mode, int B, int q_len, int Hq, int Hkv, int d, int dtype, double scale,
                      const void* q, const void* k, const void* v, int64_t s_blk, int64_t s_tok,
                      int64_t s_head, int page_size, const int32_t* page_table, int max_pages,
                      const int32_t* kv_lens, int n_sink, int window, double* o, double* lse,
                      double* probs, int probs_len, int nthreads) {
-  if (B < 0 || q_len < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || d < 1) return -1;
-  if (dtype != ORACLE_F32 && dtype != ORACLE_BF16) return -1;
   if (mode != ORACLE_VERIFY && mode != ORACLE_DRAFT) return -1;
   if (mode == ORACLE_DRAFT && (n_sink < 0 || window < 1)) return -1;
-  if (page_size < 0 || (page_size > 0 && !page_table)) return -1;
-  if (B == 0) return 0;
-  if (!q || !k || !v || !o || !kv_lens) return -1;
-  if (nthreads < 1) nthreads = 1;
   job_t base = {mode, B, q_len, Hq, Hkv, d, dtype, scale, q, k, v, s_blk, s_tok, s_head,
                 page_size, page_table, max_pages, kv_lens, n_sink, window, o, lse, probs,
-                probs_len, nthreads, 0, 0};
+                probs_len, NULL, NULL, 0, nthreads, 0, 0};
+  return run_all(base);
+}
+
+/*
+ * oracle_attention_indexed: draft attention over a listed static cache.
+ *   idx     [B][Hkv][idx_stride] int32 prompt positions, any order, unique
+ *   idx_len [B] int32, entries beyond it (or idx_stride) are ignored
+ * Other arguments as oracle_attention.
+ */
+int oracle_attention_indexed(int B, int q_len, int Hq, int Hkv, int d, int dtype, double scale,
+                             const void* q, const void* k, const void* v, int64_t s_blk,
+                             int64_t s_tok, int64_t s_head, int page_size,
+                             const int32_t* page_table, int max_pages, const int32_t* kv_lens,
+                             const int32_t* idx, const int32_t* idx_len, int idx_stride,
+                             double* o, double* lse, double* probs, int probs_len, int nthreads) {
+  if (idx_stride < 0 || (B > 0 && idx_stride > 0 && (!idx || !idx_len))) return -1;
+  if (B > 0 && !idx_len) return -1;
+  job_t base = {ORACLE_INDEXED, B, q_len, Hq, Hkv, d, dtype, scale, q, k, v, s_blk, s_tok,
+                s_head, page_size, page_table, max_pages, kv_lens, 0, 1, o, lse, probs,
+                probs_len, idx, idx_len, idx_stride, nthreads, 0, 0};
+  return run_all(base);
+}
+
+static int run_all(job_t base) {
+  const int B = base.B, q_len = base.q_len, Hq = base.Hq, Hkv = base.Hkv, d = base.d;
+  if (B < 0 || q_len < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || d < 1) return -1;
+  if (base.dtype != ORACLE_F32 && base.dtype != ORACLE_BF16) return -1;
+  if (base.page_size < 0 || (base.page_size > 0 && !base.page_table)) return -1;
+  if (B == 0) return 0;
+  if (!base.q || !base.k || !base.v || !base.o || !base.kv_lens) return -1;
+  int nthreads = base.nthreads < 1 ? 1 : base.nthreads;
+  base.nthreads = nthreads;
   job_t* jobs = (job_t*)malloc(sizeof(job_t) * (size_t)nthreads);
   pthread_t* th = (pthread_t*)malloc(sizeof(pthread_t) * (size_t)nthreads);
   if (!jobs || !th) {

@@ -299,6 +299,103 @@ def pin_bf16_decode(lib=None):
     assert lse[0, 0, 0] == 4 * 0.5  # score = scale * sum(1*1) = 4 / sqrt(4)
 
 
+# ----------------------------------------------------------------------------- indexed draft
+
+def _index_lists(rng, B, Hkv, lens, q_len, budget, stride):
+    """Seeded unique prompt positions per (b, kv head), shuffled, padded with -7."""
+    idx = np.full((B, Hkv, stride), -7, dtype=np.int32)
+    n = np.zeros(B, dtype=np.int32)
+    for b in range(B):
+        pool = lens[b] - q_len
+        n[b] = min(budget, pool)
+        for h in range(Hkv):
+            idx[b, h, : n[b]] = rng.choice(pool, size=n[b], replace=False)
+    return idx, n
+
+
+def pin_indexed_full_list_is_verify(lib=None):
+    """Listing every prompt position gives exactly the verify result."""
+    lens = [30, 19]
+    c, q, k, v = host_case(B=2, q_len=3, Hq=4, Hkv=2, d=16, kv_lens=lens, dtype="bf16", seed=31,
+                           S_alloc=30)
+    idx = np.full((2, 2, 40), -1, np.int32)
+    for b, S in enumerate(lens):
+        idx[b, :, : S - 3] = np.arange(S - 3)[::-1]
+    o, l = oracle.indexed(q, k, v, c["kv_lens_np"], idx, np.array(lens, np.int32) - 3, lib=lib)
+    ov, lv = oracle.verify(q, k, v, c["kv_lens_np"], lib=lib)
+    assert np.array_equal(o, ov) and np.array_equal(l, lv)
+
+
+def pin_indexed_streaming_list_is_draft(lib=None):
+    """q_len = 1 and the list [0, n_sink) u [S-W, S-1): exactly the StreamingLLM draft."""
+    S, n_sink, W = 50, 4, 9
+    c, q, k, v = host_case(B=1, q_len=1, Hq=2, Hkv=1, d=8, kv_lens=[S], dtype="f32", seed=32)
+    lst = list(range(n_sink)) + list(range(S - W, S - 1))
+    idx = np.array(lst, np.int32).reshape(1, 1, -1)
+    o, l = oracle.indexed(q, k, v, c["kv_lens_np"], idx, np.array([len(lst)], np.int32), lib=lib)
+    od, ld = oracle.draft(q, k, v, c["kv_lens_np"], n_sink, W, lib=lib)
+    assert np.array_equal(o, od) and np.array_equal(l, ld)
+
+
+def pin_indexed_sdpa(lib=None):
+    """Indexed draft == library SDPA over the explicitly gathered keys of each
+    row: the sorted listed positions, then the speculated positions up to p."""
+    rng = np.random.default_rng(33)
+    lens, q_len = [60, 41], 4
+    c, q, k, v = host_case(B=2, q_len=q_len, Hq=6, Hkv=2, d=16, kv_lens=lens, dtype="bf16",
+                           seed=34, S_alloc=60)
+    idx, n = _index_lists(rng, 2, 2, lens, q_len, budget=13, stride=20)
+    o, l = oracle.indexed(q, k, v, c["kv_lens_np"], idx, n, lib=lib)
+    Q, K, V = f64(q), f64(k), f64(v)
+    for b, S in enumerate(lens):
+        for i in range(q_len):
+            p = S - q_len + i
+            for h in range(6):
+                hk = h // 3
+                keys = sorted(int(x) for x in idx[b, hk, : n[b]]) + list(range(S - q_len, p + 1))
+                qt = torch.from_numpy(Q[b, i, h]).reshape(1, 1, -1)
+                kt = torch.from_numpy(K[b, keys, hk]).unsqueeze(0)
+                vt = torch.from_numpy(V[b, keys, hk]).unsqueeze(0)
+                ot, lt = sdpa_rows(qt, kt, vt, 0.25, torch.ones(1, len(keys), dtype=torch.bool))
+                close(o[b, i, h], ot[0, 0].numpy(), what="indexed O")
+                close(l[b, i, h], lt[0, 0].item(), what="indexed lse")
+
+
+def pin_indexed_ignores_unlisted_and_padding(lib=None):
+    """Unlisted prompt keys may hold NaN; entries past idx_len, negative or at
+    or after S - q_len are ignored; list order does not matter."""
+    rng = np.random.default_rng(35)
+    lens, q_len = [64, 40], 3
+    c, q, k, v = host_case(B=2, q_len=q_len, Hq=2, Hkv=1, d=8, kv_lens=lens, dtype="f32", seed=36,
+                           S_alloc=64)
+    idx, n = _index_lists(rng, 2, 1, lens, q_len, budget=10, stride=16)
+    o0, l0 = oracle.indexed(q, k, v, c["kv_lens_np"], idx, n, lib=lib)
+    k2, v2 = k.copy(), v.copy()
+    for b, S in enumerate(lens):
+        listed = set(int(x) for x in idx[b, 0, : n[b]])
+        for j in range(S - q_len):
+            if j not in listed:
+                k2[b, j] = np.nan
+                v2[b, j] = np.nan
+    idx2 = idx.copy()
+    for b in range(2):
+        idx2[b, 0, : n[b]] = rng.permutation(idx2[b, 0, : n[b]])
+        idx2[b, 0, n[b]:] = [lens[b] - 1, -3, 10 ** 6, 0, 1, 2][: 16 - n[b]] + [0] * max(0, 10 - n[b])
+    extra = np.concatenate([idx2, np.array([[[lens[0] - q_len]], [[lens[1]]]], np.int32)], axis=2)
+    o1, l1 = oracle.indexed(q, k2, v2, c["kv_lens_np"], extra, n, lib=lib)
+    assert np.array_equal(o0, o1) and np.array_equal(l0, l1)
+
+
+def pin_indexed_empty_list(lib=None):
+    """An empty list leaves only the speculated tokens, causally (row 0 sees one key)."""
+    c, q, k, v = host_case(B=1, q_len=3, Hq=2, Hkv=1, d=8, kv_lens=[20], dtype="f32", seed=37)
+    o, l = oracle.indexed(q, k, v, c["kv_lens_np"], np.zeros((1, 1, 4), np.int32),
+                          np.zeros(1, np.int32), lib=lib)
+    V = f64(v)
+    assert np.array_equal(o[0, 0, 0], V[0, 17, 0])  # p = 17 sees only itself
+    assert np.array_equal(o[0, 0, 1], V[0, 17, 0])
+
+
 # ----------------------------------------------------------------------------- merge
 
 def pin_merge_partition(lib=None):
@@ -343,4 +440,6 @@ ALL_PINS = [pin_sdpa_verify, pin_sdpa_verify_scale, pin_mpmath, pin_probs_rows_s
             pin_single_key, pin_equal_keys, pin_causal_invariance,
             pin_draft_equals_verify_when_budget_covers, pin_sdpa_draft, pin_draft_ignores_evicted,
             pin_gqa_equals_repeated_mha, pin_paged_equals_contiguous, pin_bf16_decode,
+            pin_indexed_full_list_is_verify, pin_indexed_streaming_list_is_draft, pin_indexed_sdpa,
+            pin_indexed_ignores_unlisted_and_padding, pin_indexed_empty_list,
             pin_merge_partition, pin_merge_all_empty, pin_merge_shifted]

@@ -32,6 +32,12 @@ MUTANTS = [
     ("bf16 widened wrongly", "[idx]) << 16;", "[idx]) << 15;"),
     ("merge without max shift", "total += exp(l - mx);", "total += exp(l);"),
     ("merge weight unnormalised", "double w = exp(l - lse_r);", "double w = exp(l - mx);"),
+    ("indexed: speculated tokens not visible", "return j >= S - a->q_len || member[j];",
+     "return member[j];"),
+    ("indexed: list entries past idx_len used", "int n = a->idx_len[b] < a->idx_stride ? a->idx_len[b] : a->idx_stride;",
+     "int n = a->idx_stride;"),
+    ("indexed: list ignored (full cache)", "if (a->mode == ORACLE_VERIFY) return 1;",
+     "if (a->mode != ORACLE_DRAFT) return 1;"),
     ("merge keeps empty parts", "if (l == -INFINITY) continue;\n      double w",
      "if (0) continue;\n      double w"),
 ]
