@@ -47,7 +47,7 @@ typedef enum {
 
 typedef enum { MD_F32 = 0, MD_BF16 = 1 } md_dtype;
 
-typedef enum { MD_MODE_VERIFY = 0, MD_MODE_DRAFT = 1 } md_mode;
+typedef enum { MD_MODE_VERIFY = 0, MD_MODE_DRAFT = 1, MD_MODE_DRAFT_INDEXED = 2 } md_mode;
 
 /*
  * One attention call over a batch of B sequences for one layer.
@@ -126,6 +126,26 @@ int md_verify_attn(const md_attn_args* a, void* stream);
 int md_draft_attn(const md_attn_args* a, int32_t n_sink, int32_t window, void* stream);
 
 /*
+ * Draft attention over a static compressed cache given as token positions,
+ * read in place from the full cache: the SnapKV-style drafting the paper
+ * finds best (static KV selection made at prefill, Sec. 4.4; Sec. 5.2, Table
+ * 2), with optional per-sequence budgets (Sec. 4.3).  Query row i of
+ * sequence b (position p) sees the listed positions of its kv head that lie
+ * in [0, S_b - q_len), taken as a set, plus the speculated positions
+ * S_b - q_len .. p.
+ *   idx      device int32 [B, Hkv, idx_stride]: positions, any order, unique
+ *            (a repeated position would be counted twice); entries outside
+ *            [0, S_b - q_len) are skipped
+ *   idx_len  device int32 [B]: entries of sequence b's lists that count
+ *            (clamped to [0, idx_stride])
+ *   idx_stride >= 1, host value: list capacity; sizes the grid
+ * Errors: MD_ERR_INVALID_ARG for NULL idx/idx_len (with B > 0), idx_stride
+ * < 1 or misaligned lists; others as md_verify_attn.
+ */
+int md_draft_attn_indexed(const md_attn_args* a, const int32_t* idx, const int32_t* idx_len,
+                          int32_t idx_stride, void* stream);
+
+/*
  * Log-sum-exp merge of attention computed over disjoint key sets (the
  * split-KV identity of Flash-Decoding, Sec. 2).  Per row r:
  *   lse[r] = ln sum_k exp(lse_parts[k][r]),
@@ -146,13 +166,17 @@ int md_merge_lse(int32_t n_parts, int64_t n_rows, int32_t head_dim, int32_t out_
 
 /*
  * Workspace bytes an attention call with these arguments needs (0 when the
- * call runs as a single pass).  mode is md_mode; n_sink and window are used
- * for MD_MODE_DRAFT only.  Pure host arithmetic on the sizes plus the
+ * call runs as a single pass).  mode is MD_MODE_VERIFY or MD_MODE_DRAFT;
+ * n_sink and window are used for MD_MODE_DRAFT only.  Pure host arithmetic on the sizes plus the
  * current device's compute-unit count (256 if no device is visible);
  * pointers in `a` are not read.  Returns 0 for malformed arguments too:
  * the attention call itself reports those.
  */
 size_t md_workspace_bytes(const md_attn_args* a, int32_t mode, int32_t n_sink, int32_t window);
+
+/* Workspace bytes of md_draft_attn_indexed with lists of capacity idx_stride
+ * (same conventions as md_workspace_bytes). */
+size_t md_workspace_bytes_indexed(const md_attn_args* a, int32_t idx_stride);
 
 /* Static description of a status code; never NULL. */
 const char* md_status_str(int status);

@@ -7,6 +7,7 @@ CPU fallback: if the library is missing, every call raises.
 
     md_verify_attn(q, k, v, kv_lens, ...)          -> (o, lse)
     md_draft_attn(q, k, v, kv_lens, n_sink, window, ...) -> (o, lse)
+    md_draft_attn_indexed(q, k, v, kv_lens, idx, idx_len, ...) -> (o, lse)
     md_merge_lse(o_parts, lse_parts, ...)         -> (o, lse)
     md_workspace_bytes(...)                       -> int
 
@@ -25,9 +26,10 @@ LIB_PATH = os.path.join(_HERE, "libmagicdec.so")
 
 MD_OK, MD_ERR_INVALID_ARG, MD_ERR_UNSUPPORTED, MD_ERR_WORKSPACE, MD_ERR_HIP = range(5)
 MD_F32, MD_BF16 = 0, 1
-MD_MODE_VERIFY, MD_MODE_DRAFT = 0, 1
+MD_MODE_VERIFY, MD_MODE_DRAFT, MD_MODE_DRAFT_INDEXED = 0, 1, 2
 
-EXPORTED = ["md_verify_attn", "md_draft_attn", "md_merge_lse", "md_workspace_bytes",
+EXPORTED = ["md_verify_attn", "md_draft_attn", "md_draft_attn_indexed", "md_merge_lse",
+            "md_workspace_bytes", "md_workspace_bytes_indexed",
             "md_status_str", "md_last_hip_error", "md_attn_args_size",
             "md_bench_stream_read", "md_bench_copy", "md_bench_fill"]
 
@@ -70,6 +72,10 @@ def load_library(path: str = LIB_PATH):
     lib.md_verify_attn.restype = ctypes.c_int
     lib.md_draft_attn.argtypes = [args_p, i32, i32, vp]
     lib.md_draft_attn.restype = ctypes.c_int
+    lib.md_draft_attn_indexed.argtypes = [args_p, vp, vp, i32, vp]
+    lib.md_draft_attn_indexed.restype = ctypes.c_int
+    lib.md_workspace_bytes_indexed.argtypes = [args_p, i32]
+    lib.md_workspace_bytes_indexed.restype = sz
     lib.md_merge_lse.argtypes = [i32, i64, i32, i32, vp, vp, vp, vp, vp]
     lib.md_merge_lse.restype = ctypes.c_int
     lib.md_workspace_bytes.argtypes = [args_p, i32, i32, i32]
@@ -172,7 +178,8 @@ def md_workspace_bytes(q, k, v, kv_lens, *, mode=MD_MODE_VERIFY, n_sink=0, windo
 
 
 def _attention(mode, q, k, v, kv_lens, n_sink, window, *, max_kv_len=None, page_table=None,
-               sm_scale=0.0, out=None, lse=None, return_lse=True, workspace=None, stream=None):
+               sm_scale=0.0, out=None, lse=None, return_lse=True, workspace=None, stream=None,
+               idx=None, idx_len=None):
     import torch
     lib = load_library()
     if kv_lens.dtype != torch.int32:
@@ -183,7 +190,10 @@ def _attention(mode, q, k, v, kv_lens, n_sink, window, *, max_kv_len=None, page_
         lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
     a = make_args(q, k, v, kv_lens, max_kv_len=max_kv_len, page_table=page_table,
                   sm_scale=sm_scale, out=out, lse=lse)
-    need = int(lib.md_workspace_bytes(ctypes.byref(a), mode, n_sink, window))
+    if mode == MD_MODE_DRAFT_INDEXED:
+        need = int(lib.md_workspace_bytes_indexed(ctypes.byref(a), idx.shape[2]))
+    else:
+        need = int(lib.md_workspace_bytes(ctypes.byref(a), mode, n_sink, window))
     if need and workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
     if workspace is not None:
@@ -192,8 +202,10 @@ def _attention(mode, q, k, v, kv_lens, n_sink, window, *, max_kv_len=None, page_
     s = _stream_handle(q, stream)
     if mode == MD_MODE_VERIFY:
         st = lib.md_verify_attn(ctypes.byref(a), s)
-    else:
+    elif mode == MD_MODE_DRAFT:
         st = lib.md_draft_attn(ctypes.byref(a), int(n_sink), int(window), s)
+    else:
+        st = lib.md_draft_attn_indexed(ctypes.byref(a), _ptr(idx), _ptr(idx_len), idx.shape[2], s)
     _check(st)
     return out, lse
 
@@ -206,6 +218,19 @@ def md_verify_attn(q, k, v, kv_lens, **kw):
 def md_draft_attn(q, k, v, kv_lens, n_sink, window, **kw):
     """StreamingLLM-style sparse draft attention (see include/magicdec.h)."""
     return _attention(MD_MODE_DRAFT, q, k, v, kv_lens, n_sink, window, **kw)
+
+
+def md_draft_attn_indexed(q, k, v, kv_lens, idx, idx_len, **kw):
+    """Draft attention over a listed (SnapKV-style) static cache.
+
+    idx [B, Hkv, stride] int32 prompt positions (unique), idx_len [B] int32
+    (see include/magicdec.h)."""
+    import torch
+    if idx.dtype != torch.int32 or idx_len.dtype != torch.int32:
+        raise ValueError("idx and idx_len must be int32")
+    if idx.dim() != 3 or not idx.is_contiguous() or idx.shape[:2] != (q.shape[0], k.shape[2]):
+        raise ValueError("idx must be contiguous [B, Hkv, stride]")
+    return _attention(MD_MODE_DRAFT_INDEXED, q, k, v, kv_lens, 0, 1, idx=idx, idx_len=idx_len, **kw)
 
 
 def md_merge_lse(o_parts, lse_parts, *, out_dtype=None, out=None, lse=None, stream=None):
@@ -231,5 +256,6 @@ def md_merge_lse(o_parts, lse_parts, *, out_dtype=None, out=None, lse=None, stre
 # Short aliases.
 verify_attn = md_verify_attn
 draft_attn = md_draft_attn
+draft_attn_indexed = md_draft_attn_indexed
 merge_lse = md_merge_lse
 workspace_bytes = md_workspace_bytes

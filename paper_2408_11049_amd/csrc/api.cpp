@@ -54,10 +54,16 @@ int occupancy(int NT, int depth, int mode) {
   return (mode == MD_MODE_VERIFY && NT == 2) ? 1 : 2;
 }
 
-int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void* stream) {
+int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void* stream,
+                  const int32_t* idx = nullptr, const int32_t* idx_len = nullptr) {
   int st = validate_attn(a, mode, n_sink, window);
   if (st != MD_OK) return st;
   if (a->num_seqs == 0) return MD_OK;
+  if (mode == MD_MODE_DRAFT_INDEXED) {
+    if (!idx || !idx_len) return MD_ERR_INVALID_ARG;
+    if ((reinterpret_cast<uintptr_t>(idx) & 3u) || (reinterpret_cast<uintptr_t>(idx_len) & 3u))
+      return MD_ERR_INVALID_ARG;
+  }
   const Plan pl = make_plan(a, mode, n_sink, window, device_cu_count());
   const bool bf16 = a->dtype == MD_BF16;
   const bool paged = a->page_size != 0;
@@ -87,6 +93,11 @@ int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void*
   p.mode = mode;
   p.n_sink = mode == MD_MODE_DRAFT ? n_sink : 0;
   p.window = mode == MD_MODE_DRAFT ? window : 1;
+  if (mode == MD_MODE_DRAFT_INDEXED) {
+    p.idx = idx;
+    p.idx_len = idx_len;
+    p.idx_stride = window;
+  }
   p.n_chunks = pl.n_chunks;
   p.chunk_len = pl.chunk_len;
   p.o = a->o;
@@ -142,6 +153,11 @@ int md_draft_attn(const md_attn_args* a, int32_t n_sink, int32_t window, void* s
   return md::run_attention(a, MD_MODE_DRAFT, n_sink, window, stream);
 }
 
+int md_draft_attn_indexed(const md_attn_args* a, const int32_t* idx, const int32_t* idx_len,
+                          int32_t idx_stride, void* stream) {
+  return md::run_attention(a, MD_MODE_DRAFT_INDEXED, 0, idx_stride, stream, idx, idx_len);
+}
+
 int md_merge_lse(int32_t n_parts, int64_t n_rows, int32_t head_dim, int32_t out_dtype,
                  const float* o_parts, const float* lse_parts, void* o, float* lse,
                  void* stream) {
@@ -166,6 +182,16 @@ size_t md_workspace_bytes(const md_attn_args* a, int32_t mode, int32_t n_sink, i
       (a->head_dim != 64 && a->head_dim != 128))
     return 0;
   return md::make_plan(a, mode, n_sink, window, md::device_cu_count()).workspace_bytes;
+}
+
+size_t md_workspace_bytes_indexed(const md_attn_args* a, int32_t idx_stride) {
+  if (!a || idx_stride < 1) return 0;
+  if (a->num_seqs < 0 || a->q_len < 1 || a->num_q_heads < 1 || a->num_kv_heads < 1 ||
+      a->num_q_heads % a->num_kv_heads || a->max_kv_len < a->q_len ||
+      (a->head_dim != 64 && a->head_dim != 128))
+    return 0;
+  return md::make_plan(a, MD_MODE_DRAFT_INDEXED, 0, idx_stride, md::device_cu_count())
+      .workspace_bytes;
 }
 
 const char* md_status_str(int status) {

@@ -78,7 +78,10 @@ __device__ __forceinline__ int real_token(const UnitGeom& u, int v) {
   return v < u.seg0 ? v : v - u.seg0 + u.seg1_start;
 }
 
-template <int D, bool BF16, int NT, bool PAGED, int P, int OCC>
+// IDX: the visible range is a per-(sequence, kv head) list of prompt positions
+// followed by the speculated tokens (the indexed draft); otherwise the causal
+// prefix (verify) or sinks then windows (draft).
+template <int D, bool BF16, int NT, bool PAGED, bool IDX, int P, int OCC>
 __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(OCC)))
 attn_partial_kernel(const AttnParams p) {
   using SH = Shape<D, BF16>;
@@ -108,7 +111,13 @@ attn_partial_kernel(const AttnParams p) {
   int U = u.S;
   u.seg0 = u.S;
   u.seg1_start = 0;
-  if (p.mode == MD_MODE_DRAFT) {
+  if constexpr (IDX) {
+    // The listed prompt positions, then the L speculated tokens.
+    const int nb = min(max(p.idx_len[b], 0), p.idx_stride);
+    u.seg0 = nb;
+    u.seg1_start = u.S - L;
+    U = nb + L;
+  } else if (p.mode == MD_MODE_DRAFT) {
     int lo = u.S - L - p.window + 1;
     if (lo > p.n_sink) {  // sinks, a gap that is never read, then the windows
       u.seg0 = p.n_sink;
@@ -164,20 +173,42 @@ attn_partial_kernel(const AttnParams p) {
               : 0;
   };
 
-  // Page id of the token this lane stands for (lane & 31 of tile `tile`);
-  // -1 past the chunk.  The table row of sequence b always has an entry 0.
-  auto load_pid = [&](int tile) -> int {
-    if (!PAGED) return 0;
+  // Where the token this lane stands for (lane & 31 of tile `tile`) lives:
+  // its position (-1 if it must not be read: past the chunk, an unusable list
+  // entry) and, paged, its page id.  The list row and the table row always
+  // have an entry 0, so every load here is in bounds.
+  const int32_t* idxrow =
+      IDX ? p.idx + (static_cast<int64_t>(b) * p.Hkv + hk) * p.idx_stride : nullptr;
+  struct TokRef {
+    int tok;
+    int pid;
+  };
+  auto load_ref = [&](int tile) -> TokRef {
     const int v = u.v_begin + tile * kTile + (lane & 31);
     const bool ok = tile < n_tiles && v < u.v_end;
-    const int pid = ptab[ok ? (real_token(u, v) >> p.page_shift) : 0];
-    return ok ? pid : -1;
+    int t;
+    bool valid = ok;
+    if constexpr (IDX) {
+      const bool listed = v < u.seg0;
+      const int lt = idxrow[(ok && listed) ? v : 0];
+      t = listed ? lt : v - u.seg0 + u.seg1_start;
+      valid = ok && t >= 0 && (!listed || t < u.S - L);
+    } else {
+      t = real_token(u, v);
+    }
+    int pid = 0;
+    if constexpr (PAGED) {
+      const int raw = ptab[valid ? (t >> p.page_shift) : 0];
+      pid = valid ? raw : -1;
+    }
+    return TokRef{valid ? t : -1, pid};
   };
 
   struct TileRegs {
     u32x4 k[SH::NV];
     u32x4 v[SH::NV];
     uint32_t ok;  // bit n: token row of load n is real (else V is staged as zeros)
+    int tok;      // IDX: position of this lane's tile token (lane & 31), -1 if none
   };
 
   // 16-byte streaming load: every K/V byte is read exactly once, so the
@@ -190,17 +221,26 @@ attn_partial_kernel(const AttnParams p) {
   // cover one whole token row (256 B for bf16, d = 128), TPI rows per
   // instruction -- full-row accesses stream markedly faster from HBM than
   // the 64 B-per-row pattern of the MFMA operand layout.  One address per
-  // token serves both.  tpid: this lane's page id for token lane&31.
-  auto load_tile = [&](TileRegs& T, int tile, int tpid) {
+  // token serves both.  r: where this lane's token (lane & 31) lives.
+  auto load_tile = [&](TileRegs& T, int tile, TokRef r) {
     const int v0 = u.v_begin + tile * kTile;
     const bool live = tile < n_tiles;
     T.ok = 0;
+    T.tok = r.tok;
     for (int n = 0; n < SH::NV; ++n) {
       const int tt = n * SH::TPI + lane / SH::LPT;
       const int vt = v0 + tt;
-      const int pid = PAGED ? __shfl(tpid, tt) : 0;
-      bool ok = live && vt < u.v_end;
-      const int64_t off = tok_offset(real_token(u, vt), pid, ok) * SH::ES + (lane % SH::LPT) * 16;
+      const int pid = PAGED ? __shfl(r.pid, tt) : 0;
+      int t;
+      bool ok;
+      if constexpr (IDX) {
+        t = __shfl(r.tok, tt);
+        ok = t >= 0;
+      } else {
+        t = real_token(u, vt);
+        ok = live && vt < u.v_end;
+      }
+      const int64_t off = tok_offset(t, pid, ok) * SH::ES + (lane % SH::LPT) * 16;
       T.k[n] = ld16(kbase + off);
       T.v[n] = ld16(vbase + off);
       T.ok |= static_cast<uint32_t>(ok) << n;
@@ -229,12 +269,17 @@ attn_partial_kernel(const AttnParams p) {
   const int pos_max = u.S - 1;
   constexpr float kLazy = 8.f;  // log2 headroom before the running max must move
 
-  auto process = [&](TileRegs& T, int tile, int& pid_slot) {
+  auto process = [&](TileRegs& T, int tile, TokRef& ref_slot) {
     const int v0 = u.v_begin + tile * kTile;
+    const int tok_cur = T.tok;
     // Does any key of this tile need masking for any real row?  (Uniform.)
     const bool full = v0 + kTile <= u.v_end;
     bool needs_mask = true;
-    if (full && !(v0 < u.seg0 && v0 + kTile > u.seg0)) {
+    if constexpr (IDX) {
+      // Listed prompt positions precede every query; only the speculated
+      // tokens and unusable entries need the mask.
+      needs_mask = !full || v0 + kTile > u.seg0 || __any(tok_cur < 0);
+    } else if (full && !(v0 < u.seg0 && v0 + kTile > u.seg0)) {
       const int t0 = real_token(u, v0), t1 = t0 + kTile - 1;
       needs_mask = t1 > pos_min;
       if (p.mode == MD_MODE_DRAFT)
@@ -246,7 +291,7 @@ attn_partial_kernel(const AttnParams p) {
     for (int n = 0; n < SH::NV; ++n) {
       const int tt = n * SH::TPI + lane / SH::LPT;
       u32x4 x = T.v[n];
-      if (!full) x = ((T.ok >> n) & 1u) ? x : u32x4{0, 0, 0, 0};
+      if (needs_mask) x = ((T.ok >> n) & 1u) ? x : u32x4{0, 0, 0, 0};
       *reinterpret_cast<u32x4*>(kt_lds + tt * SH::KROW + (lane % SH::LPT) * 16) = T.k[n];
       *reinterpret_cast<u32x4*>(vt_lds + tt * SH::VROW + (lane % SH::LPT) * 16) = x;
     }
@@ -256,9 +301,9 @@ attn_partial_kernel(const AttnParams p) {
     // K/V load that is not already needed.
     {
       const int ahead = tile + P * kWaves;
-      const int pid_far = load_pid(ahead + P * kWaves);
-      load_tile(T, ahead, pid_slot);
-      pid_slot = pid_far;
+      const TokRef far = load_ref(ahead + P * kWaves);
+      load_tile(T, ahead, ref_slot);
+      ref_slot = far;
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -296,12 +341,20 @@ attn_partial_kernel(const AttnParams p) {
       for (int tb = 0; tb < 2; ++tb)
         for (int e = 0; e < 4; ++e) {
           const int vt = v0 + tb * 16 + grp * 4 + e;
-          const int t = real_token(u, vt);
-          const bool tv = vt < u.v_end;
+          int t;
+          bool tv;
+          if constexpr (IDX) {
+            t = __shfl(tok_cur, tb * 16 + grp * 4 + e);
+            tv = t >= 0;
+          } else {
+            t = real_token(u, vt);
+            tv = vt < u.v_end;
+          }
           for (int rt = 0; rt < NT; ++rt) {
             const int pos = row_pos[rt];
             bool vis = tv && t <= pos;
-            if (p.mode == MD_MODE_DRAFT) vis = vis && (t < p.n_sink || t >= pos - p.window + 1);
+            if (!IDX && p.mode == MD_MODE_DRAFT)
+              vis = vis && (t < p.n_sink || t >= pos - p.window + 1);
             x[rt][tb][e] = vis ? sacc[rt][tb][e] * p.scale_log2 : -INFINITY;
           }
         }
@@ -386,22 +439,22 @@ attn_partial_kernel(const AttnParams p) {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   };
 
-  // Prologue: this wave's first P tiles in flight; page ids of the P tiles
-  // after them.
+  // Prologue: this wave's first P tiles in flight; the token locations of
+  // the P tiles after them.
   TileRegs ring[P];
-  int pid_ring[P];
+  TokRef ref_ring[P];
   {
-    int pid0[P];
-    for (int s = 0; s < P; ++s) pid0[s] = load_pid(wave + s * kWaves);
-    for (int s = 0; s < P; ++s) pid_ring[s] = load_pid(wave + (s + P) * kWaves);
-    for (int s = 0; s < P; ++s) load_tile(ring[s], wave + s * kWaves, pid0[s]);
+    TokRef ref0[P];
+    for (int s = 0; s < P; ++s) ref0[s] = load_ref(wave + s * kWaves);
+    for (int s = 0; s < P; ++s) ref_ring[s] = load_ref(wave + (s + P) * kWaves);
+    for (int s = 0; s < P; ++s) load_tile(ring[s], wave + s * kWaves, ref0[s]);
   }
   // Every ring slot is processed unconditionally (a tile past the chunk is
   // fully masked: it leaves m, l and O unchanged), so no slot becomes a
   // conditionally-updated loop-carried value that would force a full wait.
   for (int base = wave; base < n_tiles; base += P * kWaves) {
 #pragma unroll
-    for (int s = 0; s < P; ++s) process(ring[s], base + s * kWaves, pid_ring[s]);
+    for (int s = 0; s < P; ++s) process(ring[s], base + s * kWaves, ref_ring[s]);
   }
 
   // ---- row sums: add the 4 lanes that share a row
@@ -490,57 +543,65 @@ attn_partial_kernel(const AttnParams p) {
 // ---------------------------------------------------------------------------
 // Host-side dispatch over the compiled instances.
 
-template <int D, bool BF16, int NT, int P, int OCC>
+template <int D, bool BF16, int NT, bool IDX, int P, int OCC>
 static hipError_t launch_p(const AttnParams& p, bool paged, int64_t n_blocks, hipStream_t s) {
   dim3 grid(static_cast<uint32_t>(n_blocks)), block(kWaves * 64);
   if (paged)
-    hipLaunchKernelGGL((attn_partial_kernel<D, BF16, NT, true, P, OCC>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((attn_partial_kernel<D, BF16, NT, true, IDX, P, OCC>), grid, block, 0, s, p);
   else
-    hipLaunchKernelGGL((attn_partial_kernel<D, BF16, NT, false, P, OCC>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((attn_partial_kernel<D, BF16, NT, false, IDX, P, OCC>), grid, block, 0, s,
+                       p);
   return hipGetLastError();
 }
 
 // Instances: tiles in flight per wave (depth) x waves per SIMD (occupancy).
 // Two waves per SIMD fit the register file with one tile in flight and up to
-// two row tiles; deeper rings and more row tiles run one wave per SIMD.
-template <int D, bool BF16, int NT>
+// two row tiles; a second tile in flight is built for the bf16 range modes
+// with up to two row tiles; everything else runs one tile, one wave per SIMD.
+template <int D, bool BF16, int NT, bool IDX>
 static hipError_t launch_nt(const AttnParams& p, bool paged, int depth, int occ,
                             int64_t n_blocks, hipStream_t s) {
   if constexpr (BF16) {
-    if (depth <= 1) {
-      if constexpr (NT <= 2)
-        if (occ >= 2) return launch_p<D, BF16, NT, 1, 2>(p, paged, n_blocks, s);
-      return launch_p<D, BF16, NT, 1, 1>(p, paged, n_blocks, s);
-    }
-    if (depth == 2) return launch_p<D, BF16, NT, 2, 1>(p, paged, n_blocks, s);
-    return launch_p<D, BF16, NT, 3, 1>(p, paged, n_blocks, s);
+    if constexpr (!IDX && NT <= 2)
+      if (depth >= 2) return launch_p<D, BF16, NT, IDX, 2, 1>(p, paged, n_blocks, s);
+    if constexpr (NT <= 2)
+      if (occ >= 2) return launch_p<D, BF16, NT, IDX, 1, 2>(p, paged, n_blocks, s);
+    return launch_p<D, BF16, NT, IDX, 1, 1>(p, paged, n_blocks, s);
   } else {
     (void)depth;  // fp32 serves small problems: one tile in flight
     (void)occ;
-    return launch_p<D, BF16, NT, 1, 1>(p, paged, n_blocks, s);
+    return launch_p<D, BF16, NT, IDX, 1, 1>(p, paged, n_blocks, s);
   }
 }
 
-template <int D, bool BF16>
+template <int D, bool BF16, bool IDX>
 static hipError_t launch_d(const AttnParams& p, int NT, bool paged, int depth, int occ,
                            int64_t n_blocks, hipStream_t s) {
   switch (NT) {
-    case 1: return launch_nt<D, BF16, 1>(p, paged, depth, occ, n_blocks, s);
-    case 2: return launch_nt<D, BF16, 2>(p, paged, depth, occ, n_blocks, s);
-    case 3: return launch_nt<D, BF16, 3>(p, paged, depth, occ, n_blocks, s);
-    case 4: return launch_nt<D, BF16, 4>(p, paged, depth, occ, n_blocks, s);
+    case 1: return launch_nt<D, BF16, 1, IDX>(p, paged, depth, occ, n_blocks, s);
+    case 2: return launch_nt<D, BF16, 2, IDX>(p, paged, depth, occ, n_blocks, s);
+    case 3: return launch_nt<D, BF16, 3, IDX>(p, paged, depth, occ, n_blocks, s);
+    case 4: return launch_nt<D, BF16, 4, IDX>(p, paged, depth, occ, n_blocks, s);
   }
   return hipErrorInvalidValue;
+}
+
+template <bool IDX>
+static hipError_t launch_i(const AttnParams& p, int head_dim, bool bf16, int NT, bool paged,
+                           int depth, int occ, int64_t n_blocks, hipStream_t s) {
+  if (head_dim == 128)
+    return bf16 ? launch_d<128, true, IDX>(p, NT, paged, depth, occ, n_blocks, s)
+                : launch_d<128, false, IDX>(p, NT, paged, depth, occ, n_blocks, s);
+  return bf16 ? launch_d<64, true, IDX>(p, NT, paged, depth, occ, n_blocks, s)
+              : launch_d<64, false, IDX>(p, NT, paged, depth, occ, n_blocks, s);
 }
 
 hipError_t launch_attn_partial(const AttnParams& p, int head_dim, bool bf16, int NT, bool paged,
                                int depth, int occ, int64_t n_blocks, hipStream_t s) {
   if (n_blocks <= 0) return hipSuccess;
-  if (head_dim == 128)
-    return bf16 ? launch_d<128, true>(p, NT, paged, depth, occ, n_blocks, s)
-                : launch_d<128, false>(p, NT, paged, depth, occ, n_blocks, s);
-  return bf16 ? launch_d<64, true>(p, NT, paged, depth, occ, n_blocks, s)
-              : launch_d<64, false>(p, NT, paged, depth, occ, n_blocks, s);
+  if (p.mode == MD_MODE_DRAFT_INDEXED)
+    return launch_i<true>(p, head_dim, bf16, NT, paged, depth, occ, n_blocks, s);
+  return launch_i<false>(p, head_dim, bf16, NT, paged, depth, occ, n_blocks, s);
 }
 
 }  // namespace md

@@ -40,10 +40,12 @@ struct Plan {
 };
 
 // Checks every argument the host can see.  Returns MD_OK or an md_status.
+// mode MD_MODE_DRAFT_INDEXED reads `window` as the list capacity idx_stride.
 int validate_attn(const md_attn_args* a, int mode, int n_sink, int window);
 
 // The decomposition for these sizes on a device with num_cus compute units.
 // Only sizes are read from `a`.  Call after validate_attn succeeded.
+// mode MD_MODE_DRAFT_INDEXED reads `window` as the list capacity idx_stride.
 Plan make_plan(const md_attn_args* a, int mode, int n_sink, int window, int num_cus);
 
 // Compute units of the current device (cached per device); 256 when no

@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "magicdec.h"
+
 namespace md {
 
 // Everything one attention launch needs, passed by value as the kernel
@@ -29,6 +31,9 @@ struct AttnParams {
   float* part_o;              // [n_chunks][n_rows][d] (several chunks)
   float* part_lse;            // [n_chunks][n_rows]
   int64_t n_rows;
+  const int32_t* idx;         // indexed draft: [B, Hkv, idx_stride] prompt positions
+  const int32_t* idx_len;     // indexed draft: [B] list lengths
+  int32_t idx_stride;
 };
 
 // depth: K/V tiles each wave keeps in flight (1..3; bf16 instances).

@@ -18,6 +18,7 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // [S - L - W + 1, S) -- or the whole prefix when that reaches the sinks.
 int64_t visible_bound(int64_t max_kv_len, int L, int mode, int64_t n_sink, int64_t window) {
   if (mode == MD_MODE_VERIFY) return max_kv_len;
+  if (mode == MD_MODE_DRAFT_INDEXED) return window + L;  // list capacity + speculated tokens
   int64_t lo = max_kv_len - L - window + 1;
   if (lo <= n_sink) return max_kv_len;
   return n_sink + (max_kv_len - lo);
@@ -27,8 +28,10 @@ int64_t visible_bound(int64_t max_kv_len, int L, int mode, int64_t n_sink, int64
 
 int validate_attn(const md_attn_args* a, int mode, int n_sink, int window) {
   if (!a) return MD_ERR_INVALID_ARG;
-  if (mode != MD_MODE_VERIFY && mode != MD_MODE_DRAFT) return MD_ERR_INVALID_ARG;
+  if (mode != MD_MODE_VERIFY && mode != MD_MODE_DRAFT && mode != MD_MODE_DRAFT_INDEXED)
+    return MD_ERR_INVALID_ARG;
   if (mode == MD_MODE_DRAFT && (n_sink < 0 || window < 1)) return MD_ERR_INVALID_ARG;
+  if (mode == MD_MODE_DRAFT_INDEXED && window < 1) return MD_ERR_INVALID_ARG;
   if (a->num_seqs < 0) return MD_ERR_INVALID_ARG;
   if (a->q_len < 1 || a->q_len > 16) return MD_ERR_INVALID_ARG;
   if (a->num_q_heads < 1 || a->num_kv_heads < 1) return MD_ERR_INVALID_ARG;

@@ -32,6 +32,35 @@ def run_gpu(mode, c, n_sink=0, window=1, max_kv_len=None, poison=True):
     return o.float().cpu().numpy().astype(np.float64), l.cpu().numpy().astype(np.float64)
 
 
+def index_lists(B, Hkv, lens, q_len, budget, seed, device):
+    """Seeded unique prompt positions per (sequence, kv head) (a synthetic
+    stand-in for a SnapKV selection), sorted; budget capped by the prompt."""
+    g = torch.Generator(device="cpu")
+    g.manual_seed(seed)
+    idx = np.zeros((B, Hkv, budget), np.int32)
+    n = np.zeros(B, np.int32)
+    for b in range(B):
+        pool = int(lens[b]) - q_len
+        n[b] = min(budget, pool)
+        for h in range(Hkv):
+            idx[b, h, : n[b]] = np.sort(torch.randperm(pool, generator=g)[: n[b]].numpy())
+    return idx, n
+
+
+def run_gpu_indexed(c, budget, seed):
+    idx, n = index_lists(c["B"], c["Hkv"], c["kv_lens_np"], c["q"].shape[1], budget, seed,
+                         c["q"].device)
+    out = torch.full_like(c["q"], float("nan"))
+    lse = torch.full(c["q"].shape[:3], float("nan"), dtype=torch.float32, device=c["q"].device)
+    o, l = md.md_draft_attn_indexed(c["q"], c["k"], c["v"], c["kv_lens"],
+                                    torch.from_numpy(idx).to(c["q"].device),
+                                    torch.from_numpy(n).to(c["q"].device),
+                                    max_kv_len=c["max_kv_len"], page_table=c["page_table"],
+                                    out=out, lse=lse)
+    torch.cuda.synchronize()
+    return (o.float().cpu().numpy().astype(np.float64), l.cpu().numpy().astype(np.float64), idx, n)
+
+
 def run_oracle(mode, c, n_sink=0, window=1):
     q, k, v = wl.to_host_bits(c["q"]), wl.to_host_bits(c["k"]), wl.to_host_bits(c["v"])
     return oracle.attention(mode, q, k, v, c["kv_lens_np"], n_sink=n_sink, window=window,

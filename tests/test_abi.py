@@ -121,6 +121,27 @@ def test_verify_rejects(lib, name, over, want):
     assert lib.md_draft_attn(ctypes.byref(good_args(**over)), 4, 16, None) == want
 
 
+def test_indexed_rejects(lib):
+    a = good_args()
+    assert lib.md_draft_attn_indexed(ctypes.byref(a), None, FAKE, 8, None) == md.MD_ERR_INVALID_ARG
+    assert lib.md_draft_attn_indexed(ctypes.byref(a), FAKE, None, 8, None) == md.MD_ERR_INVALID_ARG
+    assert lib.md_draft_attn_indexed(ctypes.byref(a), FAKE, FAKE, 0, None) == md.MD_ERR_INVALID_ARG
+    assert lib.md_draft_attn_indexed(ctypes.byref(a), FAKE + 2, FAKE, 8, None) == md.MD_ERR_INVALID_ARG
+    assert lib.md_draft_attn_indexed(ctypes.byref(good_args(q_len=0)), FAKE, FAKE, 8, None) == \
+        md.MD_ERR_INVALID_ARG
+    assert lib.md_workspace_bytes_indexed(ctypes.byref(a), 0) == 0
+    e = good_args(num_seqs=0, q=None, k=None, v=None, o=None, kv_lens=None)
+    assert lib.md_draft_attn_indexed(ctypes.byref(e), None, None, 8, None) == md.MD_OK
+
+
+def test_indexed_workspace_tracks_list_capacity(lib):
+    a = good_args(num_seqs=1, num_kv_heads=1, num_q_heads=4, max_kv_len=1 << 17,
+                  kv_stride_tok=128, kv_stride_blk=(1 << 17) * 128)
+    small = lib.md_workspace_bytes_indexed(ctypes.byref(a), 1000)
+    big = lib.md_workspace_bytes_indexed(ctypes.byref(a), 60000)
+    assert small == 0 and big > 0
+
+
 def test_null_args(lib):
     assert lib.md_verify_attn(None, None) == md.MD_ERR_INVALID_ARG
     assert lib.md_draft_attn(None, 1, 1, None) == md.MD_ERR_INVALID_ARG

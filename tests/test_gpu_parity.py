@@ -17,7 +17,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_util import TOL, compare, run_gpu, run_oracle, sample_units, say, unit_rows
+from gpu_util import TOL, compare, run_gpu, run_gpu_indexed, run_oracle, sample_units, say, unit_rows
 from paper_2408_11049_amd import workloads as wl
 
 pytestmark = pytest.mark.gpu
@@ -60,6 +60,74 @@ def test_small_against_oracle(case, mode):
     compare(go, gl, ro, rl, dtype, f"{name}/{'verify' if mode == 0 else 'draft'}")
 
 
+# name, B, q_len, Hq, Hkv, d, kv_lens, dtype, page_size, budget, stride
+INDEXED = [
+    ("idx_bf16_d128_paged", 3, 4, 8, 2, 128, [900, 300, 1500], "bf16", 16, 257, 300),
+    ("idx_bf16_rows20_contig", 2, 5, 8, 2, 128, [700, 2100], "bf16", 0, 400, 512),
+    ("idx_f32_d64", 2, 3, 4, 1, 64, [200, 90], "f32", 0, 50, 64),
+    ("idx_bf16_split", 1, 4, 8, 1, 128, [9000], "bf16", 16, 2049, 2049),
+    ("idx_bf16_rows40", 2, 5, 16, 2, 128, [600, 1200], "bf16", 0, 129, 160),
+    ("idx_bf16_budget_zero", 2, 4, 4, 2, 64, [50, 80], "bf16", 0, 0, 8),
+    ("idx_bf16_page1_q1", 2, 1, 4, 4, 64, [70, 33], "bf16", 1, 20, 24),
+]
+
+
+def _lists(rng, B, Hkv, lens, q_len, budget, stride, junk=True):
+    """Unique prompt positions per (b, kv head), shuffled; per-sequence budgets;
+    entries past idx_len hold positions that must be ignored."""
+    idx = np.zeros((B, Hkv, stride), np.int32)
+    n = np.zeros(B, np.int32)
+    for b in range(B):
+        pool = lens[b] - q_len
+        n[b] = min(budget - (b % 2) * (budget // 3), pool, stride)  # heterogeneous budgets
+        for h in range(Hkv):
+            idx[b, h, : n[b]] = rng.choice(pool, size=n[b], replace=False)
+            if junk:
+                idx[b, h, n[b]:] = rng.integers(-5, lens[b] + 5, size=stride - n[b])
+    return idx, n
+
+
+@pytest.mark.parametrize("case", INDEXED, ids=[s[0] for s in INDEXED])
+def test_indexed_against_oracle(case):
+    import paper_2408_11049_amd as md
+    name, B, L, Hq, Hkv, d, lens, dtype, ps, budget, stride = case
+    say(f"[parity] {name} indexed B={B} L={L} Hq={Hq} Hkv={Hkv} d={d} lens={lens} {dtype} "
+        f"page={ps} budget={budget} stride={stride}")
+    c = wl.make_case(B=B, q_len=L, Hq=Hq, Hkv=Hkv, d=d, kv_lens=lens, dtype=dtype, page_size=ps,
+                     seed=zlib.crc32(name.encode()) % 1000, device=DEV,
+                     S_alloc=None if ps else max(lens) + 5)
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    idx, n = _lists(rng, B, Hkv, lens, L, budget, stride)
+    # Unlisted prompt keys are poisoned: a correct kernel never reads them.
+    listed = [[set(int(x) for x in idx[b, h, : n[b]]) for h in range(Hkv)] for b in range(B)]
+    out = torch.full_like(c["q"], float("nan"))
+    lse = torch.full(c["q"].shape[:3], float("nan"), device=DEV)
+    o, l = md.md_draft_attn_indexed(c["q"], c["k"], c["v"], c["kv_lens"],
+                                    torch.from_numpy(idx).to(DEV), torch.from_numpy(n).to(DEV),
+                                    max_kv_len=c["max_kv_len"], page_table=c["page_table"],
+                                    out=out, lse=lse)
+    torch.cuda.synchronize()
+    go, gl = o.float().cpu().numpy().astype(np.float64), l.cpu().numpy().astype(np.float64)
+    q, k, v = wl.to_host_bits(c["q"]), wl.to_host_bits(c["k"]), wl.to_host_bits(c["v"])
+    ro, rl = oracle.indexed(q, k, v, c["kv_lens_np"], idx, n, page_table=c["page_table_np"])
+    compare(go, gl, ro, rl, dtype, f"{name}/indexed")
+    # Poison every unlisted prompt key on the device and run again: identical bits.
+    if ps == 0:
+        k2, v2 = c["k"].clone(), c["v"].clone()
+        for b in range(B):
+            for h in range(Hkv):
+                drop = [j for j in range(lens[b] - L) if j not in listed[b][h]]
+                if drop:
+                    dj = torch.tensor(drop, device=DEV)
+                    k2[b, dj, h] = float("nan")
+                    v2[b, dj, h] = float("nan")
+        o2, l2 = md.md_draft_attn_indexed(c["q"], k2, v2, c["kv_lens"],
+                                          torch.from_numpy(idx).to(DEV),
+                                          torch.from_numpy(n).to(DEV), max_kv_len=c["max_kv_len"])
+        torch.cuda.synchronize()
+        assert torch.equal(o2, o) and torch.equal(l2, l), "an unlisted key was read"
+
+
 def test_empty_batch():
     c = wl.make_case(B=0, q_len=4, Hq=8, Hkv=2, d=128, kv_lens=[], dtype="bf16", device=DEV)
     import paper_2408_11049_amd as md
@@ -82,20 +150,27 @@ def test_full_size_sampled(name):
     G = w.Hq // w.Hkv
     units = sample_units(c, 6, seed=w.seed_base)
     try:
-        for mode, L in [(oracle.VERIFY, w.q_len), (oracle.DRAFT, w.q_len), (oracle.DRAFT, 1)]:
+        for mode, L in [(oracle.VERIFY, w.q_len), (oracle.DRAFT, w.q_len), (oracle.DRAFT, 1),
+                        (oracle.INDEXED, w.q_len)]:
             cc = c
             if L != w.q_len:  # the real one-token draft step
                 cc = dict(c)
                 cc["q"] = c["q"][:, :1].contiguous()
                 cc["q_len"] = 1
-            go, gl = run_gpu(mode, cc, w.n_sink, w.window)
+            if mode == oracle.INDEXED:  # SnapKV-sized budget (2049) of random prompt positions
+                go, gl, idx, n = run_gpu_indexed(cc, budget=2049, seed=w.seed_base)
+            else:
+                go, gl = run_gpu(mode, cc, w.n_sink, w.window)
             assert not np.isnan(go).any() and not np.isnan(gl).any(), "NaN in a full-size output"
             assert np.isfinite(gl).all()
             for b, hk in units:
                 q, k, v, lens = wl.gather_unit(cc, b, hk)
-                ro, rl = oracle.attention(mode, q, k, v, lens, n_sink=w.n_sink, window=w.window)
+                if mode == oracle.INDEXED:
+                    ro, rl = oracle.indexed(q, k, v, lens, idx[b:b + 1, hk:hk + 1], n[b:b + 1])
+                else:
+                    ro, rl = oracle.attention(mode, q, k, v, lens, n_sink=w.n_sink, window=w.window)
                 compare(unit_rows(go, b, hk, G)[None], unit_rows(gl[..., None], b, hk, G)[None, ..., 0],
-                        ro, rl, w.dtype, f"{name}/{['verify', 'draft'][mode]}/L={L}/unit({b},{hk})")
+                        ro, rl, w.dtype, f"{name}/{['verify', 'draft', 'indexed'][mode]}/L={L}/unit({b},{hk})")
     finally:
         del c
         torch.cuda.empty_cache()
