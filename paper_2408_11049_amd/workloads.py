@@ -192,6 +192,21 @@ def make_workload(w: Workload, device="cpu", *, q_len: Optional[int] = None, nan
                      nan_pad=nan_pad, extra_pages=2 if w.page_size else 0)
 
 
+def index_lists(B, Hkv, lens, q_len, budget, seed):
+    """Seeded stand-in for a SnapKV selection: for every (sequence, kv head),
+    min(budget, S_b - q_len) distinct prompt positions in ascending order.
+    Returns (idx [B, Hkv, budget] int32, idx_len [B] int32)."""
+    g = _gen(seed * 10 + STREAM_PAGE + 100, "cpu")
+    idx = np.zeros((B, Hkv, max(1, budget)), np.int32)
+    n = np.zeros(B, np.int32)
+    for b in range(B):
+        pool = int(lens[b]) - q_len
+        n[b] = max(0, min(budget, pool))
+        for h in range(Hkv):
+            idx[b, h, : n[b]] = np.sort(torch.randperm(pool, generator=g)[: n[b]].numpy())
+    return idx, n
+
+
 def to_host_bits(t: torch.Tensor) -> np.ndarray:
     """Device/host tensor -> numpy array the oracle accepts (float32, or bf16 bit patterns)."""
     t = t.detach().contiguous().cpu()

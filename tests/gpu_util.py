@@ -32,24 +32,8 @@ def run_gpu(mode, c, n_sink=0, window=1, max_kv_len=None, poison=True):
     return o.float().cpu().numpy().astype(np.float64), l.cpu().numpy().astype(np.float64)
 
 
-def index_lists(B, Hkv, lens, q_len, budget, seed, device):
-    """Seeded unique prompt positions per (sequence, kv head) (a synthetic
-    stand-in for a SnapKV selection), sorted; budget capped by the prompt."""
-    g = torch.Generator(device="cpu")
-    g.manual_seed(seed)
-    idx = np.zeros((B, Hkv, budget), np.int32)
-    n = np.zeros(B, np.int32)
-    for b in range(B):
-        pool = int(lens[b]) - q_len
-        n[b] = min(budget, pool)
-        for h in range(Hkv):
-            idx[b, h, : n[b]] = np.sort(torch.randperm(pool, generator=g)[: n[b]].numpy())
-    return idx, n
-
-
 def run_gpu_indexed(c, budget, seed):
-    idx, n = index_lists(c["B"], c["Hkv"], c["kv_lens_np"], c["q"].shape[1], budget, seed,
-                         c["q"].device)
+    idx, n = wl.index_lists(c["B"], c["Hkv"], c["kv_lens_np"], c["q"].shape[1], budget, seed)
     out = torch.full_like(c["q"], float("nan"))
     lse = torch.full(c["q"].shape[:3], float("nan"), dtype=torch.float32, device=c["q"].device)
     o, l = md.md_draft_attn_indexed(c["q"], c["k"], c["v"], c["kv_lens"],
