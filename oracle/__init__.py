@@ -32,6 +32,11 @@ def open_library(path):
                                      i32, i32, vp, vp, vp, i32, i32]
     lib.oracle_merge_lse.restype = i32
     lib.oracle_merge_lse.argtypes = [i32, i64, i32, vp, vp, vp, vp]
+    lib.oracle_snapkv_votes.restype = i32
+    lib.oracle_snapkv_votes.argtypes = [i32, i32, i32, i32, i32, i32, dbl, vp, vp, i64, i64, i64,
+                                        i32, vp, i32, vp, i32, i32, vp]
+    lib.oracle_snapkv_select.restype = i32
+    lib.oracle_snapkv_select.argtypes = [i32, vp, i32, vp, i32, i32, vp, vp]
     lib.oracle_attention_indexed.restype = i32
     lib.oracle_attention_indexed.argtypes = [i32, i32, i32, i32, i32, i32, dbl, vp, vp, vp, i64,
                                              i64, i64, i32, vp, i32, vp, vp, vp, i32, vp, vp,
@@ -148,6 +153,53 @@ def indexed(q, k, v, kv_lens, idx, idx_len, *, scale=None, page_table=None, want
     if rc != 0:
         raise ValueError("oracle_attention_indexed rejected its arguments")
     return (o, lse, probs) if want_probs else (o, lse)
+
+
+def snapkv_votes(q_obs, k, kv_lens, *, pool=5, stride=None, scale=None, page_table=None,
+                 lib=None):
+    """Pooled observation-window votes per (sequence, kv head), fp64.
+    q_obs [B, n_obs, Hq, d]; k as attention(); kv_lens = prompt lengths.
+    Returns [B, Hkv, stride] (stride defaults to max(S_b) - n_obs)."""
+    lib = lib or _load()
+    q_obs, dt = _raw(q_obs)
+    k, dtk = _raw(k)
+    if dt != dtk:
+        raise TypeError("q_obs and k must share a dtype")
+    B, n_obs, Hq, d = q_obs.shape
+    Hkv = k.shape[2]
+    kv_lens = np.ascontiguousarray(kv_lens, dtype=np.int32)
+    if stride is None:
+        stride = max(1, int(kv_lens.max()) - n_obs) if B else 1
+    page_size, max_pages, pt = 0, 0, None
+    if page_table is not None:
+        pt = np.ascontiguousarray(page_table, dtype=np.int32)
+        page_size, max_pages = k.shape[1], pt.shape[1]
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    out = np.zeros((B, Hkv, stride), dtype=np.float64)
+    rc = lib.oracle_snapkv_votes(B, n_obs, Hq, Hkv, d, dt, float(scale), _ptr(q_obs), _ptr(k),
+                                 k.shape[1] * Hkv * d, Hkv * d, d, page_size, _ptr(pt), max_pages,
+                                 _ptr(kv_lens), pool, stride, _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle_snapkv_votes rejected its arguments")
+    return out
+
+
+def snapkv_select(vals, lens, n_obs, budget, lib=None):
+    """Ascending kept positions per row: top (budget - n_obs) prefix positions by
+    value (ties: smaller position), then the observation window.
+    vals [rows, stride] (float64), lens [rows] -> (idx [rows, budget] int32, counts [rows])."""
+    lib = lib or _load()
+    vals = np.ascontiguousarray(vals, dtype=np.float64)
+    rows, stride = vals.shape
+    lens = np.ascontiguousarray(lens, dtype=np.int32)
+    idx = np.full((rows, budget), -1, dtype=np.int32)
+    counts = np.zeros(rows, dtype=np.int32)
+    rc = lib.oracle_snapkv_select(rows, _ptr(vals), stride, _ptr(lens), n_obs, budget, _ptr(idx),
+                                  _ptr(counts))
+    if rc != 0:
+        raise ValueError("oracle_snapkv_select rejected its arguments")
+    return idx, counts
 
 
 def verify(q, k, v, kv_lens, **kw):

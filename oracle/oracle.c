@@ -295,3 +295,130 @@ int oracle_merge_lse(int n_parts, int64_t n_rows, int d, const double* o_parts,
   }
   return 0;
 }
+
+/*
+ * SnapKV-style selection of the static draft cache at prefill (the static
+ * selection the paper finds best, Sec. 4.4, Sec. 5.2; its footnote fixes an
+ * observation window of 32 queries and average pooling with kernel 5).  The
+ * steps restate the published SnapKV algorithm.
+ *
+ * oracle_snapkv_votes: for sequence b (prompt length S = kv_lens[b]) and kv
+ * head hk, with the n_obs observation queries at positions
+ * p_o = S - n_obs + o (o = 0 .. n_obs-1):
+ *   a_{h,o}(j) = softmax over keys j' <= p_o of scale * q[b,o,h,:] . k[b,j',hk,:]
+ *   vote(j)    = sum over the G query heads h of kv head hk and over o of a_{h,o}(j),
+ *                for prefix positions j in [0, S - n_obs)
+ *   pooled(j)  = (1/pool) * sum_{t = j - pool/2}^{j + pool/2} vote(t), with vote = 0
+ *                outside [0, S - n_obs) (zero padding counted in the divisor)
+ *   q_obs  [B, n_obs, Hq, d];  k as in oracle_attention
+ *   pooled [B][Hkv][stride] doubles; entries at j >= S - n_obs are set to 0
+ */
+int oracle_snapkv_votes(int B, int n_obs, int Hq, int Hkv, int d, int dtype, double scale,
+                        const void* q_obs, const void* k, int64_t s_blk, int64_t s_tok,
+                        int64_t s_head, int page_size, const int32_t* page_table, int max_pages,
+                        const int32_t* kv_lens, int pool, int stride, double* pooled) {
+  if (B < 0 || n_obs < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || d < 1 || pool < 1 || pool % 2 == 0)
+    return -1;
+  if (dtype != ORACLE_F32 && dtype != ORACLE_BF16) return -1;
+  if (B == 0) return 0;
+  if (!q_obs || !k || !kv_lens || !pooled || stride < 1) return -1;
+  job_t a = {ORACLE_VERIFY, B, n_obs, Hq, Hkv, d, dtype, scale, q_obs, k, NULL, s_blk, s_tok,
+             s_head, page_size, page_table, max_pages, kv_lens, 0, 1, NULL, NULL, NULL, 0,
+             NULL, NULL, 0, 1, 0, 0};
+  const int G = Hq / Hkv;
+  for (int b = 0; b < B; ++b) {
+    const int S = kv_lens[b];
+    const int n = S - n_obs;
+    if (n > stride) return -1;
+    double* vote = (double*)calloc((size_t)(n > 0 ? n : 1), sizeof(double));
+    double* score = (double*)malloc(sizeof(double) * (size_t)(S > 0 ? S : 1));
+    if (!vote || !score) {
+      free(vote);
+      free(score);
+      return -1;
+    }
+    for (int hk = 0; hk < Hkv; ++hk) {
+      for (int j = 0; j < (n > 0 ? n : 1); ++j) vote[j] = 0.0;
+      for (int g = 0; g < G; ++g) {
+        const int h = hk * G + g;
+        for (int o = 0; o < n_obs; ++o) {
+          const int p = S - n_obs + o;
+          const int64_t q_off = (((int64_t)b * n_obs + o) * Hq + h) * d;
+          double m = -INFINITY;
+          for (int j = 0; j <= p && j < S; ++j) {
+            const int64_t k_off = kv_offset(&a, b, j, hk);
+            double dot = 0.0;
+            for (int c = 0; c < d; ++c)
+              dot += load_elem(q_obs, dtype, q_off + c) * load_elem(k, dtype, k_off + c);
+            score[j] = scale * dot;
+            if (score[j] > m) m = score[j];
+          }
+          double Z = 0.0;
+          for (int j = 0; j <= p && j < S; ++j) Z += exp(score[j] - m);
+          for (int j = 0; j < n; ++j) vote[j] += exp(score[j] - m) / Z;
+        }
+      }
+      double* out = pooled + ((int64_t)b * Hkv + hk) * stride;
+      for (int j = 0; j < stride; ++j) out[j] = 0.0;
+      for (int j = 0; j < n; ++j) {
+        double s = 0.0;
+        for (int t = j - pool / 2; t <= j + pool / 2; ++t)
+          if (t >= 0 && t < n) s += vote[t];
+        out[j] = s / pool;
+      }
+    }
+    free(vote);
+    free(score);
+  }
+  return 0;
+}
+
+/* qsort order for selection: larger value first, then smaller position. */
+static const double* g_sel_vals;
+static int sel_cmp(const void* x, const void* y) {
+  const int i = *(const int*)x, j = *(const int*)y;
+  if (g_sel_vals[i] > g_sel_vals[j]) return -1;
+  if (g_sel_vals[i] < g_sel_vals[j]) return 1;
+  return i < j ? -1 : (i > j);
+}
+static int asc_cmp(const void* x, const void* y) {
+  const int i = *(const int*)x, j = *(const int*)y;
+  return i < j ? -1 : (i > j);
+}
+
+/*
+ * oracle_snapkv_select: per row r (a (sequence, kv head) pair) with
+ * n = lens[r] - n_obs prefix positions, keep the `budget - n_obs` prefix
+ * positions of largest value (ties: the smaller position), all of them if
+ * there are fewer, then the n_obs observation positions [n, lens[r]);
+ * write them ascending to idx[r][0 .. count) and count to counts[r].
+ *   vals [rows][stride] double, idx [rows][budget] int32, counts [rows] int32
+ * Not thread-safe (qsort comparator state).
+ */
+int oracle_snapkv_select(int rows, const double* vals, int stride, const int32_t* lens, int n_obs,
+                         int budget, int32_t* idx, int32_t* counts) {
+  if (rows < 0 || stride < 1 || n_obs < 0 || budget < n_obs || !vals || !lens || !idx || !counts)
+    return -1;
+  int* order = (int*)malloc(sizeof(int) * (size_t)stride);
+  if (!order) return -1;
+  for (int r = 0; r < rows; ++r) {
+    const int S = lens[r];
+    const int n = S - n_obs > 0 ? S - n_obs : 0;
+    if (n > stride) {
+      free(order);
+      return -1;
+    }
+    for (int j = 0; j < n; ++j) order[j] = j;
+    g_sel_vals = vals + (int64_t)r * stride;
+    qsort(order, (size_t)n, sizeof(int), sel_cmp);
+    int keep = budget - n_obs < n ? budget - n_obs : n;
+    qsort(order, (size_t)keep, sizeof(int), asc_cmp);
+    int32_t* out = idx + (int64_t)r * budget;
+    int c = 0;
+    for (int t = 0; t < keep; ++t) out[c++] = order[t];
+    for (int j = n; j < S; ++j) out[c++] = j;
+    counts[r] = c;
+  }
+  free(order);
+  return 0;
+}

@@ -396,6 +396,75 @@ def pin_indexed_empty_list(lib=None):
     assert np.array_equal(o[0, 0, 1], V[0, 17, 0])
 
 
+# ----------------------------------------------------------------------------- SnapKV selection
+
+def pin_snapkv_votes_library(lib=None):
+    """Pooled votes == torch float64: softmax of the observation queries over
+    their causal keys (torch's bottom-right causal bias), summed over the
+    window's queries and the group's query heads, prefix slice, then
+    avg_pool1d(kernel 5, stride 1, padding 2)."""
+    lens, n_obs, G = [40, 29], 6, 2
+    c, q, k, v = host_case(B=2, q_len=n_obs, Hq=4, Hkv=2, d=16, kv_lens=lens, dtype="bf16",
+                           seed=41, S_alloc=40)
+    pooled = oracle.snapkv_votes(q, k, c["kv_lens_np"], pool=5, stride=40, lib=lib)
+    Q, K = f64(q), f64(k)
+    for b, S in enumerate(lens):
+        n = S - n_obs
+        for hk in range(2):
+            vote = torch.zeros(n, dtype=torch.float64)
+            for g in range(G):
+                h = hk * G + g
+                qt = torch.from_numpy(Q[b, :, h])                 # [n_obs, d]
+                kt = torch.from_numpy(K[b, :S, hk])               # [S, d]
+                s = (qt @ kt.T) * 0.25
+                mask = causal_lower_right(n_obs, S)._materialize()
+                a = torch.softmax(s.masked_fill(~mask, float("-inf")), dim=-1)
+                vote += a[:, :n].sum(0)
+            ref = F.avg_pool1d(vote.view(1, 1, -1), kernel_size=5, stride=1, padding=2).view(-1)
+            close(pooled[b, hk, :n], ref.numpy(), what="snapkv pooled votes")
+            assert np.all(pooled[b, hk, n:] == 0.0)
+
+
+def pin_snapkv_single_spike(lib=None):
+    """A key that takes (nearly) all attention spreads 1/5 of its vote to each of
+    its four neighbours and itself: the pooling closed form."""
+    n_obs, S, d = 2, 20, 8
+    q = np.zeros((1, n_obs, 1, d), np.float32)
+    q[..., 0] = 1.0
+    k = np.zeros((1, S, 1, d), np.float32)
+    k[0, 7, 0, 0] = 400.0           # score 400/sqrt(8): every other weight ~ e^-141
+    pooled = oracle.snapkv_votes(q, k, np.array([S], np.int32), pool=5, stride=S, lib=lib)
+    want = np.zeros(S)
+    want[5:10] = n_obs / 5.0
+    close(pooled[0, 0], want, tol=1e-12, what="spike pooling")
+
+
+def pin_snapkv_select_library(lib=None):
+    """Selection == numpy stable argsort of the negated values (ties: smaller
+    position), top budget - n_obs, ascending, then the observation window."""
+    rng = np.random.default_rng(43)
+    rows, stride, n_obs, budget = 5, 300, 8, 40
+    vals = np.round(rng.random((rows, stride)), 2)          # many exact ties
+    lens = np.array([300, 308, 45, 20, 150], np.int32) + 0
+    lens = np.minimum(lens, stride + n_obs)
+    idx, cnt = oracle.snapkv_select(vals, lens, n_obs, budget, lib=lib)
+    for r in range(rows):
+        n = max(0, lens[r] - n_obs)
+        keep = min(budget - n_obs, n)
+        top = np.sort(np.argsort(-vals[r, :n], kind="stable")[:keep])
+        want = np.concatenate([top, np.arange(n, lens[r])]).astype(np.int32)
+        assert cnt[r] == len(want) and np.array_equal(idx[r, : cnt[r]], want), r
+
+
+def pin_snapkv_select_ties_and_short(lib=None):
+    """All-equal values keep the first positions; a prompt shorter than the
+    budget keeps everything."""
+    idx, cnt = oracle.snapkv_select(np.ones((1, 50)), np.array([58], np.int32), 8, 20, lib=lib)
+    assert cnt[0] == 20 and np.array_equal(idx[0], np.r_[np.arange(12), np.arange(50, 58)])
+    idx, cnt = oracle.snapkv_select(np.ones((1, 50)), np.array([15], np.int32), 8, 20, lib=lib)
+    assert cnt[0] == 15 and np.array_equal(idx[0, :15], np.arange(15))
+
+
 # ----------------------------------------------------------------------------- merge
 
 def pin_merge_partition(lib=None):
@@ -442,4 +511,6 @@ ALL_PINS = [pin_sdpa_verify, pin_sdpa_verify_scale, pin_mpmath, pin_probs_rows_s
             pin_gqa_equals_repeated_mha, pin_paged_equals_contiguous, pin_bf16_decode,
             pin_indexed_full_list_is_verify, pin_indexed_streaming_list_is_draft, pin_indexed_sdpa,
             pin_indexed_ignores_unlisted_and_padding, pin_indexed_empty_list,
+            pin_snapkv_votes_library, pin_snapkv_single_spike, pin_snapkv_select_library,
+            pin_snapkv_select_ties_and_short,
             pin_merge_partition, pin_merge_all_empty, pin_merge_shifted]

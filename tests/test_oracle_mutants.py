@@ -38,6 +38,15 @@ MUTANTS = [
      "int n = a->idx_stride;"),
     ("indexed: list ignored (full cache)", "if (a->mode == ORACLE_VERIFY) return 1;",
      "if (a->mode != ORACLE_DRAFT) return 1;"),
+    ("snapkv: pooling divisor off", "out[j] = s / pool;", "out[j] = s / (pool - 1);"),
+    ("snapkv: pooling window shifted", "for (int t = j - pool / 2; t <= j + pool / 2; ++t)",
+     "for (int t = j - pool / 2 + 1; t <= j + pool / 2 + 1; ++t)"),
+    ("snapkv: window queries not causal", "for (int j = 0; j <= p && j < S; ++j)",
+     "for (int j = 0; j < S; ++j)"),
+    ("snapkv: ties to the larger position", "return i < j ? -1 : (i > j);\n}\nstatic int asc_cmp",
+     "return i > j ? -1 : (i < j);\n}\nstatic int asc_cmp"),
+    ("snapkv: observation window dropped", "for (int j = n; j < S; ++j) out[c++] = j;",
+     "for (int j = S; j < S; ++j) out[c++] = j;"),
     ("merge keeps empty parts", "if (l == -INFINITY) continue;\n      double w",
      "if (0) continue;\n      double w"),
 ]
