@@ -178,6 +178,65 @@ size_t md_workspace_bytes(const md_attn_args* a, int32_t mode, int32_t n_sink, i
  * (same conventions as md_workspace_bytes). */
 size_t md_workspace_bytes_indexed(const md_attn_args* a, int32_t idx_stride);
 
+/*
+ * SnapKV-style selection of the static draft cache at prefill: the static
+ * KV selection the paper finds best (Sec. 4.4; budget 2049 in Sec. 5.2),
+ * with its observation window (32 queries) and average pooling (kernel 5).
+ * The steps restate the published SnapKV method:
+ *   vote(j)   = sum over the n_obs observation queries o (positions
+ *               S_b - n_obs + o) and the G query heads of kv head hk of the
+ *               softmax weight of key j, each query's softmax running over
+ *               the keys at or before its own position;
+ *   pooled(j) = mean of vote over j - pool/2 .. j + pool/2, zero outside the
+ *               prefix [0, S_b - n_obs);
+ *   kept      = the budget - n_obs prefix positions of largest pooled vote
+ *               (ties: the smaller position), all of them if fewer, then the
+ *               n_obs observation positions; ascending.
+ * md_snapkv_votes writes vote(j) (before pooling) for j in [0, S_b - n_obs);
+ * md_snapkv_select pools and selects, writing lists md_draft_attn_indexed
+ * reads directly.
+ */
+typedef struct {
+  int32_t num_seqs;       /* B >= 0 */
+  int32_t n_obs;          /* observation queries, >= 1, G * n_obs <= 256 */
+  int32_t num_q_heads, num_kv_heads, head_dim, dtype;  /* as md_attn_args */
+  float sm_scale;         /* <= 0: 1/sqrt(d) */
+  const void* q_obs;      /* [B, n_obs, Hq, d], contiguous, 16-byte aligned */
+  const void* k;          /* as md_attn_args (contiguous or paged) */
+  int64_t kv_stride_blk, kv_stride_tok, kv_stride_head;
+  int32_t page_size, max_pages_per_seq;
+  int64_t num_pages;
+  const int32_t* page_table;
+  const int32_t* prompt_lens;  /* [B], S_b (the prompt includes the window) */
+  int32_t max_prompt_len;      /* host bound on every S_b */
+  float* votes;                /* [B, Hkv, votes_stride] fp32 */
+  int32_t votes_stride;        /* >= max_prompt_len - n_obs */
+  void* workspace;             /* >= md_snapkv_workspace_bytes(), 256-byte aligned */
+  size_t workspace_bytes;
+} md_snapkv_args;
+
+/* Votes of every (sequence, kv head) prefix position.  Errors:
+ * MD_ERR_INVALID_ARG for NULL or misaligned pointers, bad sizes, a votes
+ * stride below max_prompt_len - n_obs, max_prompt_len < n_obs;
+ * MD_ERR_UNSUPPORTED for head_dim not in {64,128} or G * n_obs > 256;
+ * MD_ERR_WORKSPACE; MD_ERR_HIP. */
+int md_snapkv_votes(const md_snapkv_args* a, void* stream);
+size_t md_snapkv_workspace_bytes(const md_snapkv_args* a);
+
+/*
+ * Pool the votes and select, per (sequence, kv head) row r = b * Hkv + hk:
+ *   votes   [B * Hkv][votes_stride] fp32 (only [0, S_b - n_obs) is read)
+ *   idx     [B * Hkv][budget] int32 out: ascending kept positions
+ *   idx_len [B] int32 out: kept count per sequence (min(budget, S_b) when
+ *           S_b >= n_obs)
+ * pool odd >= 1; budget >= n_obs; S_b is clamped to votes_stride + n_obs.
+ * Errors: MD_ERR_INVALID_ARG for bad sizes or NULL/misaligned pointers;
+ * MD_ERR_HIP.
+ */
+int md_snapkv_select(int32_t num_seqs, int32_t num_kv_heads, const float* votes,
+                     int32_t votes_stride, const int32_t* prompt_lens, int32_t n_obs,
+                     int32_t pool, int32_t budget, int32_t* idx, int32_t* idx_len, void* stream);
+
 /* Static description of a status code; never NULL. */
 const char* md_status_str(int status);
 

@@ -29,7 +29,8 @@ MD_F32, MD_BF16 = 0, 1
 MD_MODE_VERIFY, MD_MODE_DRAFT, MD_MODE_DRAFT_INDEXED = 0, 1, 2
 
 EXPORTED = ["md_verify_attn", "md_draft_attn", "md_draft_attn_indexed", "md_merge_lse",
-            "md_workspace_bytes", "md_workspace_bytes_indexed",
+            "md_workspace_bytes", "md_workspace_bytes_indexed", "md_snapkv_votes",
+            "md_snapkv_workspace_bytes", "md_snapkv_select",
             "md_status_str", "md_last_hip_error", "md_attn_args_size",
             "md_bench_stream_read", "md_bench_copy", "md_bench_fill"]
 
@@ -47,6 +48,23 @@ class MdAttnArgs(ctypes.Structure):
         ("num_pages", ctypes.c_int64), ("page_table", ctypes.c_void_p),
         ("kv_lens", ctypes.c_void_p), ("max_kv_len", ctypes.c_int32),
         ("o", ctypes.c_void_p), ("lse", ctypes.c_void_p),
+        ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
+    ]
+
+
+class MdSnapkvArgs(ctypes.Structure):
+    """Mirror of ``md_snapkv_args``."""
+    _fields_ = [
+        ("num_seqs", ctypes.c_int32), ("n_obs", ctypes.c_int32),
+        ("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32), ("sm_scale", ctypes.c_float),
+        ("q_obs", ctypes.c_void_p), ("k", ctypes.c_void_p),
+        ("kv_stride_blk", ctypes.c_int64), ("kv_stride_tok", ctypes.c_int64),
+        ("kv_stride_head", ctypes.c_int64),
+        ("page_size", ctypes.c_int32), ("max_pages_per_seq", ctypes.c_int32),
+        ("num_pages", ctypes.c_int64), ("page_table", ctypes.c_void_p),
+        ("prompt_lens", ctypes.c_void_p), ("max_prompt_len", ctypes.c_int32),
+        ("votes", ctypes.c_void_p), ("votes_stride", ctypes.c_int32),
         ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
     ]
 
@@ -76,6 +94,13 @@ def load_library(path: str = LIB_PATH):
     lib.md_draft_attn_indexed.restype = ctypes.c_int
     lib.md_workspace_bytes_indexed.argtypes = [args_p, i32]
     lib.md_workspace_bytes_indexed.restype = sz
+    sk_p = ctypes.POINTER(MdSnapkvArgs)
+    lib.md_snapkv_votes.argtypes = [sk_p, vp]
+    lib.md_snapkv_votes.restype = ctypes.c_int
+    lib.md_snapkv_workspace_bytes.argtypes = [sk_p]
+    lib.md_snapkv_workspace_bytes.restype = sz
+    lib.md_snapkv_select.argtypes = [i32, i32, vp, i32, vp, i32, i32, i32, vp, vp, vp]
+    lib.md_snapkv_select.restype = ctypes.c_int
     lib.md_merge_lse.argtypes = [i32, i64, i32, i32, vp, vp, vp, vp, vp]
     lib.md_merge_lse.restype = ctypes.c_int
     lib.md_workspace_bytes.argtypes = [args_p, i32, i32, i32]
@@ -231,6 +256,66 @@ def md_draft_attn_indexed(q, k, v, kv_lens, idx, idx_len, **kw):
     if idx.dim() != 3 or not idx.is_contiguous() or idx.shape[:2] != (q.shape[0], k.shape[2]):
         raise ValueError("idx must be contiguous [B, Hkv, stride]")
     return _attention(MD_MODE_DRAFT_INDEXED, q, k, v, kv_lens, 0, 1, idx=idx, idx_len=idx_len, **kw)
+
+
+def md_snapkv_votes(q_obs, k, prompt_lens, *, max_prompt_len=None, page_table=None,
+                    sm_scale=0.0, votes=None, workspace=None, stream=None):
+    """Raw SnapKV votes [B, Hkv, stride] fp32 of every prefix position
+    (q_obs [B, n_obs, Hq, d]; k contiguous or paged; see include/magicdec.h)."""
+    import torch
+    lib = load_library()
+    B, n_obs, Hq, d = q_obs.shape
+    paged = page_table is not None
+    if k.stride(3) != 1 or not q_obs.is_contiguous():
+        raise ValueError("q_obs must be contiguous and k unit-stride in head_dim")
+    if prompt_lens.dtype != torch.int32:
+        raise ValueError("prompt_lens must be int32")
+    if max_prompt_len is None:
+        max_prompt_len = page_table.shape[1] * k.shape[1] if paged else k.shape[1]
+    if B > 0 and not paged and k.shape[1] < max_prompt_len:
+        raise ValueError("contiguous k must hold max_prompt_len tokens per sequence")
+    stride = max(1, int(max_prompt_len) - n_obs)
+    if votes is None:
+        votes = torch.zeros((B, k.shape[2], stride), dtype=torch.float32, device=q_obs.device)
+    a = MdSnapkvArgs()
+    a.num_seqs, a.n_obs, a.num_q_heads, a.num_kv_heads, a.head_dim = B, n_obs, Hq, k.shape[2], d
+    a.dtype = _dtype_code(q_obs)
+    if _dtype_code(k) != a.dtype:
+        raise ValueError("q_obs and k must share a dtype")
+    a.sm_scale = float(sm_scale)
+    a.q_obs, a.k = q_obs.data_ptr(), k.data_ptr()
+    a.kv_stride_blk, a.kv_stride_tok, a.kv_stride_head = k.stride(0), k.stride(1), k.stride(2)
+    if paged:
+        a.page_size, a.max_pages_per_seq = k.shape[1], page_table.shape[1]
+        a.num_pages = k.shape[0]
+        a.page_table = page_table.data_ptr()
+    a.prompt_lens = prompt_lens.data_ptr()
+    a.max_prompt_len = int(max_prompt_len)
+    a.votes, a.votes_stride = votes.data_ptr(), votes.shape[-1]
+    need = int(lib.md_snapkv_workspace_bytes(ctypes.byref(a)))
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=q_obs.device)
+    a.workspace, a.workspace_bytes = workspace.data_ptr(), workspace.numel()
+    _check(lib.md_snapkv_votes(ctypes.byref(a), _stream_handle(q_obs, stream)))
+    return votes
+
+
+def md_snapkv_select(votes, prompt_lens, n_obs, budget, *, pool=5, idx=None, idx_len=None,
+                     stream=None):
+    """Pool the votes [B, Hkv, stride] and keep budget positions per (sequence,
+    kv head): returns (idx [B, Hkv, budget] int32 ascending, idx_len [B] int32)."""
+    import torch
+    lib = load_library()
+    B, Hkv, stride = votes.shape
+    if votes.dtype != torch.float32 or not votes.is_contiguous():
+        raise ValueError("votes must be contiguous float32 [B, Hkv, stride]")
+    if idx is None:
+        idx = torch.full((B, Hkv, budget), -1, dtype=torch.int32, device=votes.device)
+    if idx_len is None:
+        idx_len = torch.zeros((B,), dtype=torch.int32, device=votes.device)
+    _check(lib.md_snapkv_select(B, Hkv, _ptr(votes), stride, _ptr(prompt_lens), n_obs, pool,
+                                budget, _ptr(idx), _ptr(idx_len), _stream_handle(votes, stream)))
+    return idx, idx_len
 
 
 def md_merge_lse(o_parts, lse_parts, *, out_dtype=None, out=None, lse=None, stream=None):

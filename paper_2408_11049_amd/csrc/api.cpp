@@ -194,6 +194,84 @@ size_t md_workspace_bytes_indexed(const md_attn_args* a, int32_t idx_stride) {
       .workspace_bytes;
 }
 
+int md_snapkv_votes(const md_snapkv_args* a, void* stream) {
+  const int st = md::validate_snapkv(a);
+  if (st != MD_OK) return st;
+  if (a->num_seqs == 0) return MD_OK;
+  const md::SnapkvPlan pl = md::make_snapkv_plan(a, md::device_cu_count());
+  md::SnapkvParams p{};
+  p.q = a->q_obs;
+  p.k = a->k;
+  p.s_blk = a->kv_stride_blk;
+  p.s_tok = a->kv_stride_tok;
+  p.s_head = a->kv_stride_head;
+  p.page_table = a->page_table;
+  p.page_shift = 0;
+  if (a->page_size)
+    while ((1 << p.page_shift) < a->page_size) ++p.page_shift;
+  p.max_pages = a->max_pages_per_seq;
+  p.num_pages = a->num_pages;
+  p.kv_lens = a->prompt_lens;
+  p.max_kv_len = a->max_prompt_len;
+  p.n_obs = a->n_obs;
+  p.Hq = a->num_q_heads;
+  p.Hkv = a->num_kv_heads;
+  p.G = pl.G;
+  p.R = pl.R;
+  const float scale =
+      a->sm_scale > 0.f ? a->sm_scale : 1.0f / sqrtf(static_cast<float>(a->head_dim));
+  p.scale_log2 = scale * 1.44269504088896340736f;
+  p.n_units = pl.n_units;
+  p.n_chunks_stats = pl.n_chunks_stats;
+  p.chunk_len_stats = pl.chunk_len_stats;
+  p.n_chunks_votes = pl.n_chunks_votes;
+  p.chunk_len_votes = pl.chunk_len_votes;
+  unsigned char* ws = static_cast<unsigned char*>(a->workspace);
+  p.part_m = reinterpret_cast<float*>(ws);
+  p.part_l = reinterpret_cast<float*>(ws + pl.part_bytes);
+  p.lse2 = reinterpret_cast<float*>(ws + 2 * pl.part_bytes);
+  p.votes = a->votes;
+  p.votes_stride = a->votes_stride;
+  const hipError_t e = md::launch_snapkv_votes(p, a->head_dim, a->dtype == MD_BF16, pl.TW,
+                                               a->page_size != 0,
+                                               static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? MD_OK : md::hip_fail(e);
+}
+
+size_t md_snapkv_workspace_bytes(const md_snapkv_args* a) {
+  if (!a || a->num_seqs < 0 || a->n_obs < 1 || a->num_q_heads < 1 || a->num_kv_heads < 1 ||
+      a->num_q_heads % a->num_kv_heads || a->max_prompt_len < a->n_obs)
+    return 0;
+  return md::make_snapkv_plan(a, md::device_cu_count()).workspace_bytes;
+}
+
+int md_snapkv_select(int32_t num_seqs, int32_t num_kv_heads, const float* votes,
+                     int32_t votes_stride, const int32_t* prompt_lens, int32_t n_obs,
+                     int32_t pool, int32_t budget, int32_t* idx, int32_t* idx_len, void* stream) {
+  if (num_seqs < 0 || num_kv_heads < 1 || votes_stride < 1 || n_obs < 0 || pool < 1 ||
+      pool % 2 == 0 || budget < n_obs || budget < 1)
+    return MD_ERR_INVALID_ARG;
+  if (num_seqs == 0) return MD_OK;
+  if (!votes || !prompt_lens || !idx || !idx_len) return MD_ERR_INVALID_ARG;
+  if ((reinterpret_cast<uintptr_t>(votes) & 3u) || (reinterpret_cast<uintptr_t>(prompt_lens) & 3u) ||
+      (reinterpret_cast<uintptr_t>(idx) & 3u) || (reinterpret_cast<uintptr_t>(idx_len) & 3u))
+    return MD_ERR_INVALID_ARG;
+  if (static_cast<int64_t>(num_seqs) * num_kv_heads > INT32_MAX) return MD_ERR_INVALID_ARG;
+  md::SnapkvSelectParams p{};
+  p.votes = votes;
+  p.stride = votes_stride;
+  p.lens = prompt_lens;
+  p.rows = num_seqs * num_kv_heads;
+  p.rows_per_seq = num_kv_heads;
+  p.n_obs = n_obs;
+  p.pool = pool;
+  p.budget = budget;
+  p.idx = idx;
+  p.counts = idx_len;
+  const hipError_t e = md::launch_snapkv_select(p, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? MD_OK : md::hip_fail(e);
+}
+
 const char* md_status_str(int status) {
   switch (status) {
     case MD_OK: return "ok";

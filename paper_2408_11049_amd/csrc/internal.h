@@ -48,6 +48,20 @@ int validate_attn(const md_attn_args* a, int mode, int n_sink, int window);
 // mode MD_MODE_DRAFT_INDEXED reads `window` as the list capacity idx_stride.
 Plan make_plan(const md_attn_args* a, int mode, int n_sink, int window, int num_cus);
 
+// SnapKV selection: validation and the chunking of its two passes.
+constexpr int kSnapkvMaxRows = 256;  // G * n_obs
+struct SnapkvPlan {
+  int32_t G = 0, R = 0, TW = 0;
+  int32_t n_units = 0;
+  int32_t n_chunks_stats = 0, chunk_len_stats = 0;
+  int32_t n_chunks_votes = 0, chunk_len_votes = 0;
+  size_t part_bytes = 0;   // part_m and part_l each: [units][n_chunks_stats][R] fp32
+  size_t lse_bytes = 0;    // [units][R] fp32
+  size_t workspace_bytes = 0;
+};
+int validate_snapkv(const md_snapkv_args* a);
+SnapkvPlan make_snapkv_plan(const md_snapkv_args* a, int num_cus);
+
 // Compute units of the current device (cached per device); 256 when no
 // device is visible, so sizes stay defined on a host without a GPU.
 int device_cu_count();

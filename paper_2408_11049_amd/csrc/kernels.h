@@ -39,6 +39,43 @@ struct AttnParams {
 // depth: K/V tiles each wave keeps in flight (1..3; bf16 instances).
 // occ: waves per SIMD the instance is compiled for (2 only with depth 1 and
 // NT <= 2; otherwise 1).
+// SnapKV-style selection (prefill): votes passes and the selection.
+struct SnapkvParams {
+  const void* q;              // observation queries [B, n_obs, Hq, d]
+  const void* k;
+  int64_t s_blk, s_tok, s_head;
+  const int32_t* page_table;
+  int32_t page_shift, max_pages;
+  int64_t num_pages;
+  const int32_t* kv_lens;     // prompt lengths [B]
+  int32_t max_kv_len;
+  int32_t n_obs, Hq, Hkv, G, R;
+  float scale_log2;
+  int32_t n_units;
+  int32_t n_chunks, chunk_len;              // of the pass being launched
+  int32_t n_chunks_stats, chunk_len_stats;  // softmax statistics pass
+  int32_t n_chunks_votes, chunk_len_votes;  // votes pass
+  float* part_m;              // [units][n_chunks_stats][R]
+  float* part_l;
+  float* lse2;                // [units][R]
+  float* votes;               // [B, Hkv, votes_stride]
+  int32_t votes_stride;
+};
+
+struct SnapkvSelectParams {
+  const float* votes;         // [rows][stride]
+  int32_t stride;
+  const int32_t* lens;        // prompt lengths [B]
+  int32_t rows, rows_per_seq;
+  int32_t n_obs, pool, budget;
+  int32_t* idx;               // [rows][budget]
+  int32_t* counts;            // [B]
+};
+
+hipError_t launch_snapkv_votes(const SnapkvParams& p, int head_dim, bool bf16, int TW, bool paged,
+                               hipStream_t s);
+hipError_t launch_snapkv_select(const SnapkvSelectParams& p, hipStream_t s);
+
 hipError_t launch_attn_partial(const AttnParams& p, int head_dim, bool bf16, int NT, bool paged,
                                int depth, int occ, int64_t n_blocks, hipStream_t s);
 

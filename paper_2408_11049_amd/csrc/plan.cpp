@@ -115,4 +115,80 @@ Plan make_plan(const md_attn_args* a, int mode, int n_sink, int window, int num_
   return p;
 }
 
+namespace {
+
+// Chunks of a range of U keys over n_units units: about two waiting
+// workgroups per resident slot, never below kMinChunkTokens per chunk.
+void split_range(int64_t U, int64_t n_units, int num_cus, int32_t* n_chunks_out,
+                 int32_t* chunk_len_out) {
+  const int64_t slots = static_cast<int64_t>(num_cus > 0 ? num_cus : 256) * 2;
+  int64_t n_chunks = 1;
+  if (n_units > 0 && n_units < 2 * slots) {
+    n_chunks = ceil_div(2 * slots, n_units);
+    const int64_t cap = ceil_div(U, kMinChunkTokens);
+    if (n_chunks > cap) n_chunks = cap;
+    if (n_chunks < 1) n_chunks = 1;
+  }
+  int64_t chunk_len = ceil_div(ceil_div(U > 0 ? U : 1, n_chunks), kTile) * kTile;
+  n_chunks = ceil_div(U > 0 ? U : 1, chunk_len);
+  *n_chunks_out = static_cast<int32_t>(n_chunks);
+  *chunk_len_out = static_cast<int32_t>(chunk_len);
+}
+
+}  // namespace
+
+int validate_snapkv(const md_snapkv_args* a) {
+  if (!a) return MD_ERR_INVALID_ARG;
+  if (a->num_seqs < 0 || a->n_obs < 1 || a->num_q_heads < 1 || a->num_kv_heads < 1)
+    return MD_ERR_INVALID_ARG;
+  if (a->num_q_heads % a->num_kv_heads) return MD_ERR_INVALID_ARG;
+  if (a->dtype != MD_F32 && a->dtype != MD_BF16) return MD_ERR_INVALID_ARG;
+  if (a->max_prompt_len < a->n_obs) return MD_ERR_INVALID_ARG;
+  if (a->votes_stride < 1 || a->votes_stride < a->max_prompt_len - a->n_obs)
+    return MD_ERR_INVALID_ARG;
+  const bool paged = a->page_size != 0;
+  if (a->page_size < 0) return MD_ERR_INVALID_ARG;
+  if (paged) {
+    if (!is_pow2(a->page_size) || a->max_pages_per_seq < 1 || a->num_pages < 1 ||
+        a->num_pages > INT32_MAX)
+      return MD_ERR_INVALID_ARG;
+    if (ceil_div(a->max_prompt_len, a->page_size) > a->max_pages_per_seq) return MD_ERR_INVALID_ARG;
+  }
+  if (a->kv_stride_blk < 0 || a->kv_stride_tok < 0 || a->kv_stride_head < 0)
+    return MD_ERR_INVALID_ARG;
+  if (a->head_dim != 64 && a->head_dim != 128) return MD_ERR_UNSUPPORTED;
+  if (static_cast<int64_t>(a->num_q_heads / a->num_kv_heads) * a->n_obs > kSnapkvMaxRows)
+    return MD_ERR_UNSUPPORTED;
+  if (a->num_seqs == 0) return MD_OK;
+  if (!a->q_obs || !a->k || !a->prompt_lens || !a->votes) return MD_ERR_INVALID_ARG;
+  if (paged != (a->page_table != nullptr)) return MD_ERR_INVALID_ARG;
+  if (!aligned16(a->q_obs) || !aligned16(a->k) || (reinterpret_cast<uintptr_t>(a->votes) & 3u) ||
+      (reinterpret_cast<uintptr_t>(a->prompt_lens) & 3u))
+    return MD_ERR_INVALID_ARG;
+  const int64_t per16 = a->dtype == MD_BF16 ? 8 : 4;
+  if (a->kv_stride_blk % per16 || a->kv_stride_tok % per16 || a->kv_stride_head % per16)
+    return MD_ERR_INVALID_ARG;
+  if (a->num_kv_heads > 1 && a->kv_stride_head < a->head_dim) return MD_ERR_INVALID_ARG;
+  const SnapkvPlan pl = make_snapkv_plan(a, device_cu_count());
+  if (!a->workspace || a->workspace_bytes < pl.workspace_bytes ||
+      (reinterpret_cast<uintptr_t>(a->workspace) & 255u))
+    return MD_ERR_WORKSPACE;
+  return MD_OK;
+}
+
+SnapkvPlan make_snapkv_plan(const md_snapkv_args* a, int num_cus) {
+  SnapkvPlan p;
+  p.G = a->num_q_heads / a->num_kv_heads;
+  p.R = p.G * a->n_obs;
+  p.TW = p.R <= 64 ? 1 : (p.R <= 128 ? 2 : 4);
+  p.n_units = a->num_seqs * a->num_kv_heads;
+  split_range(a->max_prompt_len, p.n_units, num_cus, &p.n_chunks_stats, &p.chunk_len_stats);
+  split_range(a->max_prompt_len - a->n_obs, p.n_units, num_cus, &p.n_chunks_votes,
+              &p.chunk_len_votes);
+  p.part_bytes = align_up(static_cast<size_t>(p.n_units) * p.n_chunks_stats * p.R * 4, 256);
+  p.lse_bytes = align_up(static_cast<size_t>(p.n_units) * p.R * 4, 256);
+  p.workspace_bytes = 2 * p.part_bytes + p.lse_bytes;
+  return p;
+}
+
 }  // namespace md

@@ -1,0 +1,423 @@
+// snapkv.hip -- SnapKV-style selection of the static draft cache at prefill.
+//
+// The paper's best drafter keeps a static compressed KV cache chosen by
+// SnapKV (static KV selection, Sec. 4.4; best budget 2049, Sec. 5.2), with an
+// observation window of 32 queries and average pooling of kernel 5 (the
+// footnote of Sec. 4.4).  Per (sequence, kv head):
+//   vote(j)   = sum over the observation queries o and the kv head's G query
+//               heads h of softmax_j'(scale q_{o,h} . k_j') at j, the softmax
+//               running over the keys each query sees (j' <= its position);
+//   pooled(j) = mean of vote over j-2 .. j+2 (zero outside the prefix);
+//   keep the budget - 32 prefix positions of largest pooled vote plus the
+//   32 observation positions, ascending.
+//
+// Kernels:
+//   snapkv_pass_kernel<PASS=0>  per (unit, key chunk): each observation row's
+//       running max and sum of exp over the chunk (softmax statistics);
+//   snapkv_lse_kernel           merges the chunks into one log2-sum-exp per row;
+//   snapkv_pass_kernel<PASS=1>  per (unit, prefix chunk): p = 2^(s - lse) and
+//       the per-key sum over all rows: the raw votes;
+//   snapkv_select_kernel        per unit: pooled votes, radix select of the
+//       top keep, ordered compaction, plus the window.
+// In the pass kernels all G*n_obs rows of a unit share each 32-key tile,
+// loaded once into LDS as whole 256 B rows; each wave owns a quarter of the
+// rows (16-row MFMA tiles) and computes S^T = K Q^T on v_mfma_f32_16x16x32_bf16.
+#include <hip/hip_runtime.h>
+
+#include "internal.h"
+#include "kernels.h"
+
+namespace md {
+
+namespace {
+
+typedef __bf16 sk_bf16x8 __attribute__((ext_vector_type(8)));
+typedef float sk_f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t sk_u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kSkWaves = 4;
+constexpr int kSkTile = 32;
+
+template <int D, bool BF16>
+struct SkShape {
+  static constexpr int ES = BF16 ? 2 : 4;
+  static constexpr int KCB = D * ES / 64;     // 16 B A-operand chunks per lane per 16-key block
+  static constexpr int LPT = D * ES / 16;     // lanes per key row
+  static constexpr int ROWS_PER_WG_LOAD = kSkWaves * 64 / LPT;  // key rows one pass of all waves loads
+  static constexpr int NLD = kSkTile / ROWS_PER_WG_LOAD;        // loads per lane per tile
+  static constexpr int KROW = D * ES + 16;    // padded LDS row (odd multiple of 16 B)
+};
+
+}  // namespace
+
+// TW: 16-row tiles per wave (rows per workgroup = 64 * TW).
+template <int D, bool BF16, int TW, bool PAGED, int PASS>
+__global__ void __launch_bounds__(kSkWaves * 64)
+snapkv_pass_kernel(const SnapkvParams p) {
+  using SH = SkShape<D, BF16>;
+  __shared__ __attribute__((aligned(16))) unsigned char kt[2][kSkTile * SH::KROW];
+  __shared__ float red[kSkWaves][kSkTile];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int l16 = lane & 15;
+  const int grp = lane >> 4;
+  const int chunk = blockIdx.x % p.n_chunks;
+  const int unit = blockIdx.x / p.n_chunks;
+  const int hk = unit % p.Hkv;
+  const int b = unit / p.Hkv;
+  const int S = min(max(p.kv_lens[b], 0), p.max_kv_len);
+  const int n_pre = max(S - p.n_obs, 0);
+  // PASS 0 covers every key a query sees; PASS 1 only the prefix that is voted on.
+  const int U = PASS == 0 ? S : n_pre;
+  const int v_begin = chunk * p.chunk_len;
+  const int v_end = min(U, v_begin + p.chunk_len);
+  const int n_tiles = v_end > v_begin ? (v_end - v_begin + kSkTile - 1) / kSkTile : 0;
+
+  // Rows of this wave: r = (wave * TW + t) * 16 + l16, r = o * G + g.
+  int row_pos[TW];
+  sk_u32x4 qreg[TW][SH::KCB];
+  float lse2[TW];
+  for (int t = 0; t < TW; ++t) {
+    const int r = (wave * TW + t) * 16 + l16;
+    const bool real = r < p.R;
+    const int o = real ? r / p.G : 0, g = real ? r % p.G : 0;
+    row_pos[t] = real ? S - p.n_obs + o : -1;
+    for (int cb = 0; cb < SH::KCB; ++cb) qreg[t][cb] = sk_u32x4{0, 0, 0, 0};
+    if (real) {
+      const unsigned char* qp = static_cast<const unsigned char*>(p.q) +
+                                ((static_cast<int64_t>(b) * p.n_obs + o) * p.Hq + hk * p.G + g) *
+                                    D * SH::ES;
+      for (int cb = 0; cb < SH::KCB; ++cb)
+        qreg[t][cb] = *reinterpret_cast<const sk_u32x4*>(qp + cb * 64 + grp * 16);
+    }
+    // PASS 1: rows that are not real get lse = +inf, so their p is exactly 0.
+    lse2[t] = INFINITY;
+    if (PASS == 1 && real) lse2[t] = p.lse2[static_cast<int64_t>(unit) * p.R + r];
+  }
+
+  const unsigned char* kbase = static_cast<const unsigned char*>(p.k);
+  const int64_t head_off = static_cast<int64_t>(hk) * p.s_head;
+  const int32_t* ptab = PAGED ? p.page_table + static_cast<int64_t>(b) * p.max_pages : nullptr;
+  const int pmask = (1 << p.page_shift) - 1;
+
+  // Cooperative tile load: thread -> key row (threadIdx / LPT) + n * ROWS_PER_WG_LOAD,
+  // 16 B chunk threadIdx % LPT.  Keys past the range read element 0 and are masked.
+  auto load_tile = [&](sk_u32x4 (&x)[SH::NLD], int tile) {
+    for (int n = 0; n < SH::NLD; ++n) {
+      const int tt = n * SH::ROWS_PER_WG_LOAD + threadIdx.x / SH::LPT;
+      const int j = v_begin + tile * kSkTile + tt;
+      bool ok = tile < n_tiles && j < v_end;
+      int64_t off = 0;
+      if (PAGED) {
+        const int pid = ptab[ok ? (j >> p.page_shift) : 0];
+        ok = ok && pid >= 0 && pid < p.num_pages;
+        off = ok ? static_cast<int64_t>(pid) * p.s_blk + static_cast<int64_t>(j & pmask) * p.s_tok +
+                       head_off
+                 : 0;
+      } else {
+        off = ok ? static_cast<int64_t>(b) * p.s_blk + static_cast<int64_t>(j) * p.s_tok + head_off
+                 : 0;
+      }
+      x[n] = __builtin_nontemporal_load(reinterpret_cast<const sk_u32x4*>(
+          kbase + off * SH::ES + (threadIdx.x % SH::LPT) * 16));
+    }
+  };
+  auto store_tile = [&](const sk_u32x4 (&x)[SH::NLD], int buf) {
+    for (int n = 0; n < SH::NLD; ++n) {
+      const int tt = n * SH::ROWS_PER_WG_LOAD + threadIdx.x / SH::LPT;
+      *reinterpret_cast<sk_u32x4*>(kt[buf] + tt * SH::KROW + (threadIdx.x % SH::LPT) * 16) = x[n];
+    }
+  };
+
+  float m_run[TW], l_run[TW];
+  for (int t = 0; t < TW; ++t) {
+    m_run[t] = -INFINITY;
+    l_run[t] = 0.f;
+  }
+
+  sk_u32x4 xr[SH::NLD];
+  load_tile(xr, 0);
+  for (int tile = 0; tile < n_tiles; ++tile) {
+    const int buf = tile & 1;
+    store_tile(xr, buf);
+    __syncthreads();
+    load_tile(xr, tile + 1);  // next tile in flight while this one is used
+    const int v0 = v_begin + tile * kSkTile;
+
+    // S^T = K Q^T for this wave's row tiles.
+    sk_f32x4 sacc[TW][2];
+    for (int tb = 0; tb < 2; ++tb) {
+      for (int t = 0; t < TW; ++t) sacc[t][tb] = sk_f32x4{0.f, 0.f, 0.f, 0.f};
+      const unsigned char* krow = kt[buf] + (tb * 16 + l16) * SH::KROW + grp * 16;
+      for (int cb = 0; cb < SH::KCB; ++cb) {
+        const sk_u32x4 kk = *reinterpret_cast<const sk_u32x4*>(krow + cb * 64);
+        for (int t = 0; t < TW; ++t) {
+          if constexpr (BF16) {
+            sacc[t][tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(sk_bf16x8, kk), __builtin_bit_cast(sk_bf16x8, qreg[t][cb]),
+                sacc[t][tb], 0, 0, 0);
+          } else {
+            for (int jj = 0; jj < 4; ++jj)
+              sacc[t][tb] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                  __uint_as_float(kk[jj]), __uint_as_float(qreg[t][cb][jj]), sacc[t][tb], 0, 0, 0);
+          }
+        }
+      }
+    }
+
+    if constexpr (PASS == 0) {
+      // Online max and sum of 2^(s*scale*log2e) per row (this lane's 8 keys).
+      for (int t = 0; t < TW; ++t) {
+        float x8[8];
+        float mx = -INFINITY;
+        for (int tb = 0; tb < 2; ++tb)
+          for (int e = 0; e < 4; ++e) {
+            const int j = v0 + tb * 16 + grp * 4 + e;
+            const bool vis = j < v_end && j <= row_pos[t];
+            x8[tb * 4 + e] = vis ? sacc[t][tb][e] * p.scale_log2 : -INFINITY;
+            mx = fmaxf(mx, x8[tb * 4 + e]);
+          }
+        const float m_new = fmaxf(m_run[t], mx);
+        const float m_use = m_new == -INFINITY ? 0.f : m_new;
+        float s = 0.f;
+        for (int jj = 0; jj < 8; ++jj) s += __builtin_amdgcn_exp2f(x8[jj] - m_use);
+        l_run[t] = l_run[t] * __builtin_amdgcn_exp2f(m_run[t] - m_use) + s;
+        m_run[t] = m_new;
+      }
+    } else {
+      // p = 2^(s*scale*log2e - lse2) summed over every row, per key.
+      float col[8];
+      for (int jj = 0; jj < 8; ++jj) col[jj] = 0.f;
+      for (int t = 0; t < TW; ++t)
+        for (int tb = 0; tb < 2; ++tb)
+          for (int e = 0; e < 4; ++e)
+            col[tb * 4 + e] += __builtin_amdgcn_exp2f(sacc[t][tb][e] * p.scale_log2 - lse2[t]);
+      // Sum over the 16 rows of each 16-lane group.
+      for (int off = 1; off < 16; off <<= 1)
+        for (int jj = 0; jj < 8; ++jj) col[jj] += __shfl_xor(col[jj], off);
+      if (l16 == 0)
+        for (int tb = 0; tb < 2; ++tb)
+          for (int e = 0; e < 4; ++e) red[wave][tb * 16 + grp * 4 + e] = col[tb * 4 + e];
+      __syncthreads();
+      if (threadIdx.x < kSkTile) {
+        const int j = v0 + threadIdx.x;
+        if (j < v_end) {
+          float sum = 0.f;
+          for (int w = 0; w < kSkWaves; ++w) sum += red[w][threadIdx.x];
+          p.votes[(static_cast<int64_t>(b) * p.Hkv + hk) * p.votes_stride + j] = sum;
+        }
+      }
+    }
+    __syncthreads();  // the tile buffer and the reduction slots are reused
+  }
+
+  if constexpr (PASS == 0) {
+    // Combine the 4 lanes of each row, then write (m, l) for this chunk.
+    for (int t = 0; t < TW; ++t) {
+      float m_all = fmaxf(m_run[t], __shfl_xor(m_run[t], 16));
+      m_all = fmaxf(m_all, __shfl_xor(m_all, 32));
+      const float m_use = m_all == -INFINITY ? 0.f : m_all;
+      float l = l_run[t] * __builtin_amdgcn_exp2f(m_run[t] - m_use);
+      l += __shfl_xor(l, 16);
+      l += __shfl_xor(l, 32);
+      const int r = (wave * TW + t) * 16 + l16;
+      if (grp == 0 && r < p.R) {
+        const int64_t at = (static_cast<int64_t>(unit) * p.n_chunks + chunk) * p.R + r;
+        p.part_m[at] = m_all;
+        p.part_l[at] = l;
+      }
+    }
+  }
+}
+
+// lse2[unit][r] = log2 sum over chunks of l_c * 2^(m_c).
+__global__ void __launch_bounds__(256) snapkv_lse_kernel(const SnapkvParams p) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= static_cast<int64_t>(p.n_units) * p.R) return;
+  const int64_t unit = i / p.R, r = i % p.R;
+  float M = -INFINITY;
+  for (int c = 0; c < p.n_chunks; ++c) M = fmaxf(M, p.part_m[(unit * p.n_chunks + c) * p.R + r]);
+  float L = 0.f;
+  if (M != -INFINITY)
+    for (int c = 0; c < p.n_chunks; ++c) {
+      const float m = p.part_m[(unit * p.n_chunks + c) * p.R + r];
+      if (m != -INFINITY) L += p.part_l[(unit * p.n_chunks + c) * p.R + r] * __builtin_amdgcn_exp2f(m - M);
+    }
+  p.lse2[i] = L > 0.f ? M + __builtin_amdgcn_logf(L) : INFINITY;
+}
+
+// ---------------------------------------------------------------------------
+// Selection.  One workgroup per (sequence, kv head) row.
+
+namespace {
+
+// Order-preserving map of a float onto uint32 (larger float -> larger key).
+__device__ __forceinline__ uint32_t sk_key(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ float sk_pooled(const float* v, int n, int j, int pool) {
+  float s = 0.f;
+  for (int t = j - pool / 2; t <= j + pool / 2; ++t)
+    if (t >= 0 && t < n) s += v[t];
+  return s / static_cast<float>(pool);
+}
+
+}  // namespace
+
+__global__ void __launch_bounds__(256) snapkv_select_kernel(const SnapkvSelectParams p) {
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t s_prefix, s_above;
+  __shared__ uint32_t w_eq[4], w_take[4];
+  __shared__ uint32_t s_out, s_eq_seen;
+
+  const int row = blockIdx.x;
+  const int b = row / p.rows_per_seq;
+  const int S = min(max(p.lens[b], 0), p.stride + p.n_obs);
+  const int n = max(S - p.n_obs, 0);
+  const int keep = min(p.budget - p.n_obs, n);
+  const float* v = p.votes + static_cast<int64_t>(row) * p.stride;
+  int32_t* out = p.idx + static_cast<int64_t>(row) * p.budget;
+  const int tid = threadIdx.x;
+  const int w = tid >> 6;
+  const uint64_t below = (1ull << (tid & 63)) - 1ull;
+
+  // Radix select, most significant byte first: after four passes tau is the
+  // key of the keep-th largest pooled vote and `above` keys exceed it.
+  uint32_t prefix = 0, above = 0;
+  if (keep > 0) {
+    for (int pass = 0; pass < 4; ++pass) {
+      const int shift = 24 - 8 * pass;
+      const uint32_t hi_mask = pass == 0 ? 0u : (0xffffffffu << (32 - 8 * pass));
+      hist[tid] = 0;
+      __syncthreads();
+      for (int j = tid; j < n; j += 256) {
+        const uint32_t key = sk_key(sk_pooled(v, n, j, p.pool));
+        if ((key & hi_mask) == (prefix & hi_mask)) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+      }
+      __syncthreads();
+      if (tid == 0) {
+        // Walk the digits from the top until the running count reaches keep.
+        uint32_t run = above;
+        int d = 255;
+        for (; d > 0; --d) {
+          if (run + hist[d] >= static_cast<uint32_t>(keep)) break;
+          run += hist[d];
+        }
+        s_above = run;
+        s_prefix = prefix | (static_cast<uint32_t>(d) << shift);
+      }
+      __syncthreads();
+      prefix = s_prefix;
+      above = s_above;
+      __syncthreads();
+    }
+  }
+  const uint32_t tau = prefix;
+  const uint32_t need_eq = keep > 0 ? static_cast<uint32_t>(keep) - above : 0;
+
+  // Ordered compaction over 256-position slices: keep key > tau, and key ==
+  // tau while fewer than need_eq of those were kept; positions come out
+  // ascending, so ties go to the smaller position.
+  if (tid == 0) {
+    s_out = 0;
+    s_eq_seen = 0;
+  }
+  __syncthreads();
+  for (int base = 0; base < n && keep > 0; base += 256) {
+    const int j = base + tid;
+    bool gt = false, eq = false;
+    if (j < n) {
+      const uint32_t key = sk_key(sk_pooled(v, n, j, p.pool));
+      gt = key > tau;
+      eq = key == tau;
+    }
+    const uint64_t eq_mask = __ballot(eq);
+    if ((tid & 63) == 0) w_eq[w] = __popcll(eq_mask);
+    __syncthreads();
+    uint32_t eq_before = s_eq_seen + __popcll(eq_mask & below);
+    for (int x = 0; x < w; ++x) eq_before += w_eq[x];
+    const bool take = gt || (eq && eq_before < need_eq);
+    const uint64_t take_mask = __ballot(take);
+    if ((tid & 63) == 0) w_take[w] = __popcll(take_mask);
+    __syncthreads();
+    uint32_t pos = s_out + __popcll(take_mask & below);
+    for (int x = 0; x < w; ++x) pos += w_take[x];
+    if (take) out[pos] = j;
+    __syncthreads();
+    if (tid == 0) {
+      s_out += w_take[0] + w_take[1] + w_take[2] + w_take[3];
+      s_eq_seen += w_eq[0] + w_eq[1] + w_eq[2] + w_eq[3];
+    }
+    __syncthreads();
+  }
+  // The observation window, always kept.
+  const int kept = keep > 0 ? keep : 0;
+  for (int j = n + tid; j < S; j += 256) out[kept + (j - n)] = j;
+  if (tid == 0 && (row % p.rows_per_seq) == 0) p.counts[b] = kept + (S - n);
+}
+
+// ---------------------------------------------------------------------------
+// Host-side dispatch.
+
+template <int D, bool BF16, int TW, int PASS>
+static hipError_t sk_launch_tw(const SnapkvParams& p, bool paged, int64_t blocks, hipStream_t s) {
+  if (paged)
+    hipLaunchKernelGGL((snapkv_pass_kernel<D, BF16, TW, true, PASS>), dim3(blocks),
+                       dim3(kSkWaves * 64), 0, s, p);
+  else
+    hipLaunchKernelGGL((snapkv_pass_kernel<D, BF16, TW, false, PASS>), dim3(blocks),
+                       dim3(kSkWaves * 64), 0, s, p);
+  return hipGetLastError();
+}
+
+template <int D, bool BF16, int PASS>
+static hipError_t sk_launch_d(const SnapkvParams& p, int TW, bool paged, int64_t blocks,
+                              hipStream_t s) {
+  switch (TW) {
+    case 1: return sk_launch_tw<D, BF16, 1, PASS>(p, paged, blocks, s);
+    case 2: return sk_launch_tw<D, BF16, 2, PASS>(p, paged, blocks, s);
+    case 4: return sk_launch_tw<D, BF16, 4, PASS>(p, paged, blocks, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+template <int PASS>
+static hipError_t sk_launch(const SnapkvParams& p, int head_dim, bool bf16, int TW, bool paged,
+                            int64_t blocks, hipStream_t s) {
+  if (blocks <= 0) return hipSuccess;
+  if (head_dim == 128)
+    return bf16 ? sk_launch_d<128, true, PASS>(p, TW, paged, blocks, s)
+                : sk_launch_d<128, false, PASS>(p, TW, paged, blocks, s);
+  return bf16 ? sk_launch_d<64, true, PASS>(p, TW, paged, blocks, s)
+              : sk_launch_d<64, false, PASS>(p, TW, paged, blocks, s);
+}
+
+hipError_t launch_snapkv_votes(const SnapkvParams& p, int head_dim, bool bf16, int TW, bool paged,
+                               hipStream_t s) {
+  SnapkvParams q = p;
+  q.chunk_len = p.chunk_len_stats;
+  q.n_chunks = p.n_chunks_stats;
+  hipError_t e = sk_launch<0>(q, head_dim, bf16, TW, paged,
+                              static_cast<int64_t>(p.n_units) * q.n_chunks, s);
+  if (e != hipSuccess) return e;
+  const int64_t rows = static_cast<int64_t>(p.n_units) * p.R;
+  hipLaunchKernelGGL(snapkv_lse_kernel, dim3(static_cast<uint32_t>((rows + 255) / 256)), dim3(256),
+                     0, s, q);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  q.chunk_len = p.chunk_len_votes;
+  q.n_chunks = p.n_chunks_votes;
+  return sk_launch<1>(q, head_dim, bf16, TW, paged,
+                      static_cast<int64_t>(p.n_units) * q.n_chunks, s);
+}
+
+hipError_t launch_snapkv_select(const SnapkvSelectParams& p, hipStream_t s) {
+  if (p.rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(snapkv_select_kernel, dim3(p.rows), dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
+}  // namespace md

@@ -142,6 +142,47 @@ def test_indexed_workspace_tracks_list_capacity(lib):
     assert small == 0 and big > 0
 
 
+def good_snapkv(**over):
+    a = md.MdSnapkvArgs()
+    a.num_seqs, a.n_obs, a.num_q_heads, a.num_kv_heads, a.head_dim = 2, 32, 8, 2, 128
+    a.dtype = md.MD_BF16
+    a.q_obs = a.k = a.prompt_lens = a.votes = FAKE
+    a.kv_stride_head, a.kv_stride_tok, a.kv_stride_blk = 128, 256, 100 * 256
+    a.max_prompt_len, a.votes_stride = 100, 68
+    for k, v in over.items():
+        setattr(a, k, v)
+    return a
+
+
+SNAP_BAD = [
+    ("n_obs 0", dict(n_obs=0), md.MD_ERR_INVALID_ARG),
+    ("stride too small", dict(votes_stride=67), md.MD_ERR_INVALID_ARG),
+    ("prompt shorter than window", dict(max_prompt_len=31), md.MD_ERR_INVALID_ARG),
+    ("null votes", dict(votes=None), md.MD_ERR_INVALID_ARG),
+    ("null q_obs", dict(q_obs=None), md.MD_ERR_INVALID_ARG),
+    ("misaligned k", dict(k=FAKE + 4), md.MD_ERR_INVALID_ARG),
+    ("rows over 256", dict(n_obs=65, max_prompt_len=200, votes_stride=200), md.MD_ERR_UNSUPPORTED),
+    ("head_dim 80", dict(head_dim=80), md.MD_ERR_UNSUPPORTED),
+    ("no workspace", dict(), md.MD_ERR_WORKSPACE),
+]
+
+
+@pytest.mark.parametrize("name,over,want", SNAP_BAD, ids=[b[0] for b in SNAP_BAD])
+def test_snapkv_votes_rejects(lib, name, over, want):
+    assert lib.md_snapkv_votes(ctypes.byref(good_snapkv(**over)), None) == want
+
+
+def test_snapkv_workspace_and_select_args(lib):
+    assert lib.md_snapkv_workspace_bytes(ctypes.byref(good_snapkv())) > 0
+    assert lib.md_snapkv_workspace_bytes(None) == 0
+    sel = lib.md_snapkv_select
+    assert sel(2, 2, FAKE, 68, FAKE, 32, 4, 64, FAKE, FAKE, None) == md.MD_ERR_INVALID_ARG  # even pool
+    assert sel(2, 2, FAKE, 68, FAKE, 32, 5, 16, FAKE, FAKE, None) == md.MD_ERR_INVALID_ARG  # budget < n_obs
+    assert sel(2, 2, None, 68, FAKE, 32, 5, 64, FAKE, FAKE, None) == md.MD_ERR_INVALID_ARG
+    assert sel(2, 0, FAKE, 68, FAKE, 32, 5, 64, FAKE, FAKE, None) == md.MD_ERR_INVALID_ARG
+    assert sel(0, 2, None, 68, None, 32, 5, 64, None, None, None) == md.MD_OK
+
+
 def test_null_args(lib):
     assert lib.md_verify_attn(None, None) == md.MD_ERR_INVALID_ARG
     assert lib.md_draft_attn(None, 1, 1, None) == md.MD_ERR_INVALID_ARG
