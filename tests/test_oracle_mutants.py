@@ -76,3 +76,49 @@ def test_mutant_is_caught(name, old, new, tmpdir_mod):
         except (AssertionError, ValueError):
             caught.append(pin.__name__)
     assert caught, f"no pin catches the planted mistake '{name}'"
+
+
+# Planted mistakes in copies of oracle/sdstep.py: (name, text, replacement)
+SDSTEP_SRC = os.path.join(os.path.dirname(obuild.__file__), "sdstep.py")
+SDSTEP_MUTANTS = [
+    ("accept: last draft never accepted", "while a < L - 1 and", "while a < L - 2 and"),
+    ("accept: bonus from the next input", "tokens[b, a] = target[b, a]",
+     "tokens[b, a] = target[b, min(a + 1, L - 1)]"),
+    ("accept: ties to the last index", "return np.argmax(x, axis=-1).astype(np.int64)",
+     "return (x.shape[-1] - 1 - np.argmax(x[..., ::-1], axis=-1)).astype(np.int64)"),
+    ("accept: NaN wins", "x = np.where(np.isnan(x), -np.inf, x)", "x = x"),
+    ("accept: bf16 widened wrongly", "astype(np.uint32) << 16", "astype(np.uint32) << 15"),
+    ("eq1: exponent gamma", "alpha ** (gamma + 1)", "alpha ** gamma"),
+    ("append: one slot late", "int(pos0[b]) + i,", "int(pos0[b]) + i + 1,"),
+    ("append: page slot wrong", "return int(page_table[b, j // page_size]), j % page_size",
+     "return int(page_table[b, j // page_size]), (j + 1) % page_size"),
+    ("commit: bonus input not kept", "np.asarray(accepted, np.int64) + 1",
+     "np.asarray(accepted, np.int64)"),
+    ("ring: last kept position dropped", "range(C, C + int(accepted[b]) + 1)",
+     "range(C, C + int(accepted[b]))"),
+    ("ring: slot shifted", "idx[b, :, ring_start + j % ring_len] = j",
+     "idx[b, :, ring_start + (j + 1) % ring_len] = j"),
+    ("streaming: window one short", "range(max(n_sink, C - window), C)",
+     "range(max(n_sink, C - window + 1), C)"),
+    ("streaming: sinks dropped", "for j in range(min(n_sink, C)):", "for j in range(0):"),
+]
+
+
+@pytest.mark.parametrize("name,old,new", SDSTEP_MUTANTS, ids=[m[0] for m in SDSTEP_MUTANTS])
+def test_sdstep_mutant_is_caught(name, old, new):
+    import importlib.util
+
+    from sdstep_pins import ALL_SDSTEP_PINS
+
+    text = open(SDSTEP_SRC).read()
+    assert text.count(old) == 1, f"mutation anchor not found once: {old!r}"
+    spec = importlib.util.spec_from_loader("sdstep_mutant", loader=None)
+    mod = importlib.util.module_from_spec(spec)
+    exec(compile(text.replace(old, new), "sdstep_mutant.py", "exec"), mod.__dict__)
+    caught = []
+    for pin in ALL_SDSTEP_PINS:
+        try:
+            pin(mod=mod)
+        except (AssertionError, ValueError, IndexError):
+            caught.append(pin.__name__)
+    assert caught, f"no pin catches the planted mistake '{name}'"
