@@ -237,6 +237,122 @@ int md_snapkv_select(int32_t num_seqs, int32_t num_kv_heads, const float* votes,
                      int32_t votes_stride, const int32_t* prompt_lens, int32_t n_obs,
                      int32_t pool, int32_t budget, int32_t* idx, int32_t* idx_len, void* stream);
 
+/*
+ * ---- The speculative step around verification (Sec. 3.1; greedy decoding,
+ * Sec. 5.1) ----
+ *
+ * A sequence holds C committed tokens.  One step runs the verifier on
+ * q_len = gamma + 1 tokens [t0, d_1 .. d_gamma] (t0 = the last token produced,
+ * then the drafts), whose K/V go to positions C .. C + gamma (md_kv_append),
+ * so verification sees S = C + q_len.  Greedy acceptance (md_greedy_accept)
+ * keeps the drafts that match the target's argmax up to the first mismatch
+ * plus one bonus token; with a drafts accepted the K/V of t0, d_1 .. d_a stay
+ * and the cache is committed to C' = C + a + 1 (md_kv_commit), which rolls
+ * the rejected positions back.  The expected a + 1 per step is Eq. 1.
+ */
+
+/* One layer's KV cache as a write target, addressed as in md_attn_args. */
+typedef struct {
+  int32_t num_seqs;           /* B >= 0 */
+  int32_t num_kv_heads;       /* Hkv >= 1 */
+  int32_t head_dim;           /* d >= 1; d * element size a multiple of 16 bytes */
+  int32_t dtype;              /* md_dtype of k, v and the appended rows */
+  void* k;
+  void* v;
+  int64_t kv_stride_blk, kv_stride_tok, kv_stride_head;  /* element strides, 16-byte multiples */
+  int32_t page_size;          /* 0 = contiguous, else tokens per page (power of two) */
+  int32_t max_pages_per_seq;  /* columns of page_table (paged only) */
+  int64_t num_pages;          /* pages in the pool (paged only) */
+  const int32_t* page_table;  /* device [B, max_pages_per_seq], or NULL when contiguous */
+  int32_t capacity;           /* contiguous: tokens each sequence's block holds (>= 1);
+                                 paged: ignored (max_pages_per_seq * page_size) */
+} md_kv_cache;
+
+/*
+ * Write n_new tokens' K and V rows of every sequence into the cache:
+ *   k_new, v_new  device [B, n_new, Hkv, d], contiguous, dtype of the cache,
+ *                 16-byte aligned
+ *   pos0          device int32 [B]: row i of sequence b goes to position
+ *                 pos0[b] + i (pages through page_table when paged)
+ *   lens_out      device int32 [B] or NULL: set to pos0[b] + n_new; must not
+ *                 be pos0 itself
+ * Positions past the capacity (or the table), and pages outside
+ * [0, num_pages), are not written: memory stays in bounds, those rows are
+ * lost.  Values move bit for bit.  The caller provides the pages.
+ * Errors: MD_ERR_INVALID_ARG for NULL or misaligned pointers, bad sizes,
+ * n_new < 0, lens_out == pos0; MD_ERR_HIP.
+ */
+int md_kv_append(const md_kv_cache* c, int32_t n_new, const void* k_new, const void* v_new,
+                 const int32_t* pos0, int32_t* lens_out, void* stream);
+
+/*
+ * Greedy acceptance with a bonus token, per sequence b:
+ *   target[b][i] = the first index of the largest of logits[b][i][0 .. vocab),
+ *                  a NaN logit comparing as -inf (a row of NaN and -inf gives 0);
+ *   accepted[b]  = the length of the leading run of i < n_draft with
+ *                  draft[b][i] == target[b][i];
+ *   tokens[b][i] = draft[b][i] for i < accepted[b], target[b][accepted[b]] (the
+ *                  bonus) at i = accepted[b], -1 after.
+ *   logits    device [B, n_draft + 1, vocab] in dtype (MD_F32 or MD_BF16), contiguous
+ *   draft     device int32 [B, n_draft]
+ *   accepted  device int32 [B] out
+ *   tokens    device int32 [B, n_draft + 1] out
+ *   target    device int32 [B, n_draft + 1] out, or NULL
+ *   workspace >= md_greedy_accept_workspace_bytes(), 256-byte aligned
+ * The argmax is exact (a comparison), so results are bit-exact in any
+ * reduction order.  Errors: MD_ERR_INVALID_ARG for NULL or misaligned
+ * pointers, n_draft outside [0, 1023], vocab < 1, a bad dtype;
+ * MD_ERR_WORKSPACE; MD_ERR_HIP.
+ */
+int md_greedy_accept(int32_t num_seqs, int32_t n_draft, int32_t vocab, int32_t dtype,
+                     const void* logits, const int32_t* draft, int32_t* accepted,
+                     int32_t* tokens, int32_t* target, void* workspace, size_t workspace_bytes,
+                     void* stream);
+
+/* Workspace bytes of md_greedy_accept for these sizes on the current device
+ * (0 for malformed sizes). */
+size_t md_greedy_accept_workspace_bytes(int32_t num_seqs, int32_t n_draft, int32_t vocab);
+
+/*
+ * Commit (and roll back) one step:
+ *   lens      device int32 [B], in: C (committed before the step); out:
+ *             C + a + 1 with a = accepted[b] clamped to [0, q_len - 1]
+ *   accepted  device int32 [B]
+ * With idx != NULL the kept positions C .. C + a are also recorded in every
+ * kv head's listed draft cache (idx [B, Hkv, idx_stride], as read by
+ * md_draft_attn_indexed): position j goes to slot ring_start + j % ring_len,
+ * which held j - ring_len, so slots [ring_start, ring_start + ring_len) hold
+ * the last ring_len committed positions: a rolling window.  Empty ring slots
+ * hold -1 (skipped by the attention), and the lists' idx_len must cover the
+ * ring.  Positions recorded this way must not also sit in the static part
+ * of the list.
+ * Errors: MD_ERR_INVALID_ARG for NULL or misaligned pointers, q_len < 1, and,
+ * with idx, num_kv_heads < 1, ring_start < 0, ring_len < 1 or
+ * ring_start + ring_len > idx_stride; MD_ERR_HIP.
+ */
+int md_kv_commit(int32_t num_seqs, int32_t q_len, int32_t* lens, const int32_t* accepted,
+                 int32_t num_kv_heads, int32_t* idx, int32_t idx_stride, int32_t ring_start,
+                 int32_t ring_len, void* stream);
+
+/*
+ * The StreamingLLM-style draft cache built at prefill, as lists for
+ * md_draft_attn_indexed that md_kv_commit(..., ring_start = n_sink,
+ * ring_len = window) then rolls forward (the static sink-plus-window cache
+ * the paper drafts with, Sec. 5.1, kept current as tokens are committed):
+ *   idx      device int32 [B, Hkv, n_sink + window] out: slots 0 .. n_sink-1
+ *            hold the sinks 0 .. min(n_sink, C) - 1, slot n_sink + j % window
+ *            holds prompt position j for the last `window` positions
+ *            j >= n_sink; other slots -1.  (A prompt shorter than n_sink has
+ *            fewer sinks.)
+ *   idx_len  device int32 [B] out: n_sink + window
+ *   prompt_lens device int32 [B]: C
+ * Errors: MD_ERR_INVALID_ARG for NULL or misaligned pointers, num_kv_heads
+ * < 1, n_sink < 0, window < 1; MD_ERR_HIP.
+ */
+int md_streaming_list(int32_t num_seqs, int32_t num_kv_heads, const int32_t* prompt_lens,
+                      int32_t n_sink, int32_t window, int32_t* idx, int32_t* idx_len,
+                      void* stream);
+
 /* Static description of a status code; never NULL. */
 const char* md_status_str(int status);
 

@@ -10,6 +10,10 @@ CPU fallback: if the library is missing, every call raises.
     md_draft_attn_indexed(q, k, v, kv_lens, idx, idx_len, ...) -> (o, lse)
     md_merge_lse(o_parts, lse_parts, ...)         -> (o, lse)
     md_workspace_bytes(...)                       -> int
+    md_kv_append(k, v, k_new, v_new, pos0, ...)   -> lens_out
+    md_greedy_accept(logits, draft, ...)          -> (accepted, tokens, target)
+    md_kv_commit(lens, accepted, q_len, ...)      (in place)
+    md_streaming_list(prompt_lens, Hkv, n_sink, window) -> (idx, idx_len)
 
 Shapes: q/o [B, L, Hq, d] (L = gamma + 1); k/v contiguous [B, S_alloc, Hkv, d]
 or, with ``page_table`` [B, max_pages] int32, paged [P, page_size, Hkv, d];
@@ -30,7 +34,9 @@ MD_MODE_VERIFY, MD_MODE_DRAFT, MD_MODE_DRAFT_INDEXED = 0, 1, 2
 
 EXPORTED = ["md_verify_attn", "md_draft_attn", "md_draft_attn_indexed", "md_merge_lse",
             "md_workspace_bytes", "md_workspace_bytes_indexed", "md_snapkv_votes",
-            "md_snapkv_workspace_bytes", "md_snapkv_select",
+            "md_snapkv_workspace_bytes", "md_snapkv_select", "md_kv_append",
+            "md_greedy_accept", "md_greedy_accept_workspace_bytes", "md_kv_commit",
+            "md_streaming_list",
             "md_status_str", "md_last_hip_error", "md_attn_args_size",
             "md_bench_stream_read", "md_bench_copy", "md_bench_fill"]
 
@@ -69,6 +75,20 @@ class MdSnapkvArgs(ctypes.Structure):
     ]
 
 
+class MdKvCache(ctypes.Structure):
+    """Mirror of ``md_kv_cache``."""
+    _fields_ = [
+        ("num_seqs", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32),
+        ("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
+        ("kv_stride_blk", ctypes.c_int64), ("kv_stride_tok", ctypes.c_int64),
+        ("kv_stride_head", ctypes.c_int64),
+        ("page_size", ctypes.c_int32), ("max_pages_per_seq", ctypes.c_int32),
+        ("num_pages", ctypes.c_int64), ("page_table", ctypes.c_void_p),
+        ("capacity", ctypes.c_int32),
+    ]
+
+
 _lib = None
 
 
@@ -101,6 +121,16 @@ def load_library(path: str = LIB_PATH):
     lib.md_snapkv_workspace_bytes.restype = sz
     lib.md_snapkv_select.argtypes = [i32, i32, vp, i32, vp, i32, i32, i32, vp, vp, vp]
     lib.md_snapkv_select.restype = ctypes.c_int
+    lib.md_kv_append.argtypes = [ctypes.POINTER(MdKvCache), i32, vp, vp, vp, vp, vp]
+    lib.md_kv_append.restype = ctypes.c_int
+    lib.md_greedy_accept.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.md_greedy_accept.restype = ctypes.c_int
+    lib.md_greedy_accept_workspace_bytes.argtypes = [i32, i32, i32]
+    lib.md_greedy_accept_workspace_bytes.restype = sz
+    lib.md_kv_commit.argtypes = [i32, i32, vp, vp, i32, vp, i32, i32, i32, vp]
+    lib.md_kv_commit.restype = ctypes.c_int
+    lib.md_streaming_list.argtypes = [i32, i32, vp, i32, i32, vp, vp, vp]
+    lib.md_streaming_list.restype = ctypes.c_int
     lib.md_merge_lse.argtypes = [i32, i64, i32, i32, vp, vp, vp, vp, vp]
     lib.md_merge_lse.restype = ctypes.c_int
     lib.md_workspace_bytes.argtypes = [args_p, i32, i32, i32]
@@ -338,9 +368,122 @@ def md_merge_lse(o_parts, lse_parts, *, out_dtype=None, out=None, lse=None, stre
     return out, lse
 
 
+def make_kv_cache(k, v, *, num_seqs=None, page_table=None) -> MdKvCache:
+    """Fill md_kv_cache from the cache tensors: contiguous [B, S_alloc, Hkv, d]
+    or, with page_table [B, max_pages] int32, paged [P, page_size, Hkv, d]."""
+    import torch
+    if k.dim() != 4 or k.shape != v.shape or k.stride() != v.stride() or k.stride(3) != 1:
+        raise ValueError("k and v must be 4-D with equal shapes and strides, head_dim unit-stride")
+    c = MdKvCache()
+    paged = page_table is not None
+    c.num_seqs = int(num_seqs if num_seqs is not None else
+                     (page_table.shape[0] if paged else k.shape[0]))
+    c.num_kv_heads, c.head_dim = k.shape[2], k.shape[3]
+    c.dtype = _dtype_code(k)
+    if _dtype_code(v) != c.dtype:
+        raise ValueError("k and v must share a dtype")
+    c.k, c.v = k.data_ptr(), v.data_ptr()
+    c.kv_stride_blk, c.kv_stride_tok, c.kv_stride_head = k.stride(0), k.stride(1), k.stride(2)
+    if paged:
+        if page_table.dtype != torch.int32 or not page_table.is_contiguous():
+            raise ValueError("page_table must be contiguous int32 [B, max_pages]")
+        c.page_size, c.max_pages_per_seq = k.shape[1], page_table.shape[1]
+        c.num_pages = k.shape[0]
+        c.page_table = page_table.data_ptr()
+    else:
+        if c.num_seqs > k.shape[0]:
+            raise ValueError("contiguous k/v must hold num_seqs sequences")
+        c.capacity = k.shape[1]
+    return c
+
+
+def md_kv_append(k, v, k_new, v_new, pos0, *, page_table=None, lens_out=None, stream=None):
+    """Write k_new/v_new [B, n_new, Hkv, d] at positions pos0[b] + i of the cache
+    (in place).  Returns lens_out [B] int32 = pos0 + n_new."""
+    import torch
+    lib = load_library()
+    B, n_new = k_new.shape[:2]
+    if k_new.shape != v_new.shape or not k_new.is_contiguous() or not v_new.is_contiguous():
+        raise ValueError("k_new and v_new must be contiguous [B, n_new, Hkv, d] of equal shape")
+    if k_new.dtype != k.dtype or v_new.dtype != v.dtype:
+        raise ValueError("appended rows must have the cache dtype")
+    c = make_kv_cache(k, v, num_seqs=B, page_table=page_table)
+    if B and (k_new.shape[2] != c.num_kv_heads or k_new.shape[3] != c.head_dim):
+        raise ValueError("appended rows must have the cache's heads and head_dim")
+    if lens_out is None:
+        lens_out = torch.empty((B,), dtype=torch.int32, device=k.device)
+    _check(lib.md_kv_append(ctypes.byref(c), n_new, _ptr(k_new), _ptr(v_new), _ptr(pos0),
+                            _ptr(lens_out), _stream_handle(k, stream)))
+    return lens_out
+
+
+def md_greedy_accept(logits, draft, *, accepted=None, tokens=None, target=None,
+                     want_target=True, workspace=None, stream=None):
+    """logits [B, gamma + 1, vocab] float32/bfloat16, draft [B, gamma] int32 ->
+    (accepted [B], tokens [B, gamma + 1], target [B, gamma + 1] or None), int32."""
+    import torch
+    lib = load_library()
+    B, L, vocab = logits.shape
+    if not logits.is_contiguous():
+        raise ValueError("logits must be contiguous [B, gamma + 1, vocab]")
+    if draft.shape != (B, L - 1) or draft.dtype != torch.int32 or not draft.is_contiguous():
+        raise ValueError("draft must be contiguous int32 [B, gamma]")
+    dev = logits.device
+    if accepted is None:
+        accepted = torch.empty((B,), dtype=torch.int32, device=dev)
+    if tokens is None:
+        tokens = torch.empty((B, L), dtype=torch.int32, device=dev)
+    if target is None and want_target:
+        target = torch.empty((B, L), dtype=torch.int32, device=dev)
+    if workspace is None:
+        nbytes = lib.md_greedy_accept_workspace_bytes(B, L - 1, vocab)
+        workspace = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=dev)
+    _check(lib.md_greedy_accept(B, L - 1, vocab, _dtype_code(logits), _ptr(logits),
+                                _ptr(draft) if L > 1 else None, _ptr(accepted), _ptr(tokens),
+                                _ptr(target), _ptr(workspace),
+                                workspace.numel() * workspace.element_size(),
+                                _stream_handle(logits, stream)))
+    return accepted, tokens, target
+
+
+def md_kv_commit(lens, accepted, q_len, *, idx=None, ring_start=0, ring_len=None, stream=None):
+    """lens [B] int32 in place: C -> C + accepted + 1; with idx [B, Hkv, stride]
+    the kept positions also enter each list's ring [ring_start, ring_start + ring_len)."""
+    lib = load_library()
+    B = lens.shape[0]
+    Hkv, stride = (idx.shape[1], idx.shape[2]) if idx is not None else (0, 0)
+    if idx is not None and not idx.is_contiguous():
+        raise ValueError("idx must be contiguous [B, Hkv, stride]")
+    if ring_len is None:
+        ring_len = stride - ring_start
+    _check(lib.md_kv_commit(B, q_len, _ptr(lens), _ptr(accepted), Hkv, _ptr(idx), stride,
+                            ring_start, ring_len, _stream_handle(lens, stream)))
+    return lens
+
+
+def md_streaming_list(prompt_lens, num_kv_heads, n_sink, window, *, idx=None, idx_len=None,
+                      stream=None):
+    """Sink-plus-window draft lists [B, Hkv, n_sink + window] and idx_len [B]."""
+    import torch
+    lib = load_library()
+    B = prompt_lens.shape[0]
+    dev = prompt_lens.device
+    if idx is None:
+        idx = torch.empty((B, num_kv_heads, n_sink + window), dtype=torch.int32, device=dev)
+    if idx_len is None:
+        idx_len = torch.empty((B,), dtype=torch.int32, device=dev)
+    _check(lib.md_streaming_list(B, num_kv_heads, _ptr(prompt_lens), n_sink, window, _ptr(idx),
+                                 _ptr(idx_len), _stream_handle(prompt_lens, stream)))
+    return idx, idx_len
+
+
 # Short aliases.
 verify_attn = md_verify_attn
 draft_attn = md_draft_attn
 draft_attn_indexed = md_draft_attn_indexed
 merge_lse = md_merge_lse
 workspace_bytes = md_workspace_bytes
+kv_append = md_kv_append
+greedy_accept = md_greedy_accept
+kv_commit = md_kv_commit
+streaming_list = md_streaming_list

@@ -272,6 +272,119 @@ int md_snapkv_select(int32_t num_seqs, int32_t num_kv_heads, const float* votes,
   return e == hipSuccess ? MD_OK : md::hip_fail(e);
 }
 
+int md_kv_append(const md_kv_cache* c, int32_t n_new, const void* k_new, const void* v_new,
+                 const int32_t* pos0, int32_t* lens_out, void* stream) {
+  const int st = md::validate_kv_cache(c, n_new);
+  if (st != MD_OK) return st;
+  if (c->num_seqs == 0 || n_new == 0) return MD_OK;
+  if (!c->k || !c->v || !k_new || !v_new || !pos0) return MD_ERR_INVALID_ARG;
+  if (!md::aligned16(c->k) || !md::aligned16(c->v) || !md::aligned16(k_new) ||
+      !md::aligned16(v_new) || (reinterpret_cast<uintptr_t>(pos0) & 3u) ||
+      (reinterpret_cast<uintptr_t>(lens_out) & 3u))
+    return MD_ERR_INVALID_ARG;
+  if (lens_out == pos0) return MD_ERR_INVALID_ARG;
+  const int es = c->dtype == MD_BF16 ? 2 : 4;
+  md::AppendParams p{};
+  p.k_new = static_cast<const unsigned char*>(k_new);
+  p.v_new = static_cast<const unsigned char*>(v_new);
+  p.k = static_cast<unsigned char*>(c->k);
+  p.v = static_cast<unsigned char*>(c->v);
+  p.s_blk = c->kv_stride_blk;
+  p.s_tok = c->kv_stride_tok;
+  p.s_head = c->kv_stride_head;
+  p.esize = es;
+  p.page_table = c->page_table;
+  p.page_shift = 0;
+  if (c->page_size)
+    while ((1 << p.page_shift) < c->page_size) ++p.page_shift;
+  p.max_pages = c->max_pages_per_seq;
+  p.num_pages = c->num_pages;
+  p.capacity = c->capacity;
+  p.pos0 = pos0;
+  p.lens_out = lens_out;
+  p.B = c->num_seqs;
+  p.n_new = n_new;
+  p.Hkv = c->num_kv_heads;
+  p.row_vecs = c->head_dim * es / 16;
+  p.n_items = 2 * static_cast<int64_t>(c->num_seqs) * n_new * c->num_kv_heads * p.row_vecs;
+  const hipError_t e = md::launch_kv_append(p, c->page_size != 0, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? MD_OK : md::hip_fail(e);
+}
+
+size_t md_greedy_accept_workspace_bytes(int32_t num_seqs, int32_t n_draft, int32_t vocab) {
+  if (md::validate_accept(num_seqs, n_draft, vocab, MD_F32) != MD_OK) return 0;
+  return md::make_accept_plan(num_seqs, n_draft, vocab, md::device_cu_count()).workspace_bytes;
+}
+
+int md_greedy_accept(int32_t num_seqs, int32_t n_draft, int32_t vocab, int32_t dtype,
+                     const void* logits, const int32_t* draft, int32_t* accepted,
+                     int32_t* tokens, int32_t* target, void* workspace, size_t workspace_bytes,
+                     void* stream) {
+  const int st = md::validate_accept(num_seqs, n_draft, vocab, dtype);
+  if (st != MD_OK) return st;
+  if (num_seqs == 0) return MD_OK;
+  if (!logits || (n_draft > 0 && !draft) || !accepted || !tokens) return MD_ERR_INVALID_ARG;
+  if (!md::aligned16(logits) || (reinterpret_cast<uintptr_t>(draft) & 3u) ||
+      (reinterpret_cast<uintptr_t>(accepted) & 3u) || (reinterpret_cast<uintptr_t>(tokens) & 3u) ||
+      (reinterpret_cast<uintptr_t>(target) & 3u))
+    return MD_ERR_INVALID_ARG;
+  const md::AcceptPlan pl = md::make_accept_plan(num_seqs, n_draft, vocab, md::device_cu_count());
+  if (!workspace || workspace_bytes < pl.workspace_bytes ||
+      (reinterpret_cast<uintptr_t>(workspace) & 255u))
+    return MD_ERR_WORKSPACE;
+  md::AcceptParams p{};
+  p.logits = logits;
+  p.vocab = vocab;
+  p.n_chunks = pl.n_chunks;
+  p.chunk_len = pl.chunk_len;
+  p.B = num_seqs;
+  p.L = n_draft + 1;
+  p.part_val = static_cast<float*>(workspace);
+  p.part_idx = reinterpret_cast<int32_t*>(static_cast<unsigned char*>(workspace) + pl.part_bytes);
+  p.draft = draft;
+  p.accepted = accepted;
+  p.tokens = tokens;
+  p.target = target;
+  const int epv = dtype == MD_BF16 ? 8 : 4;
+  const hipError_t e = md::launch_greedy_accept(p, dtype == MD_BF16, vocab % epv == 0,
+                                                static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? MD_OK : md::hip_fail(e);
+}
+
+int md_kv_commit(int32_t num_seqs, int32_t q_len, int32_t* lens, const int32_t* accepted,
+                 int32_t num_kv_heads, int32_t* idx, int32_t idx_stride, int32_t ring_start,
+                 int32_t ring_len, void* stream) {
+  if (num_seqs < 0 || q_len < 1) return MD_ERR_INVALID_ARG;
+  if (idx && (num_kv_heads < 1 || idx_stride < 1 || ring_start < 0 || ring_len < 1 ||
+              static_cast<int64_t>(ring_start) + ring_len > idx_stride))
+    return MD_ERR_INVALID_ARG;
+  if (num_seqs == 0) return MD_OK;
+  if (!lens || !accepted || (reinterpret_cast<uintptr_t>(lens) & 3u) ||
+      (reinterpret_cast<uintptr_t>(accepted) & 3u) || (reinterpret_cast<uintptr_t>(idx) & 3u))
+    return MD_ERR_INVALID_ARG;
+  const hipError_t e = md::launch_kv_commit(num_seqs, q_len, lens, accepted, num_kv_heads, idx,
+                                            idx_stride, ring_start, ring_len,
+                                            static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? MD_OK : md::hip_fail(e);
+}
+
+int md_streaming_list(int32_t num_seqs, int32_t num_kv_heads, const int32_t* prompt_lens,
+                      int32_t n_sink, int32_t window, int32_t* idx, int32_t* idx_len,
+                      void* stream) {
+  if (num_seqs < 0 || num_kv_heads < 1 || n_sink < 0 || window < 1 ||
+      static_cast<int64_t>(n_sink) + window > INT32_MAX ||
+      static_cast<int64_t>(num_seqs) * num_kv_heads > INT32_MAX)
+    return MD_ERR_INVALID_ARG;
+  if (num_seqs == 0) return MD_OK;
+  if (!prompt_lens || !idx || !idx_len || (reinterpret_cast<uintptr_t>(prompt_lens) & 3u) ||
+      (reinterpret_cast<uintptr_t>(idx) & 3u) || (reinterpret_cast<uintptr_t>(idx_len) & 3u))
+    return MD_ERR_INVALID_ARG;
+  const hipError_t e = md::launch_streaming_list(num_seqs, num_kv_heads, prompt_lens, n_sink,
+                                                 window, idx, idx_len,
+                                                 static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? MD_OK : md::hip_fail(e);
+}
+
 const char* md_status_str(int status) {
   switch (status) {
     case MD_OK: return "ok";

@@ -62,6 +62,20 @@ struct SnapkvPlan {
 int validate_snapkv(const md_snapkv_args* a);
 SnapkvPlan make_snapkv_plan(const md_snapkv_args* a, int num_cus);
 
+// Greedy acceptance: rows = B * L logits rows, each cut into n_chunks chunks
+// of chunk_len elements (a multiple of 8; every chunk non-empty), one
+// workgroup per chunk, enough of them to fill the device.
+struct AcceptPlan {
+  int32_t n_chunks = 0, chunk_len = 0;
+  size_t part_bytes = 0;       // part_val and part_idx each: [rows][n_chunks] 4-byte
+  size_t workspace_bytes = 0;
+};
+int validate_accept(int32_t num_seqs, int32_t n_draft, int32_t vocab, int32_t dtype);
+AcceptPlan make_accept_plan(int32_t num_seqs, int32_t n_draft, int32_t vocab, int num_cus);
+
+// The KV-cache write target of md_kv_append.
+int validate_kv_cache(const md_kv_cache* c, int32_t n_new);
+
 // Compute units of the current device (cached per device); 256 when no
 // device is visible, so sizes stay defined on a host without a GPU.
 int device_cu_count();

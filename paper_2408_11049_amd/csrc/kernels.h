@@ -83,6 +83,44 @@ hipError_t launch_merge_lse(int n_parts, int64_t n_rows, int head_dim, bool out_
                             const float* o_parts, const float* lse_parts, void* o, float* lse,
                             hipStream_t s);
 
+// The speculative step around verification.
+struct AppendParams {
+  const unsigned char* k_new;  // [B, n_new, Hkv, d] bytes
+  const unsigned char* v_new;
+  unsigned char* k;            // cache base pointers (bytes)
+  unsigned char* v;
+  int64_t s_blk, s_tok, s_head;  // element strides
+  int32_t esize;
+  const int32_t* page_table;
+  int32_t page_shift, max_pages;
+  int64_t num_pages;
+  int32_t capacity;            // contiguous: tokens per sequence block
+  const int32_t* pos0;
+  int32_t* lens_out;
+  int32_t B, n_new, Hkv, row_vecs;  // row_vecs = 16-byte vectors per (token, head) row
+  int64_t n_items;             // 2 * B * n_new * Hkv * row_vecs
+};
+
+struct AcceptParams {
+  const void* logits;          // [rows][vocab]
+  int32_t vocab, n_chunks, chunk_len;  // chunk_len: elements, a multiple of 8
+  int32_t B, L;                // rows = B * L
+  float* part_val;             // [rows][n_chunks]
+  int32_t* part_idx;
+  const int32_t* draft;        // [B, L - 1]
+  int32_t* accepted;
+  int32_t* tokens;             // [B, L]
+  int32_t* target;             // [B, L] or nullptr
+};
+
+hipError_t launch_kv_append(const AppendParams& p, bool paged, hipStream_t s);
+hipError_t launch_greedy_accept(const AcceptParams& p, bool bf16, bool vec, hipStream_t s);
+hipError_t launch_kv_commit(int B, int q_len, int32_t* lens, const int32_t* accepted, int Hkv,
+                            int32_t* idx, int idx_stride, int ring_start, int ring_len,
+                            hipStream_t s);
+hipError_t launch_streaming_list(int B, int Hkv, const int32_t* prompt_lens, int n_sink,
+                                 int window, int32_t* idx, int32_t* idx_len, hipStream_t s);
+
 hipError_t launch_bench_read(const void* buf, size_t bytes, float* sink, int n_blocks,
                              hipStream_t s);
 hipError_t launch_bench_copy(void* dst, const void* src, size_t bytes, int n_blocks,

@@ -3,6 +3,8 @@
 // exercised on a machine without a GPU.
 #include <limits.h>
 
+#include <algorithm>
+
 #include "internal.h"
 
 namespace md {
@@ -189,6 +191,50 @@ SnapkvPlan make_snapkv_plan(const md_snapkv_args* a, int num_cus) {
   p.lse_bytes = align_up(static_cast<size_t>(p.n_units) * p.R * 4, 256);
   p.workspace_bytes = 2 * p.part_bytes + p.lse_bytes;
   return p;
+}
+
+int validate_accept(int32_t num_seqs, int32_t n_draft, int32_t vocab, int32_t dtype) {
+  if (num_seqs < 0 || n_draft < 0 || n_draft > 1023 || vocab < 1) return MD_ERR_INVALID_ARG;
+  if (dtype != MD_F32 && dtype != MD_BF16) return MD_ERR_INVALID_ARG;
+  const int64_t rows = static_cast<int64_t>(num_seqs) * (n_draft + 1);
+  if (rows * 64 > INT32_MAX) return MD_ERR_INVALID_ARG;  // grid bound at the largest split
+  return MD_OK;
+}
+
+AcceptPlan make_accept_plan(int32_t num_seqs, int32_t n_draft, int32_t vocab, int num_cus) {
+  AcceptPlan pl;
+  const int64_t rows = static_cast<int64_t>(num_seqs) * (n_draft + 1);
+  if (rows <= 0 || vocab < 1) return pl;
+  constexpr int64_t kMinChunk = 2048;
+  int64_t n = (8 * static_cast<int64_t>(num_cus) + rows - 1) / rows;
+  n = std::min<int64_t>(n, (vocab + kMinChunk - 1) / kMinChunk);
+  n = std::max<int64_t>(1, std::min<int64_t>(n, 64));
+  int64_t len = (vocab + n - 1) / n;
+  len = (len + 7) / 8 * 8;
+  pl.chunk_len = static_cast<int32_t>(len);
+  pl.n_chunks = static_cast<int32_t>((vocab + len - 1) / len);
+  pl.part_bytes = align_up(static_cast<size_t>(rows) * pl.n_chunks * 4, 256);
+  pl.workspace_bytes = 2 * pl.part_bytes;
+  return pl;
+}
+
+int validate_kv_cache(const md_kv_cache* c, int32_t n_new) {
+  if (!c || n_new < 0) return MD_ERR_INVALID_ARG;
+  if (c->num_seqs < 0 || c->num_kv_heads < 1 || c->head_dim < 1) return MD_ERR_INVALID_ARG;
+  if (c->dtype != MD_F32 && c->dtype != MD_BF16) return MD_ERR_INVALID_ARG;
+  const int64_t es = c->dtype == MD_BF16 ? 2 : 4;
+  if ((c->head_dim * es) % 16) return MD_ERR_INVALID_ARG;
+  if (c->kv_stride_blk < 0 || c->kv_stride_tok < 0 || c->kv_stride_head < 0 ||
+      (c->kv_stride_blk * es) % 16 || (c->kv_stride_tok * es) % 16 || (c->kv_stride_head * es) % 16)
+    return MD_ERR_INVALID_ARG;
+  if (c->page_size != 0) {
+    if (c->page_size < 0 || (c->page_size & (c->page_size - 1)) || !c->page_table ||
+        c->max_pages_per_seq < 1 || c->num_pages < 1)
+      return MD_ERR_INVALID_ARG;
+  } else {
+    if (c->page_table || c->capacity < 1) return MD_ERR_INVALID_ARG;
+  }
+  return MD_OK;
 }
 
 }  // namespace md

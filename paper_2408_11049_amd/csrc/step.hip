@@ -1,0 +1,293 @@
+// step.hip -- the kernels on either side of verification in one speculative
+// step (Sec. 3.1; greedy decoding, Sec. 5.1):
+//
+//   kv_append       writes the gamma+1 verified tokens' K/V rows into the
+//                   cache (contiguous or paged), 16 bytes per thread;
+//   argmax_partial  first pass of greedy acceptance: each workgroup reduces
+//                   one chunk of one logits row to (largest value, first
+//                   index);
+//   accept          second pass, one wave per sequence: reduces each row's
+//                   chunks to the target token, then walks the rows in order
+//                   to count the leading matching drafts and emit the bonus;
+//   kv_commit       C' = C + a + 1, recording the kept positions in the
+//                   rolling ring of a listed draft cache;
+//   streaming_list  the sink-plus-window lists a StreamingLLM-style draft
+//                   cache starts from at prefill.
+//
+// All of them are bound by HBM or by launch latency; none is a contraction.
+#include <hip/hip_runtime.h>
+#include <limits.h>
+
+#include "kernels.h"
+
+namespace md {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------- append --
+
+template <bool PAGED>
+__global__ void __launch_bounds__(256) kv_append_kernel(const AppendParams p) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * 256;
+  for (int64_t item = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; item < p.n_items;
+       item += stride) {
+    int64_t r = item;
+    const int c = static_cast<int>(r % p.row_vecs);
+    r /= p.row_vecs;
+    const int hk = static_cast<int>(r % p.Hkv);
+    r /= p.Hkv;
+    const int i = static_cast<int>(r % p.n_new);
+    r /= p.n_new;
+    const int b = static_cast<int>(r % p.B);
+    const bool is_v = r >= p.B;
+
+    const int32_t base = p.pos0[b];
+    if (!is_v && i == 0 && hk == 0 && c == 0 && p.lens_out) p.lens_out[b] = base + p.n_new;
+    const int64_t j = static_cast<int64_t>(base) + i;
+    if (j < 0) continue;
+    int64_t blk, tok;
+    if (PAGED) {
+      const int64_t pg = j >> p.page_shift;
+      if (pg >= p.max_pages) continue;
+      blk = p.page_table[static_cast<int64_t>(b) * p.max_pages + pg];
+      if (blk < 0 || blk >= p.num_pages) continue;
+      tok = j & ((int64_t{1} << p.page_shift) - 1);
+    } else {
+      if (j >= p.capacity) continue;
+      blk = b;
+      tok = j;
+    }
+    const int64_t src = ((static_cast<int64_t>(b) * p.n_new + i) * p.Hkv + hk) * p.row_vecs + c;
+    const int64_t dst = (blk * p.s_blk + tok * p.s_tok + hk * p.s_head) * p.esize + c * 16;
+    const uint4 val = reinterpret_cast<const uint4*>(is_v ? p.v_new : p.k_new)[src];
+    *reinterpret_cast<uint4*>((is_v ? p.v : p.k) + dst) = val;
+  }
+}
+
+hipError_t launch_kv_append(const AppendParams& p, bool paged, hipStream_t s) {
+  const int64_t want = (p.n_items + 255) / 256;
+  const uint32_t blocks = static_cast<uint32_t>(want < (1 << 20) ? want : (1 << 20));
+  if (paged)
+    hipLaunchKernelGGL(kv_append_kernel<true>, dim3(blocks), dim3(256), 0, s, p);
+  else
+    hipLaunchKernelGGL(kv_append_kernel<false>, dim3(blocks), dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- accept --
+
+// Keep the larger value; between equal values the smaller index.  NaN never
+// reaches here (it is read as -inf), so the order is total and any reduction
+// order gives the same (value, index).
+__device__ __forceinline__ void take(float& bv, int& bi, float v, int i) {
+  if (v > bv || (v == bv && i < bi)) {
+    bv = v;
+    bi = i;
+  }
+}
+
+__device__ __forceinline__ void wave_take(float& bv, int& bi) {
+  for (int off = 32; off > 0; off >>= 1) {
+    const float ov = __shfl_xor(bv, off);
+    const int oi = __shfl_xor(bi, off);
+    take(bv, bi, ov, oi);
+  }
+}
+
+__device__ __forceinline__ float logit_value(float v) { return v != v ? -INFINITY : v; }
+
+template <bool BF16>
+__device__ __forceinline__ float load_logit(const void* base, int64_t e) {
+  if (BF16) {
+    const uint32_t u = static_cast<const uint16_t*>(base)[e];
+    return logit_value(__uint_as_float(u << 16));
+  }
+  return logit_value(static_cast<const float*>(base)[e]);
+}
+
+// One workgroup per (row, chunk); block = row * n_chunks + chunk.  VEC: the
+// rows start 16-byte aligned (vocab a multiple of the vector width), so each
+// thread streams 16-byte vectors, four in flight.
+template <bool BF16, bool VEC>
+__global__ void __launch_bounds__(256) argmax_partial_kernel(const AcceptParams p) {
+  constexpr int EPV = BF16 ? 8 : 4;  // elements per 16-byte vector
+  constexpr int U = 4;
+  const int64_t row = blockIdx.x / p.n_chunks;
+  const int chunk = static_cast<int>(blockIdx.x % p.n_chunks);
+  const int c0 = chunk * p.chunk_len;
+  const int c1 = min(p.vocab, c0 + p.chunk_len);
+  const int tid = threadIdx.x;
+  float bv = -INFINITY;
+  int bi = INT_MAX;
+  const unsigned char* rowp =
+      static_cast<const unsigned char*>(p.logits) + row * p.vocab * (BF16 ? 2 : 4);
+  if (VEC) {
+    const u32x4* vp = reinterpret_cast<const u32x4*>(rowp);
+    const int v0 = c0 / EPV, v1 = c1 / EPV;
+    for (int v = v0 + tid; v < v1; v += 256 * U) {
+      u32x4 x[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int vv = v + u * 256;
+        // Out-of-range lanes re-read the first vector of the chunk (in bounds)
+        // and are discarded below.
+        x[u] = __builtin_nontemporal_load(vp + (vv < v1 ? vv : v0));
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int vv = v + u * 256;
+        if (vv >= v1) continue;
+        const uint32_t w[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (BF16) {
+            take(bv, bi, logit_value(__uint_as_float(w[e] << 16)), vv * EPV + 2 * e);
+            take(bv, bi, logit_value(__uint_as_float(w[e] & 0xffff0000u)), vv * EPV + 2 * e + 1);
+          } else {
+            take(bv, bi, logit_value(__uint_as_float(w[e])), vv * EPV + e);
+          }
+        }
+      }
+    }
+  } else {
+    for (int e = c0 + tid; e < c1; e += 256) take(bv, bi, load_logit<BF16>(rowp, e), e);
+  }
+  wave_take(bv, bi);
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  const int wave = tid >> 6;
+  if ((tid & 63) == 0) {
+    sv[wave] = bv;
+    si[wave] = bi;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    for (int w = 1; w < 4; ++w) take(bv, bi, sv[w], si[w]);
+    p.part_val[blockIdx.x] = bv;
+    p.part_idx[blockIdx.x] = bi;
+  }
+}
+
+// One wave per sequence: rows in order, each reduced over its chunks, then
+// the acceptance walk (uniform across the wave).
+__global__ void __launch_bounds__(64) accept_kernel(const AcceptParams p) {
+  const int b = blockIdx.x;
+  const int lane = threadIdx.x;
+  int a = 0;
+  bool running = true;
+  for (int i = 0; i < p.L; ++i) {
+    const int64_t row = static_cast<int64_t>(b) * p.L + i;
+    float bv = -INFINITY;
+    int bi = INT_MAX;
+    for (int c = lane; c < p.n_chunks; c += 64)
+      take(bv, bi, p.part_val[row * p.n_chunks + c], p.part_idx[row * p.n_chunks + c]);
+    wave_take(bv, bi);
+    const int t = bi == INT_MAX ? 0 : bi;
+    int tok = -1;
+    if (running) {
+      const int d = i < p.L - 1 ? p.draft[static_cast<int64_t>(b) * (p.L - 1) + i] : -1;
+      if (i < p.L - 1 && d == t) {
+        tok = d;
+        ++a;
+      } else {
+        tok = t;
+        running = false;
+      }
+    }
+    if (lane == 0) {
+      p.tokens[row] = tok;
+      if (p.target) p.target[row] = t;
+    }
+  }
+  if (lane == 0) p.accepted[b] = a;
+}
+
+hipError_t launch_greedy_accept(const AcceptParams& p, bool bf16, bool vec, hipStream_t s) {
+  const uint32_t blocks = static_cast<uint32_t>(static_cast<int64_t>(p.B) * p.L * p.n_chunks);
+  if (bf16) {
+    if (vec)
+      hipLaunchKernelGGL((argmax_partial_kernel<true, true>), dim3(blocks), dim3(256), 0, s, p);
+    else
+      hipLaunchKernelGGL((argmax_partial_kernel<true, false>), dim3(blocks), dim3(256), 0, s, p);
+  } else {
+    if (vec)
+      hipLaunchKernelGGL((argmax_partial_kernel<false, true>), dim3(blocks), dim3(256), 0, s, p);
+    else
+      hipLaunchKernelGGL((argmax_partial_kernel<false, false>), dim3(blocks), dim3(256), 0, s, p);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(accept_kernel, dim3(p.B), dim3(64), 0, s, p);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- commit --
+
+// One wave per sequence.  Every lane reads lens[b] before the barrier; lane 0
+// writes the new length after it.
+__global__ void __launch_bounds__(64)
+kv_commit_kernel(int q_len, int32_t* __restrict__ lens, const int32_t* __restrict__ accepted,
+                 int Hkv, int32_t* __restrict__ idx, int idx_stride, int ring_start,
+                 int ring_len) {
+  const int b = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int C = lens[b];
+  int a = accepted[b];
+  a = a < 0 ? 0 : (a > q_len - 1 ? q_len - 1 : a);
+  if (idx) {
+    // Only the last ring_len kept positions survive in the ring.
+    const int n_keep = a + 1 < ring_len ? a + 1 : ring_len;
+    const int first = C + a + 1 - n_keep;
+    for (int t = lane; t < n_keep * Hkv; t += 64) {
+      const int j = first + t / Hkv;
+      const int hk = t % Hkv;
+      if (j < 0) continue;
+      idx[(static_cast<int64_t>(b) * Hkv + hk) * idx_stride + ring_start + j % ring_len] = j;
+    }
+  }
+  __syncthreads();
+  if (lane == 0) lens[b] = C + a + 1;
+}
+
+hipError_t launch_kv_commit(int B, int q_len, int32_t* lens, const int32_t* accepted, int Hkv,
+                            int32_t* idx, int idx_stride, int ring_start, int ring_len,
+                            hipStream_t s) {
+  hipLaunchKernelGGL(kv_commit_kernel, dim3(B), dim3(64), 0, s, q_len, lens, accepted, Hkv, idx,
+                     idx_stride, ring_start, ring_len);
+  return hipGetLastError();
+}
+
+// --------------------------------------------------------- streaming list --
+
+// One workgroup per (sequence, kv head) list.  Ring slot n_sink + r holds the
+// one position j in [max(n_sink, C - window), C) with j % window == r.
+__global__ void __launch_bounds__(256)
+streaming_list_kernel(int Hkv, const int32_t* __restrict__ prompt_lens, int n_sink, int window,
+                      int32_t* __restrict__ idx, int32_t* __restrict__ idx_len) {
+  const int64_t list = blockIdx.x;
+  const int b = static_cast<int>(list / Hkv);
+  const int C = prompt_lens[b];
+  const int n = n_sink + window;
+  const int lo = C - window > n_sink ? C - window : n_sink;
+  for (int s = threadIdx.x; s < n; s += 256) {
+    int val = -1;
+    if (s < n_sink) {
+      val = s < C ? s : -1;
+    } else if (lo < C) {
+      const int r = s - n_sink;
+      const int j = lo + ((r - lo % window) % window + window) % window;
+      val = j < C ? j : -1;
+    }
+    idx[list * n + s] = val;
+  }
+  if (list % Hkv == 0 && threadIdx.x == 0) idx_len[b] = n;
+}
+
+hipError_t launch_streaming_list(int B, int Hkv, const int32_t* prompt_lens, int n_sink,
+                                 int window, int32_t* idx, int32_t* idx_len, hipStream_t s) {
+  hipLaunchKernelGGL(streaming_list_kernel, dim3(static_cast<uint32_t>(int64_t{B} * Hkv)),
+                     dim3(256), 0, s, Hkv, prompt_lens, n_sink, window, idx, idx_len);
+  return hipGetLastError();
+}
+
+}  // namespace md

@@ -8,7 +8,8 @@ in for the PG-19 / RULER prompts the paper decodes (Sec. 5.1, 5.2), which are
 not used.
 
 Seeds: workload ``base`` uses generator streams ``base*10 + s`` with
-s = 0 Q, 1 K, 2 V, 3 lengths, 4 page placement, 5 outlier channels.
+s = 0 Q, 1 K, 2 V, 3 lengths, 4 page placement, 5 outlier channels,
+6 logits, 7 planted tokens and drafts, 8 appended K/V rows.
 
 Padding that a correct kernel never reads (tokens past kv_lens[b] in a
 contiguous cache, slots past the end in a sequence's last page, pages owned by
@@ -23,7 +24,8 @@ from typing import Optional
 import numpy as np
 import torch
 
-STREAM_Q, STREAM_K, STREAM_V, STREAM_LEN, STREAM_PAGE, STREAM_OUTLIER = range(6)
+(STREAM_Q, STREAM_K, STREAM_V, STREAM_LEN, STREAM_PAGE, STREAM_OUTLIER, STREAM_LOGITS,
+ STREAM_DRAFT, STREAM_NEW_KV) = range(9)
 
 
 @dataclasses.dataclass(frozen=True)
@@ -235,3 +237,61 @@ def gather_unit(case: dict, b: int, hk: int):
         k = case["k"].index_select(0, pages)[:, :, hk: hk + 1, :].reshape(1, npg * ps, 1, -1)[:, :S_b]
         v = case["v"].index_select(0, pages)[:, :, hk: hk + 1, :].reshape(1, npg * ps, 1, -1)[:, :S_b]
     return (to_host_bits(q), to_host_bits(k), to_host_bits(v), np.array([S_b], dtype=np.int32))
+
+
+def new_kv_rows(B, n_new, Hkv, d, dtype="bf16", seed=0, device="cpu"):
+    """K and V rows of n_new new tokens per sequence, [B, n_new, Hkv, d], N(0, 1)."""
+    g = _gen(seed * 10 + STREAM_NEW_KV, device)
+    tdt = torch_dtype(dtype)
+    k = torch.randn((B, n_new, Hkv, d), generator=g, device=device).to(tdt)
+    v = torch.randn((B, n_new, Hkv, d), generator=g, device=device).to(tdt)
+    return k, v
+
+
+# Planted logit: far above any N(0, 1) draw and exact in bf16.
+PLANTED_LOGIT = 64.0
+
+
+def step_logits(B, gamma, vocab, dtype="f32", seed=0, device="cpu", accept=None, ties=0,
+                nan_rows=0, neg_inf_rows=0):
+    """Seeded verifier logits and drafts for one greedy-acceptance step.
+
+    logits [B, gamma + 1, vocab]: N(0, 1) with one planted logit PLANTED_LOGIT
+    per row, at token planted[b, i] (drawn uniformly).  draft [B, gamma]
+    int32 copies planted[b, :a_b] and then differs from the planted token at
+    a_b (a_b = accept[b], default uniform in 0..gamma), random after.
+    ties: rows (seeded) that also carry PLANTED_LOGIT at a second token;
+    nan_rows / neg_inf_rows: rows turned entirely NaN / -inf except for the
+    first half, which is NaN (for the -inf rows), so only -inf values remain.
+    Returns (logits, draft, planted [B, gamma + 1] int64 numpy, accept numpy)."""
+    L = gamma + 1
+    g = _gen(seed * 10 + STREAM_LOGITS, device)
+    x = torch.randn((B, L, vocab), generator=g, device=device, dtype=torch.float32)
+    gd = _gen(seed * 10 + STREAM_DRAFT, "cpu")
+    planted = torch.randint(0, vocab, (B, L), generator=gd).numpy()
+    if accept is None:
+        accept = torch.randint(0, gamma + 1, (B,), generator=gd).numpy()
+    accept = np.asarray(accept, dtype=np.int64)
+    draft = torch.randint(0, vocab, (B, max(gamma, 1)), generator=gd).numpy()[:, :gamma].copy()
+    for b in range(B):
+        draft[b, : accept[b]] = planted[b, : accept[b]]
+        if accept[b] < gamma:
+            draft[b, accept[b]] = (planted[b, accept[b]] + 1) % vocab
+    rows = torch.randperm(B * L, generator=gd).numpy()
+    tie_rows = rows[:ties]
+    nan_r = rows[ties: ties + nan_rows]
+    inf_r = rows[ties + nan_rows: ties + nan_rows + neg_inf_rows]
+    tie_tok = torch.randint(0, vocab, (max(ties, 1),), generator=gd).numpy()
+    bi = torch.arange(B).repeat_interleave(L).numpy()
+    ii = torch.arange(L).repeat(B).numpy()
+    x[torch.as_tensor(bi), torch.as_tensor(ii), torch.as_tensor(planted.reshape(-1))] = PLANTED_LOGIT
+    for n, r in enumerate(tie_rows):
+        x[bi[r], ii[r], int(tie_tok[n])] = PLANTED_LOGIT
+    for r in nan_r:
+        x[bi[r], ii[r]] = float("nan")
+    for r in inf_r:
+        x[bi[r], ii[r]] = float("-inf")
+        x[bi[r], ii[r], : vocab // 2] = float("nan")
+    logits = x.to(torch_dtype(dtype))
+    return (logits, torch.from_numpy(draft.astype(np.int32)).to(device),
+            planted.astype(np.int64), accept)

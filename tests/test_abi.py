@@ -255,3 +255,136 @@ def test_bench_helpers_reject_bad_args(lib):
     assert lib.md_bench_stream_read(FAKE, 17, FAKE, None) == md.MD_ERR_INVALID_ARG
     assert lib.md_bench_copy(FAKE, FAKE + 4, 32, None) == md.MD_ERR_INVALID_ARG
     assert lib.md_bench_fill(FAKE + 8, 32, 0, None) == md.MD_ERR_INVALID_ARG
+
+
+def good_cache(**over):
+    c = md.MdKvCache()
+    c.num_seqs, c.num_kv_heads, c.head_dim, c.dtype = 2, 2, 128, md.MD_BF16
+    c.k, c.v = FAKE, FAKE + 0x1000
+    c.kv_stride_blk, c.kv_stride_tok, c.kv_stride_head = 64 * 2 * 128, 2 * 128, 128
+    c.capacity = 64
+    for k, v in over.items():
+        setattr(c, k, v)
+    return c
+
+
+APPEND_BAD = [
+    ("negative n_new", {}, -1),
+    ("zero heads", {"num_kv_heads": 0}, 3),
+    ("bad dtype", {"dtype": 7}, 3),
+    ("row not 16-byte multiple", {"head_dim": 4}, 3),
+    ("stride not 16-byte multiple", {"kv_stride_tok": 100}, 3),
+    ("zero capacity", {"capacity": 0}, 3),
+    ("table without page size", {"page_table": FAKE}, 3),
+    ("page size not a power of two", {"page_size": 12, "page_table": FAKE,
+                                      "max_pages_per_seq": 4, "num_pages": 8}, 3),
+    ("paged without pages", {"page_size": 16, "page_table": FAKE, "max_pages_per_seq": 4,
+                             "num_pages": 0}, 3),
+    ("misaligned cache", {"k": FAKE + 4}, 3),
+    ("null cache", {"v": None}, 3),
+]
+
+
+@pytest.mark.parametrize("name,over,n_new", APPEND_BAD, ids=[b[0] for b in APPEND_BAD])
+def test_kv_append_rejects(lib, name, over, n_new):
+    c = good_cache(**over)
+    st = lib.md_kv_append(ctypes.byref(c), n_new, FAKE, FAKE, FAKE, FAKE + 64, None)
+    assert st == md.MD_ERR_INVALID_ARG
+
+
+def test_kv_append_pointer_rules(lib):
+    c = good_cache()
+    ap = lib.md_kv_append
+    assert ap(None, 3, FAKE, FAKE, FAKE, None, None) == md.MD_ERR_INVALID_ARG
+    assert ap(ctypes.byref(c), 3, FAKE, FAKE, FAKE, FAKE, None) == md.MD_ERR_INVALID_ARG  # lens_out == pos0
+    assert ap(ctypes.byref(c), 3, FAKE + 8, FAKE, FAKE, None, None) == md.MD_ERR_INVALID_ARG
+    assert ap(ctypes.byref(c), 3, FAKE, FAKE, None, None, None) == md.MD_ERR_INVALID_ARG
+    assert ap(ctypes.byref(c), 3, FAKE, FAKE, FAKE + 2, None, None) == md.MD_ERR_INVALID_ARG
+    # nothing to write: no launch, no pointer read
+    assert ap(ctypes.byref(c), 0, None, None, None, None, None) == md.MD_OK
+    assert ap(ctypes.byref(good_cache(num_seqs=0)), 5, None, None, None, None, None) == md.MD_OK
+
+
+def test_greedy_accept_args(lib):
+    ga = lib.md_greedy_accept
+    ws = lib.md_greedy_accept_workspace_bytes(64, 4, 128256)
+    assert ws > 0 and ws % 256 == 0
+    assert lib.md_greedy_accept_workspace_bytes(64, -1, 128256) == 0
+    assert lib.md_greedy_accept_workspace_bytes(64, 4, 0) == 0
+    ok = (64, 4, 128256, md.MD_F32, FAKE, FAKE, FAKE, FAKE, None, FAKE, ws, None)
+
+    def call(**over):
+        names = ["B", "n_draft", "vocab", "dtype", "logits", "draft", "accepted", "tokens",
+                 "target", "ws", "ws_bytes", "stream"]
+        args = dict(zip(names, ok))
+        args.update(over)
+        return ga(*[args[n] for n in names])
+
+    assert call(n_draft=-1) == md.MD_ERR_INVALID_ARG
+    assert call(n_draft=1024) == md.MD_ERR_INVALID_ARG
+    assert call(vocab=0) == md.MD_ERR_INVALID_ARG
+    assert call(dtype=5) == md.MD_ERR_INVALID_ARG
+    assert call(logits=None) == md.MD_ERR_INVALID_ARG
+    assert call(logits=FAKE + 4) == md.MD_ERR_INVALID_ARG
+    assert call(draft=None) == md.MD_ERR_INVALID_ARG
+    assert call(tokens=None) == md.MD_ERR_INVALID_ARG
+    assert call(accepted=FAKE + 1) == md.MD_ERR_INVALID_ARG
+    assert call(ws=None) == md.MD_ERR_WORKSPACE
+    assert call(ws_bytes=ws - 1) == md.MD_ERR_WORKSPACE
+    assert call(ws=FAKE + 16) == md.MD_ERR_WORKSPACE
+    assert call(B=0, logits=None, draft=None, accepted=None, tokens=None, ws=None) == md.MD_OK
+
+
+def test_accept_plan_splits_long_rows(lib):
+    # Few rows: more chunks per row (more workspace); the workspace stays tiny.
+    few = lib.md_greedy_accept_workspace_bytes(1, 4, 128256)
+    many = lib.md_greedy_accept_workspace_bytes(256, 4, 128256)
+    assert 0 < few <= 2 * 256 * ((5 * 64 * 4 + 255) // 256)
+    assert many > 0 and many < 1 << 20
+
+
+def test_kv_commit_args(lib):
+    kc = lib.md_kv_commit
+    assert kc(2, 0, FAKE, FAKE, 0, None, 0, 0, 0, None) == md.MD_ERR_INVALID_ARG  # q_len < 1
+    assert kc(2, 5, None, FAKE, 0, None, 0, 0, 0, None) == md.MD_ERR_INVALID_ARG
+    assert kc(2, 5, FAKE, None, 0, None, 0, 0, 0, None) == md.MD_ERR_INVALID_ARG
+    assert kc(2, 5, FAKE, FAKE, 0, FAKE, 64, 0, 64, None) == md.MD_ERR_INVALID_ARG  # no heads
+    assert kc(2, 5, FAKE, FAKE, 2, FAKE, 64, 16, 49, None) == md.MD_ERR_INVALID_ARG  # past stride
+    assert kc(2, 5, FAKE, FAKE, 2, FAKE, 64, -1, 8, None) == md.MD_ERR_INVALID_ARG
+    assert kc(2, 5, FAKE, FAKE, 2, FAKE, 64, 16, 0, None) == md.MD_ERR_INVALID_ARG
+    assert kc(0, 5, None, None, 2, None, 0, 0, 0, None) == md.MD_OK
+
+
+def test_streaming_list_args(lib):
+    sl = lib.md_streaming_list
+    assert sl(2, 0, FAKE, 4, 8, FAKE, FAKE, None) == md.MD_ERR_INVALID_ARG
+    assert sl(2, 2, FAKE, -1, 8, FAKE, FAKE, None) == md.MD_ERR_INVALID_ARG
+    assert sl(2, 2, FAKE, 4, 0, FAKE, FAKE, None) == md.MD_ERR_INVALID_ARG
+    assert sl(2, 2, None, 4, 8, FAKE, FAKE, None) == md.MD_ERR_INVALID_ARG
+    assert sl(2, 2, FAKE, 4, 8, FAKE + 2, FAKE, None) == md.MD_ERR_INVALID_ARG
+    assert sl(0, 2, None, 4, 8, None, None, None) == md.MD_OK
+
+
+def test_struct_layouts_match_the_header(tmp_path):
+    """Offsets and sizes of every C-ABI struct, as gcc lays them out from the
+    header, equal the binding's ctypes mirrors."""
+    structs = {"md_attn_args": md.MdAttnArgs, "md_snapkv_args": md.MdSnapkvArgs,
+               "md_kv_cache": md.MdKvCache}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "magicdec.h"',
+             "int main(void) {"]
+    for name, cls in structs.items():
+        lines.append(f'  printf("{name} size %zu\\n", sizeof({name}));')
+        for f, _ in cls._fields_:
+            lines.append(f'  printf("{name} {f} %zu\\n", offsetof({name}, {f}));')
+    lines.append("  return 0;\n}")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)],
+                   check=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout
+    got = {tuple(l.split()[:2]): int(l.split()[2]) for l in out.splitlines()}
+    for name, cls in structs.items():
+        assert got[(name, "size")] == ctypes.sizeof(cls), name
+        for f, _ in cls._fields_:
+            assert got[(name, f)] == getattr(cls, f).offset, (name, f)
