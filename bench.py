@@ -246,6 +246,52 @@ def main():
 
     t_draft_idx = timed(draft_idx)
     bytes_idx = int(sum((int(x) + L) for x in n_np)) * w.Hkv * 2 * w.d * w.esize
+
+    # The steps around verification: append the gamma+1 tokens' K/V (new seeded
+    # rows written over the cache's last L positions), greedy
+    # acceptance over fp32 logits at the Llama-3 vocabulary, and the commit
+    # with a rolling 1024-slot ring after the 2049-entry SnapKV-style lists.
+    vocab = 128256
+    k_new, v_new = wl.new_kv_rows(w.B, L, w.Hkv, w.d, w.dtype, seed=w.seed_base, device=dev)
+    pos0 = (c["kv_lens"] - L).contiguous()
+    lens_out = torch.empty_like(pos0)
+
+    def append():
+        md.md_kv_append(c["k"], c["v"], k_new, v_new, pos0, page_table=c["page_table"],
+                        lens_out=lens_out)
+
+    logits, draft_tok, _, _ = wl.step_logits(w.B, w.gamma, vocab, "f32", seed=w.seed_base,
+                                             device=dev)
+    acc = torch.empty((w.B,), dtype=torch.int32, device=dev)
+    toks = torch.empty((w.B, L), dtype=torch.int32, device=dev)
+    ws_acc = torch.empty((lib.md_greedy_accept_workspace_bytes(w.B, w.gamma, vocab),),
+                         dtype=torch.uint8, device=dev)
+
+    def accept():
+        md.md_greedy_accept(logits, draft_tok, accepted=acc, tokens=toks, want_target=False,
+                            workspace=ws_acc)
+
+    ring = 1024
+    lists = torch.full((w.B, w.Hkv, budget + ring), -1, dtype=torch.int32, device=dev)
+    lists[:, :, :budget] = idx_t
+    commit_lens = torch.empty_like(pos0)
+
+    def commit():
+        md.md_kv_commit(commit_lens, acc, L, idx=lists, ring_start=budget, ring_len=ring)
+
+    t_append = timed(append)
+    t_accept = timed(accept)
+    ts = []
+    for _ in range(10):
+        commit_lens.copy_(pos0)
+        do_flush()
+        a_ev, b_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a_ev.record(stream); commit(); b_ev.record(stream)
+        torch.cuda.synchronize()
+        ts.append(a_ev.elapsed_time(b_ev) * 1e3)
+    t_commit = float(np.median(ts))
+    bytes_append = 2 * 2 * w.B * L * w.Hkv * w.d * w.esize  # K and V rows, read + write
+    bytes_logits = logits.numel() * logits.element_size()
     # A plain 1 GiB copy of known size: its FETCH_SIZE / WRITE_SIZE readings
     # calibrate the HBM byte counters of a rocprofv3 --pmc run of this script.
     md._check(lib.md_bench_copy(md.ctypes.c_void_p(flush.data_ptr()),
@@ -263,7 +309,7 @@ def main():
     roofline = {"bound": "hbm", "achieved": round(verify_gbs, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(verify_gbs / HBM_PEAK_GBS, 4),
                 "traffic": traffic,
-                "kernel": "md::attn_partial_kernel<128, true, 2, true, 1, 1> (md_verify_attn)",
+                "kernel": "md::attn_partial_kernel<128, true, 2, true, false, 1, 1> (md_verify_attn)",
                 "algorithmic_bytes_per_launch": bytes_v}
 
     cpu = None
@@ -295,6 +341,14 @@ def main():
             "t_draft_indexed_us (SnapKV-style list, budget 2049)": round(t_draft_idx, 2),
             "draft_indexed_kv_bytes": bytes_idx,
             "draft_indexed_gbs": round(bytes_idx / (t_draft_idx * 1e-6) / 1e9, 1),
+            "t_kv_append_us (gamma+1 tokens, paged)": round(t_append, 2),
+            "kv_append_bytes (read + write)": bytes_append,
+            "t_greedy_accept_us (fp32 logits, vocab 128256)": round(t_accept, 2),
+            "greedy_accept_logits_bytes": bytes_logits,
+            "greedy_accept_gbs": round(bytes_logits / (t_accept * 1e-6) / 1e9, 1),
+            "t_kv_commit_us (lengths + 1024-slot ring)": round(t_commit, 2),
+            "t_sd_full_us (gamma*t_draft(1) + append + verify + accept + commit)": round(
+                w.gamma * t_draft1 + t_append + float(np.mean(tv)) + t_accept + t_commit, 2),
             "verify_kv_bytes": bytes_v, "draft_kv_bytes": bytes_d,
             "verify_gbs": round(verify_gbs, 1),
             "draft_gbs": round(bytes_d / (np.mean(td) * 1e-6) / 1e9, 1),

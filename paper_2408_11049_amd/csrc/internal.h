@@ -65,6 +65,9 @@ SnapkvPlan make_snapkv_plan(const md_snapkv_args* a, int num_cus);
 // Greedy acceptance: rows = B * L logits rows, each cut into n_chunks chunks
 // of chunk_len elements (a multiple of 8; every chunk non-empty), one
 // workgroup per chunk, enough of them to fill the device.
+// The acceptance pass stages one sequence's partials and drafts in LDS.
+constexpr int kAcceptMaxRowsPerSeq = 1024;      // n_draft + 1
+constexpr int kAcceptMaxPartialsPerSeq = 4096;  // (n_draft + 1) * n_chunks
 struct AcceptPlan {
   int32_t n_chunks = 0, chunk_len = 0;
   size_t part_bytes = 0;       // part_val and part_idx each: [rows][n_chunks] 4-byte

@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "internal.h"
 #include "magicdec.h"
 
 namespace md {

@@ -194,7 +194,8 @@ SnapkvPlan make_snapkv_plan(const md_snapkv_args* a, int num_cus) {
 }
 
 int validate_accept(int32_t num_seqs, int32_t n_draft, int32_t vocab, int32_t dtype) {
-  if (num_seqs < 0 || n_draft < 0 || n_draft > 1023 || vocab < 1) return MD_ERR_INVALID_ARG;
+  if (num_seqs < 0 || n_draft < 0 || n_draft + 1 > kAcceptMaxRowsPerSeq || vocab < 1)
+    return MD_ERR_INVALID_ARG;
   if (dtype != MD_F32 && dtype != MD_BF16) return MD_ERR_INVALID_ARG;
   const int64_t rows = static_cast<int64_t>(num_seqs) * (n_draft + 1);
   if (rows * 64 > INT32_MAX) return MD_ERR_INVALID_ARG;  // grid bound at the largest split
@@ -206,8 +207,10 @@ AcceptPlan make_accept_plan(int32_t num_seqs, int32_t n_draft, int32_t vocab, in
   const int64_t rows = static_cast<int64_t>(num_seqs) * (n_draft + 1);
   if (rows <= 0 || vocab < 1) return pl;
   constexpr int64_t kMinChunk = 2048;
+  const int64_t L = n_draft + 1;
   int64_t n = (8 * static_cast<int64_t>(num_cus) + rows - 1) / rows;
   n = std::min<int64_t>(n, (vocab + kMinChunk - 1) / kMinChunk);
+  n = std::min<int64_t>(n, kAcceptMaxPartialsPerSeq / L);  // the accept pass stages L * n in LDS
   n = std::max<int64_t>(1, std::min<int64_t>(n, 64));
   int64_t len = (vocab + n - 1) / n;
   len = (len + 7) / 8 * 8;

@@ -105,9 +105,34 @@ __device__ __forceinline__ float load_logit(const void* base, int64_t e) {
   return logit_value(static_cast<const float*>(base)[e]);
 }
 
+// Element e of a 16-byte vector of logits, widened to fp32 (bf16 holds two
+// per dword, the lower address in the low half).
+template <bool BF16>
+__device__ __forceinline__ float vec_elem(const u32x4& x, int e) {
+  if (BF16) {
+    const uint32_t w = x[e >> 1];
+    return __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+  }
+  return __uint_as_float(x[e]);
+}
+
+// Largest element of the vector; fmaxf drops NaN operands, so NaN counts as
+// nothing (an all-NaN vector gives NaN, which loses every comparison).
+template <bool BF16>
+__device__ __forceinline__ float vec_max(const u32x4& x) {
+  constexpr int EPV = BF16 ? 8 : 4;
+  float m = vec_elem<BF16>(x, 0);
+#pragma unroll
+  for (int e = 1; e < EPV; ++e) m = fmaxf(m, vec_elem<BF16>(x, e));
+  return m;
+}
+
 // One workgroup per (row, chunk); block = row * n_chunks + chunk.  VEC: the
 // rows start 16-byte aligned (vocab a multiple of the vector width), so each
-// thread streams 16-byte vectors, four in flight.
+// thread streams 16-byte vectors, four in flight.  A thread keeps only the
+// first vector holding its largest value (vectors arrive in increasing index
+// order, so a strict comparison keeps the earliest) and resolves the index
+// inside that vector once at the end: a few VALU operations per element.
 template <bool BF16, bool VEC>
 __global__ void __launch_bounds__(256) argmax_partial_kernel(const AcceptParams p) {
   constexpr int EPV = BF16 ? 8 : 4;  // elements per 16-byte vector
@@ -124,6 +149,8 @@ __global__ void __launch_bounds__(256) argmax_partial_kernel(const AcceptParams 
   if (VEC) {
     const u32x4* vp = reinterpret_cast<const u32x4*>(rowp);
     const int v0 = c0 / EPV, v1 = c1 / EPV;
+    int bvec = -1;
+    u32x4 bw = {0u, 0u, 0u, 0u};
     for (int v = v0 + tid; v < v1; v += 256 * U) {
       u32x4 x[U];
 #pragma unroll
@@ -136,18 +163,18 @@ __global__ void __launch_bounds__(256) argmax_partial_kernel(const AcceptParams 
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int vv = v + u * 256;
-        if (vv >= v1) continue;
-        const uint32_t w[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          if (BF16) {
-            take(bv, bi, logit_value(__uint_as_float(w[e] << 16)), vv * EPV + 2 * e);
-            take(bv, bi, logit_value(__uint_as_float(w[e] & 0xffff0000u)), vv * EPV + 2 * e + 1);
-          } else {
-            take(bv, bi, logit_value(__uint_as_float(w[e])), vv * EPV + e);
-          }
+        const float m = vec_max<BF16>(x[u]);
+        if (vv < v1 && m > bv) {
+          bv = m;
+          bvec = vv;
+          bw = x[u];
         }
       }
+    }
+    if (bvec >= 0) {
+#pragma unroll
+      for (int e = EPV - 1; e >= 0; --e)
+        if (vec_elem<BF16>(bw, e) == bv) bi = bvec * EPV + e;
     }
   } else {
     for (int e = c0 + tid; e < c1; e += 256) take(bv, bi, load_logit<BF16>(rowp, e), e);
@@ -168,37 +195,45 @@ __global__ void __launch_bounds__(256) argmax_partial_kernel(const AcceptParams 
   }
 }
 
-// One wave per sequence: rows in order, each reduced over its chunks, then
-// the acceptance walk (uniform across the wave).
+// One wave per sequence.  Every chunk partial of the sequence's rows and its
+// drafts are staged in LDS in one round of loads; lane i then reduces row i
+// to its target token, and a ballot finds the first mismatching draft.
 __global__ void __launch_bounds__(64) accept_kernel(const AcceptParams p) {
+  __shared__ float s_val[kAcceptMaxPartialsPerSeq];
+  __shared__ int s_idx[kAcceptMaxPartialsPerSeq];
+  __shared__ int s_tgt[kAcceptMaxRowsPerSeq];
+  __shared__ int s_draft[kAcceptMaxRowsPerSeq];
   const int b = blockIdx.x;
   const int lane = threadIdx.x;
-  int a = 0;
-  bool running = true;
-  for (int i = 0; i < p.L; ++i) {
-    const int64_t row = static_cast<int64_t>(b) * p.L + i;
+  const int L = p.L, nc = p.n_chunks, n = L * nc;
+  const int64_t base = static_cast<int64_t>(b) * n;  // rows of b are contiguous
+  for (int t = lane; t < n; t += 64) {
+    s_val[t] = p.part_val[base + t];
+    s_idx[t] = p.part_idx[base + t];
+  }
+  for (int i = lane; i < L - 1; i += 64) s_draft[i] = p.draft[static_cast<int64_t>(b) * (L - 1) + i];
+  __syncthreads();
+  for (int i = lane; i < L; i += 64) {
     float bv = -INFINITY;
     int bi = INT_MAX;
-    for (int c = lane; c < p.n_chunks; c += 64)
-      take(bv, bi, p.part_val[row * p.n_chunks + c], p.part_idx[row * p.n_chunks + c]);
-    wave_take(bv, bi);
+    for (int c = 0; c < nc; ++c) take(bv, bi, s_val[i * nc + c], s_idx[i * nc + c]);
     const int t = bi == INT_MAX ? 0 : bi;
-    int tok = -1;
-    if (running) {
-      const int d = i < p.L - 1 ? p.draft[static_cast<int64_t>(b) * (p.L - 1) + i] : -1;
-      if (i < p.L - 1 && d == t) {
-        tok = d;
-        ++a;
-      } else {
-        tok = t;
-        running = false;
-      }
-    }
-    if (lane == 0) {
-      p.tokens[row] = tok;
-      if (p.target) p.target[row] = t;
+    s_tgt[i] = t;
+    if (p.target) p.target[static_cast<int64_t>(b) * L + i] = t;
+  }
+  __syncthreads();
+  // a = the first i < L - 1 whose draft differs from the target (L - 1 if none).
+  int a = L - 1;
+  for (int i0 = 0; i0 < L - 1; i0 += 64) {
+    const int i = i0 + lane;
+    const unsigned long long miss = __ballot(i < L - 1 && s_draft[i] != s_tgt[i]);
+    if (miss) {
+      a = i0 + __ffsll(static_cast<long long>(miss)) - 1;
+      break;
     }
   }
+  for (int i = lane; i < L; i += 64)
+    p.tokens[static_cast<int64_t>(b) * L + i] = i < a ? s_draft[i] : (i == a ? s_tgt[a] : -1);
   if (lane == 0) p.accepted[b] = a;
 }
 
