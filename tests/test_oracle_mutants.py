@@ -122,3 +122,37 @@ def test_sdstep_mutant_is_caught(name, old, new):
         except (AssertionError, ValueError, IndexError):
             caught.append(pin.__name__)
     assert caught, f"no pin catches the planted mistake '{name}'"
+
+
+# Planted mistakes in copies of oracle/costmodel.py.
+COSTMODEL_SRC = os.path.join(os.path.dirname(obuild.__file__), "costmodel.py")
+COSTMODEL_MUTANTS = [
+    ("eq1: exponent gamma", "alpha ** (gamma + 1)", "alpha ** gamma"),
+    ("eq1: alpha = 1 limit gamma", "return float(gamma + 1)", "return float(gamma)"),
+    ("step: drafts not multiplied by gamma", "return gamma * draft_time(", "return 1 * draft_time("),
+    ("eq3: selection ignored", "return t_draft + t_select", "return t_draft"),
+    ("eq2: not divided by Omega", "expected_tokens(gamma, alpha) * t_target)", "1.0 * t_target)"),
+    ("eq4: ties to the larger gamma", "if best is None or r < best[1]:", "if best is None or r <= best[1]:"),
+    ("eq4: gamma off by one", "enumerate(t_verify_by_gamma, start=1)", "enumerate(t_verify_by_gamma, start=0)"),
+    ("inverse: bisection reversed", "if expected_tokens(gamma, mid) < omega:", "if expected_tokens(gamma, mid) > omega:"),
+]
+
+
+@pytest.mark.parametrize("name,old,new", COSTMODEL_MUTANTS, ids=[m[0] for m in COSTMODEL_MUTANTS])
+def test_costmodel_mutant_is_caught(name, old, new):
+    import importlib.util
+
+    from costmodel_pins import ALL_COSTMODEL_PINS
+
+    text = open(COSTMODEL_SRC).read()
+    assert text.count(old) == 1, f"mutation anchor not found once: {old!r}"
+    spec = importlib.util.spec_from_loader("costmodel_mutant", loader=None)
+    mod = importlib.util.module_from_spec(spec)
+    exec(compile(text.replace(old, new), "costmodel_mutant.py", "exec"), mod.__dict__)
+    caught = []
+    for pin in ALL_COSTMODEL_PINS:
+        try:
+            pin(mod=mod)
+        except (AssertionError, ValueError, ZeroDivisionError, TypeError):
+            caught.append(pin.__name__)
+    assert caught, f"no pin catches the planted mistake '{name}'"
