@@ -353,6 +353,39 @@ int md_streaming_list(int32_t num_seqs, int32_t num_kv_heads, const int32_t* pro
                       int32_t n_sink, int32_t window, int32_t* idx, int32_t* idx_len,
                       void* stream);
 
+/*
+ * ---- Speculative-decoding cost model (Sec. 3.1 Eq. 1-2; Sec. 4.1 Eq. 3-4) ----
+ *
+ * Host-only arithmetic (no device, no stream), for choosing the speculation
+ * length from measured times.  Per decoding step of a batch at one sequence
+ * length: t_target = T_T (one token per sequence), t_draft = T_D(B, K) per
+ * drafted token with KV budget K, t_select = T_select(B, S, K) per drafted
+ * token (0 for static selections), t_verify = T_V(gamma), alpha the draft
+ * acceptance rate.  Any consistent time unit.
+ *
+ * md_sd_expected_tokens: Omega(gamma, alpha) = sum_{k=0..gamma} alpha^k, i.e.
+ *   (1 - alpha^(gamma+1)) / (1 - alpha) (Eq. 1), summed so it stays exact to
+ *   rounding as alpha -> 1.  NaN for gamma < 0 or alpha outside [0, 1].
+ * md_sd_latency_ratio: T_Avg^SD / T_T = (gamma (t_draft + t_select) + t_verify)
+ *   / (Omega t_target) (Eq. 2 with Eq. 3's draft time); below 1 means
+ *   speculation is faster.  NaN for invalid arguments (negative times,
+ *   t_target <= 0).
+ * md_sd_best_gamma: Eq. 4 over gamma = 1 .. max_gamma for a fixed budget and
+ *   selection: t_verify[g - 1] = T_V(g) (host array); writes the minimising
+ *   gamma (ties: the smaller) and its ratio.  MD_ERR_INVALID_ARG for
+ *   max_gamma < 1, NULL pointers or invalid times.
+ * md_sd_alpha_from_omega: the alpha in [0, 1] with Omega(gamma, alpha) = omega
+ *   (to ~1e-15), e.g. the acceptance rate implied by a measured Omega; NaN
+ *   outside 1 <= omega <= gamma + 1.
+ */
+double md_sd_expected_tokens(int32_t gamma, double alpha);
+double md_sd_latency_ratio(int32_t gamma, double alpha, double t_target, double t_draft,
+                           double t_select, double t_verify);
+int md_sd_best_gamma(int32_t max_gamma, double alpha, double t_target, double t_draft,
+                     double t_select, const double* t_verify, int32_t* gamma_out,
+                     double* ratio_out);
+double md_sd_alpha_from_omega(int32_t gamma, double omega);
+
 /* Static description of a status code; never NULL. */
 const char* md_status_str(int status);
 

@@ -14,6 +14,8 @@ CPU fallback: if the library is missing, every call raises.
     md_greedy_accept(logits, draft, ...)          -> (accepted, tokens, target)
     md_kv_commit(lens, accepted, q_len, ...)      (in place)
     md_streaming_list(prompt_lens, Hkv, n_sink, window) -> (idx, idx_len)
+    md_sd_expected_tokens / md_sd_latency_ratio / md_sd_best_gamma /
+    md_sd_alpha_from_omega                        (host-only cost model, Eq. 1-4)
 
 Shapes: q/o [B, L, Hq, d] (L = gamma + 1); k/v contiguous [B, S_alloc, Hkv, d]
 or, with ``page_table`` [B, max_pages] int32, paged [P, page_size, Hkv, d];
@@ -36,7 +38,8 @@ EXPORTED = ["md_verify_attn", "md_draft_attn", "md_draft_attn_indexed", "md_merg
             "md_workspace_bytes", "md_workspace_bytes_indexed", "md_snapkv_votes",
             "md_snapkv_workspace_bytes", "md_snapkv_select", "md_kv_append",
             "md_greedy_accept", "md_greedy_accept_workspace_bytes", "md_kv_commit",
-            "md_streaming_list",
+            "md_streaming_list", "md_sd_expected_tokens", "md_sd_latency_ratio",
+            "md_sd_best_gamma", "md_sd_alpha_from_omega",
             "md_status_str", "md_last_hip_error", "md_attn_args_size",
             "md_bench_stream_read", "md_bench_copy", "md_bench_fill"]
 
@@ -131,6 +134,15 @@ def load_library(path: str = LIB_PATH):
     lib.md_kv_commit.restype = ctypes.c_int
     lib.md_streaming_list.argtypes = [i32, i32, vp, i32, i32, vp, vp, vp]
     lib.md_streaming_list.restype = ctypes.c_int
+    f64 = ctypes.c_double
+    lib.md_sd_expected_tokens.argtypes = [i32, f64]
+    lib.md_sd_expected_tokens.restype = f64
+    lib.md_sd_latency_ratio.argtypes = [i32, f64, f64, f64, f64, f64]
+    lib.md_sd_latency_ratio.restype = f64
+    lib.md_sd_best_gamma.argtypes = [i32, f64, f64, f64, f64, vp, vp, vp]
+    lib.md_sd_best_gamma.restype = ctypes.c_int
+    lib.md_sd_alpha_from_omega.argtypes = [i32, f64]
+    lib.md_sd_alpha_from_omega.restype = f64
     lib.md_merge_lse.argtypes = [i32, i64, i32, i32, vp, vp, vp, vp, vp]
     lib.md_merge_lse.restype = ctypes.c_int
     lib.md_workspace_bytes.argtypes = [args_p, i32, i32, i32]
@@ -475,6 +487,35 @@ def md_streaming_list(prompt_lens, num_kv_heads, n_sink, window, *, idx=None, id
     _check(lib.md_streaming_list(B, num_kv_heads, _ptr(prompt_lens), n_sink, window, _ptr(idx),
                                  _ptr(idx_len), _stream_handle(prompt_lens, stream)))
     return idx, idx_len
+
+
+def md_sd_expected_tokens(gamma: int, alpha: float) -> float:
+    """Eq. 1: expected tokens per verification (NaN for invalid arguments)."""
+    return load_library().md_sd_expected_tokens(int(gamma), float(alpha))
+
+
+def md_sd_latency_ratio(gamma, alpha, t_target, t_draft, t_verify, t_select=0.0) -> float:
+    """Eq. 2 with Eq. 3's draft time: T_Avg^SD / T_T."""
+    return load_library().md_sd_latency_ratio(int(gamma), float(alpha), float(t_target),
+                                              float(t_draft), float(t_select), float(t_verify))
+
+
+def md_sd_best_gamma(alpha, t_target, t_draft, t_verify_by_gamma, t_select=0.0):
+    """Eq. 4 over gamma = 1 .. len(t_verify_by_gamma); t_verify_by_gamma[g-1] = T_V(g).
+    Returns (gamma, ratio)."""
+    n = len(t_verify_by_gamma)
+    arr = (ctypes.c_double * max(n, 1))(*[float(x) for x in t_verify_by_gamma])
+    g = ctypes.c_int32()
+    r = ctypes.c_double()
+    _check(load_library().md_sd_best_gamma(n, float(alpha), float(t_target), float(t_draft),
+                                           float(t_select), ctypes.cast(arr, ctypes.c_void_p),
+                                           ctypes.byref(g), ctypes.byref(r)))
+    return g.value, r.value
+
+
+def md_sd_alpha_from_omega(gamma: int, omega: float) -> float:
+    """The acceptance rate implied by a measured Omega (inverse of Eq. 1)."""
+    return load_library().md_sd_alpha_from_omega(int(gamma), float(omega))
 
 
 # Short aliases.
