@@ -54,6 +54,18 @@ int occupancy(int NT, int depth, int mode) {
   return (mode == MD_MODE_VERIFY && NT == 2) ? 1 : 2;
 }
 
+// Longest-first dispatch pays where units differ in length and each is long:
+// single-chunk verify plans of long caches (the ranking costs B compares per
+// thread, so small batches only).  MD_LPT = 1 or 2 forces it off (1) or on
+// where allowed (2), for A/B measurements.
+int longest_first(int mode, int n_chunks, int num_seqs, int max_kv_len) {
+  static const int forced = env_int("MD_LPT", 1, 2);
+  if (mode != MD_MODE_VERIFY || n_chunks != 1 || num_seqs < 2 || num_seqs > kLptMaxSeqs)
+    return 0;
+  if (forced) return forced == 2;
+  return max_kv_len >= kLptMinLen;
+}
+
 int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void* stream,
                   const int32_t* idx = nullptr, const int32_t* idx_len = nullptr) {
   int st = validate_attn(a, mode, n_sink, window);
@@ -100,6 +112,8 @@ int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void*
   }
   p.n_chunks = pl.n_chunks;
   p.chunk_len = pl.chunk_len;
+  p.num_seqs = a->num_seqs;
+  p.lpt = longest_first(mode, pl.n_chunks, a->num_seqs, a->max_kv_len);
   p.o = a->o;
   p.lse = a->lse;
   p.n_rows = pl.n_rows;

@@ -81,6 +81,38 @@ __device__ __forceinline__ int real_token(const UnitGeom& u, int v) {
 // IDX: the visible range is a per-(sequence, kv head) list of prompt positions
 // followed by the speculated tokens (the indexed draft); otherwise the causal
 // prefix (verify) or sinks then windows (draft).
+// Longest-processing-time-first dispatch.  Workgroups start roughly in
+// blockIdx order (round-robin over the XCDs), so with ragged lengths the
+// units that happen to start last set the finish time.  With p.lpt (one chunk
+// per unit, B <= kLptMaxSeqs), workgroup r instead takes the r-th unit in the
+// order (length descending, sequence ascending, kv head ascending): every
+// workgroup ranks the B clamped lengths in LDS (B compares per thread) and
+// picks the sequence of rank r / Hkv.  The order is a bijection, so each unit
+// is still computed once, with the same arithmetic.
+template <typename P>
+__device__ __forceinline__ int lpt_unit(const P& p, int r, int* sl) {
+  const int B = p.num_seqs;
+  for (int t = threadIdx.x; t < B; t += kWaves * 64) {
+    const int s = min(p.kv_lens[t], p.max_kv_len);
+    sl[t] = s < 0 ? 0 : s;
+  }
+  __syncthreads();
+  const int want = r / p.Hkv;
+  for (int t = threadIdx.x; t < B; t += kWaves * 64) {
+    const int lt = sl[t];
+    int rank = 0;
+    for (int j = 0; j < B; ++j) {
+      const int lj = sl[j];
+      rank += (lj > lt) || (lj == lt && j < t);
+    }
+    if (rank == want) sl[kLptMaxSeqs] = t;
+  }
+  __syncthreads();
+  const int b = sl[kLptMaxSeqs];
+  __syncthreads();  // the LDS is reused by the tiles
+  return b * p.Hkv + r % p.Hkv;
+}
+
 template <int D, bool BF16, int NT, bool PAGED, bool IDX, int P, int OCC>
 __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(OCC)))
 attn_partial_kernel(const AttnParams p) {
@@ -99,7 +131,8 @@ attn_partial_kernel(const AttnParams p) {
   const int grp = lane >> 4;
 
   const int chunk = blockIdx.x % p.n_chunks;
-  const int unit = blockIdx.x / p.n_chunks;
+  const int unit = p.lpt ? lpt_unit(p, blockIdx.x, reinterpret_cast<int*>(lds))
+                         : static_cast<int>(blockIdx.x / p.n_chunks);
   const int hk = unit % p.Hkv;
   const int b = unit / p.Hkv;
   const int L = p.L;

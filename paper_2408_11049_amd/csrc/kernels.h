@@ -32,6 +32,8 @@ struct AttnParams {
   float* part_o;              // [n_chunks][n_rows][d] (several chunks)
   float* part_lse;            // [n_chunks][n_rows]
   int64_t n_rows;
+  int32_t num_seqs;           // B
+  int32_t lpt;                // 1: workgroups take sequences longest first (see attn.hip)
   const int32_t* idx;         // indexed draft: [B, Hkv, idx_stride] prompt positions
   const int32_t* idx_len;     // indexed draft: [B] list lengths
   int32_t idx_stride;

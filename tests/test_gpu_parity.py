@@ -128,6 +128,22 @@ def test_indexed_against_oracle(case):
         assert torch.equal(o2, o) and torch.equal(l2, l), "an unlisted key was read"
 
 
+def test_longest_first_dispatch_ragged():
+    """A verify launch that takes units longest first (one chunk per unit:
+    64 sequences x 8 kv heads, ragged lengths up to 6000, a paged cache):
+    whole output against the oracle, NaN padding included."""
+    B, L, Hq, Hkv, d = 64, 4, 8, 8, 64
+    rng = np.random.default_rng(64)
+    lens = rng.integers(600, 6001, size=B)
+    lens[rng.integers(B)] = 6000
+    say(f"[parity] longest-first verify: B={B} Hkv={Hkv} lens {lens.min()}..{lens.max()}")
+    c = wl.make_case(B=B, q_len=L, Hq=Hq, Hkv=Hkv, d=d, kv_lens=lens, dtype="bf16", page_size=16,
+                     seed=64, device=DEV)
+    go, gl = run_gpu(oracle.VERIFY, c)
+    ro, rl = run_oracle(oracle.VERIFY, c)
+    compare(go, gl, ro, rl, "bf16", "longest-first/verify")
+
+
 def test_empty_batch():
     c = wl.make_case(B=0, q_len=4, Hq=8, Hkv=2, d=128, kv_lens=[], dtype="bf16", device=DEV)
     import paper_2408_11049_amd as md
