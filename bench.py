@@ -279,6 +279,23 @@ def main():
     def commit():
         md.md_kv_commit(commit_lens, acc, L, idx=lists, ring_start=budget, ring_len=ring)
 
+    # SnapKV-style selection at prefill over the same 32k-token prompts: 32
+    # observation queries (the prompt's last positions), pooling 5, budget 2049.
+    n_obs = 32
+    q_obs = torch.randn((w.B, n_obs, w.Hq, w.d), generator=wl._gen(w.seed_base * 10 + 9, dev),
+                        device=dev).to(torch.bfloat16)
+    sk_kw = dict(max_prompt_len=c["max_kv_len"], page_table=c["page_table"])
+    votes = md.md_snapkv_votes(q_obs, c["k"], c["kv_lens"], **sk_kw)
+    ws_sk = torch.empty((max(md.md_snapkv_workspace_bytes(q_obs, c["k"], c["kv_lens"], **sk_kw), 256),),
+                        dtype=torch.uint8, device=dev)
+    sel_idx = torch.empty((w.B, w.Hkv, budget), dtype=torch.int32, device=dev)
+    sel_len = torch.empty((w.B,), dtype=torch.int32, device=dev)
+    t_votes = timed(lambda: md.md_snapkv_votes(q_obs, c["k"], c["kv_lens"], votes=votes,
+                                               workspace=ws_sk, **sk_kw), n=5)
+    t_select = timed(lambda: md.md_snapkv_select(votes, c["kv_lens"], n_obs, budget, pool=5,
+                                                 idx=sel_idx, idx_len=sel_len), n=5)
+    bytes_votes = 2 * int(sum(int(x) for x in lens)) * w.Hkv * w.d * w.esize  # K read twice
+
     t_append = timed(append)
     t_accept = timed(accept)
     ts = []
@@ -341,6 +358,10 @@ def main():
             "t_draft_indexed_us (SnapKV-style list, budget 2049)": round(t_draft_idx, 2),
             "draft_indexed_kv_bytes": bytes_idx,
             "draft_indexed_gbs": round(bytes_idx / (t_draft_idx * 1e-6) / 1e9, 1),
+            "t_snapkv_votes_us (prefill, 32 observation queries)": round(t_votes, 2),
+            "snapkv_votes_k_bytes (two passes over K)": bytes_votes,
+            "snapkv_votes_gbs": round(bytes_votes / (t_votes * 1e-6) / 1e9, 1),
+            "t_snapkv_select_us (pool 5, budget 2049)": round(t_select, 2),
             "t_kv_append_us (gamma+1 tokens, paged)": round(t_append, 2),
             "kv_append_bytes (read + write)": bytes_append,
             "t_greedy_accept_us (fp32 logits, vocab 128256)": round(t_accept, 2),

@@ -275,12 +275,12 @@ typedef struct {
  *   pos0          device int32 [B]: row i of sequence b goes to position
  *                 pos0[b] + i (pages through page_table when paged)
  *   lens_out      device int32 [B] or NULL: set to pos0[b] + n_new; must not
- *                 be pos0 itself
+ *                 overlap pos0
  * Positions past the capacity (or the table), and pages outside
  * [0, num_pages), are not written: memory stays in bounds, those rows are
  * lost.  Values move bit for bit.  The caller provides the pages.
  * Errors: MD_ERR_INVALID_ARG for NULL or misaligned pointers, bad sizes,
- * n_new < 0, lens_out == pos0; MD_ERR_HIP.
+ * n_new < 0, lens_out overlapping pos0; MD_ERR_HIP.
  */
 int md_kv_append(const md_kv_cache* c, int32_t n_new, const void* k_new, const void* v_new,
                  const int32_t* pos0, int32_t* lens_out, void* stream);

@@ -300,12 +300,11 @@ def md_draft_attn_indexed(q, k, v, kv_lens, idx, idx_len, **kw):
     return _attention(MD_MODE_DRAFT_INDEXED, q, k, v, kv_lens, 0, 1, idx=idx, idx_len=idx_len, **kw)
 
 
-def md_snapkv_votes(q_obs, k, prompt_lens, *, max_prompt_len=None, page_table=None,
-                    sm_scale=0.0, votes=None, workspace=None, stream=None):
-    """Raw SnapKV votes [B, Hkv, stride] fp32 of every prefix position
-    (q_obs [B, n_obs, Hq, d]; k contiguous or paged; see include/magicdec.h)."""
+def make_snapkv_args(q_obs, k, prompt_lens, *, max_prompt_len=None, page_table=None,
+                     sm_scale=0.0, votes=None, workspace=None) -> MdSnapkvArgs:
+    """Fill md_snapkv_args from tensors (no data is read or moved); votes may
+    be None to size the workspace only."""
     import torch
-    lib = load_library()
     B, n_obs, Hq, d = q_obs.shape
     paged = page_table is not None
     if k.stride(3) != 1 or not q_obs.is_contiguous():
@@ -316,9 +315,6 @@ def md_snapkv_votes(q_obs, k, prompt_lens, *, max_prompt_len=None, page_table=No
         max_prompt_len = page_table.shape[1] * k.shape[1] if paged else k.shape[1]
     if B > 0 and not paged and k.shape[1] < max_prompt_len:
         raise ValueError("contiguous k must hold max_prompt_len tokens per sequence")
-    stride = max(1, int(max_prompt_len) - n_obs)
-    if votes is None:
-        votes = torch.zeros((B, k.shape[2], stride), dtype=torch.float32, device=q_obs.device)
     a = MdSnapkvArgs()
     a.num_seqs, a.n_obs, a.num_q_heads, a.num_kv_heads, a.head_dim = B, n_obs, Hq, k.shape[2], d
     a.dtype = _dtype_code(q_obs)
@@ -333,11 +329,35 @@ def md_snapkv_votes(q_obs, k, prompt_lens, *, max_prompt_len=None, page_table=No
         a.page_table = page_table.data_ptr()
     a.prompt_lens = prompt_lens.data_ptr()
     a.max_prompt_len = int(max_prompt_len)
-    a.votes, a.votes_stride = votes.data_ptr(), votes.shape[-1]
-    need = int(lib.md_snapkv_workspace_bytes(ctypes.byref(a)))
+    a.votes_stride = max(1, int(max_prompt_len) - n_obs)
+    if votes is not None:
+        a.votes, a.votes_stride = votes.data_ptr(), votes.shape[-1]
+    if workspace is not None:
+        a.workspace, a.workspace_bytes = workspace.data_ptr(), workspace.numel()
+    return a
+
+
+def md_snapkv_workspace_bytes(q_obs, k, prompt_lens, **kw) -> int:
+    """Workspace bytes md_snapkv_votes needs for these tensors."""
+    return int(load_library().md_snapkv_workspace_bytes(
+        ctypes.byref(make_snapkv_args(q_obs, k, prompt_lens, **kw))))
+
+
+def md_snapkv_votes(q_obs, k, prompt_lens, *, max_prompt_len=None, page_table=None,
+                    sm_scale=0.0, votes=None, workspace=None, stream=None):
+    """Raw SnapKV votes [B, Hkv, stride] fp32 of every prefix position
+    (q_obs [B, n_obs, Hq, d]; k contiguous or paged; see include/magicdec.h)."""
+    import torch
+    lib = load_library()
+    kw = dict(max_prompt_len=max_prompt_len, page_table=page_table, sm_scale=sm_scale)
+    if votes is None:
+        stride = make_snapkv_args(q_obs, k, prompt_lens, **kw).votes_stride
+        votes = torch.zeros((q_obs.shape[0], k.shape[2], stride), dtype=torch.float32,
+                            device=q_obs.device)
     if workspace is None:
+        need = md_snapkv_workspace_bytes(q_obs, k, prompt_lens, **kw)
         workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=q_obs.device)
-    a.workspace, a.workspace_bytes = workspace.data_ptr(), workspace.numel()
+    a = make_snapkv_args(q_obs, k, prompt_lens, votes=votes, workspace=workspace, **kw)
     _check(lib.md_snapkv_votes(ctypes.byref(a), _stream_handle(q_obs, stream)))
     return votes
 

@@ -296,7 +296,11 @@ int md_kv_append(const md_kv_cache* c, int32_t n_new, const void* k_new, const v
       !md::aligned16(v_new) || (reinterpret_cast<uintptr_t>(pos0) & 3u) ||
       (reinterpret_cast<uintptr_t>(lens_out) & 3u))
     return MD_ERR_INVALID_ARG;
-  if (lens_out == pos0) return MD_ERR_INVALID_ARG;
+  if (lens_out) {  // every thread reads pos0[b] while one writes lens_out[b]: no overlap
+    const uintptr_t lo = reinterpret_cast<uintptr_t>(lens_out), po = reinterpret_cast<uintptr_t>(pos0);
+    const uintptr_t n = static_cast<uintptr_t>(c->num_seqs) * 4;
+    if (lo < po + n && po < lo + n) return MD_ERR_INVALID_ARG;
+  }
   const int es = c->dtype == MD_BF16 ? 2 : 4;
   md::AppendParams p{};
   p.k_new = static_cast<const unsigned char*>(k_new);

@@ -267,11 +267,71 @@ __device__ __forceinline__ float sk_pooled(const float* v, int n, int j, int poo
 
 }  // namespace
 
-__global__ void __launch_bounds__(256) snapkv_select_kernel(const SnapkvSelectParams p) {
-  __shared__ uint32_t hist[256];
+constexpr int kSelThreads = 512;
+constexpr int kSelWaves = kSelThreads / 64;
+constexpr int kSelPer = 4;             // consecutive positions per thread in a step
+constexpr int kSelStep = kSelThreads * kSelPer;
+constexpr int kSelLdsKeys = 33792;     // pooled keys of one row held in LDS (132 KB)
+constexpr int kSelHalo = 16;           // LDS instance: pool / 2 <= kSelHalo
+constexpr int kSelStage = kSelStep + 2 * kSelHalo;
+constexpr int kSelStagePer = (kSelStage + kSelThreads - 1) / kSelThreads;
+
+// Count every active lane's bin in the wave's histogram h.  Pooled votes of
+// similar size share their top key bytes, so the early radix passes pile
+// onto a few bins: the wave's two most common bins go in with one atomic
+// each (led by their lowest lane), the remaining lanes add directly.
+__device__ __forceinline__ void sk_hist_add(uint32_t* h, bool active, uint32_t bin, int lane) {
+  uint64_t pending = __ballot(active);
+  for (int round = 0; round < 2 && pending; ++round) {
+    const int leader = __ffsll(static_cast<long long>(pending)) - 1;
+    const uint32_t lb = __builtin_amdgcn_readlane(bin, leader);  // leader is wave-uniform
+    const uint64_t same = __ballot(((pending >> lane) & 1ull) && bin == lb);
+    if (lane == leader) atomicAdd(&h[lb], static_cast<uint32_t>(__popcll(same)));
+    pending &= ~same;
+  }
+  if ((pending >> lane) & 1ull) atomicAdd(&h[bin], 1u);
+}
+
+// Exclusive prefix sum of x over the workgroup (thread order), and the total.
+// Uses wsum[kSelWaves]; contains two barriers.
+__device__ __forceinline__ uint32_t sk_block_scan(uint32_t x, uint32_t* wsum, uint32_t& total,
+                                                  int lane, int w) {
+  uint32_t incl = x;
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t o = __shfl_up(incl, off);
+    if (lane >= off) incl += o;
+  }
+  if (lane == 63) wsum[w] = incl;
+  __syncthreads();
+  uint32_t before = 0;
+  total = 0;
+  for (int x2 = 0; x2 < kSelWaves; ++x2) {
+    if (x2 < w) before += wsum[x2];
+    total += wsum[x2];
+  }
+  __syncthreads();
+  return before + incl - x;
+}
+
+// One workgroup per (sequence, kv head) row.
+//
+// LDS instance (rows of at most kSelLdsKeys prefix positions, pool / 2 <=
+// kSelHalo): the raw votes are copied into keys[] with 16-byte loads, then
+// replaced in place, kSelStep positions per step, by their pooled keys.  A
+// step first copies its raw window plus halos into stage[] -- its left halo
+// from the previous step's stage, which kept the raw values that step
+// overwrote -- and pools from there, so no in-place write feeds a later read.
+// Every sweep then reads one LDS word per position.  Otherwise each sweep
+// pools from global memory.  The pooled sum is formed in sk_pooled's order
+// either way (terms outside the prefix add an exact 0), so both instances
+// see the same keys.
+template <bool LDS>
+__global__ void __launch_bounds__(kSelThreads) snapkv_select_kernel(const SnapkvSelectParams p) {
+  __shared__ uint32_t keys[LDS ? kSelLdsKeys : 1];
+  __shared__ float stage[LDS ? kSelStage : 1];
+  __shared__ uint32_t hist[kSelWaves][256];
+  __shared__ uint32_t wsum[kSelWaves];
   __shared__ uint32_t s_prefix, s_above;
-  __shared__ uint32_t w_eq[4], w_take[4];
-  __shared__ uint32_t s_out, s_eq_seen;
 
   const int row = blockIdx.x;
   const int b = row / p.rows_per_seq;
@@ -282,7 +342,53 @@ __global__ void __launch_bounds__(256) snapkv_select_kernel(const SnapkvSelectPa
   int32_t* out = p.idx + static_cast<int64_t>(row) * p.budget;
   const int tid = threadIdx.x;
   const int w = tid >> 6;
-  const uint64_t below = (1ull << (tid & 63)) - 1ull;
+  const int lane = tid & 63;
+
+  auto key_at = [&](int j) -> uint32_t {
+    if (LDS) return keys[j];
+    return sk_key(sk_pooled(v, n, j, p.pool));
+  };
+
+  if (LDS && keep > 0) {
+    float* rawf = reinterpret_cast<float*>(keys);
+    const bool vec = (reinterpret_cast<uintptr_t>(v) & 15u) == 0;
+    const int n4 = vec ? n / 4 : 0;
+#pragma unroll 4
+    for (int i = tid; i < n4; i += kSelThreads)
+      reinterpret_cast<float4*>(rawf)[i] = reinterpret_cast<const float4*>(v)[i];
+    for (int j = 4 * n4 + tid; j < n; j += kSelThreads) rawf[j] = v[j];
+    __syncthreads();
+    const int h = p.pool / 2;
+    const int span = kSelStep + 2 * h;
+    for (int base = 0; base < n; base += kSelStep) {
+      // stage[i] <- raw position base - h + i (0 outside the prefix).
+      float x[kSelStagePer];
+#pragma unroll
+      for (int r = 0; r < kSelStagePer; ++r) {
+        const int i = tid + r * kSelThreads;
+        const int j = base - h + i;
+        x[r] = 0.f;
+        if (i < span && j >= 0 && j < n) x[r] = (base > 0 && i < 2 * h) ? stage[kSelStep + i] : rawf[j];
+      }
+      __syncthreads();
+#pragma unroll
+      for (int r = 0; r < kSelStagePer; ++r) {
+        const int i = tid + r * kSelThreads;
+        if (i < span) stage[i] = x[r];
+      }
+      __syncthreads();
+#pragma unroll
+      for (int e = 0; e < kSelPer; ++e) {
+        const int j = base + tid * kSelPer + e;
+        if (j < n) {
+          float s = 0.f;
+          for (int t2 = 0; t2 < p.pool; ++t2) s += stage[j - base + t2];
+          keys[j] = sk_key(s / static_cast<float>(p.pool));
+        }
+      }
+      __syncthreads();
+    }
+  }
 
   // Radix select, most significant byte first: after four passes tau is the
   // key of the keep-th largest pooled vote and `above` keys exceed it.
@@ -291,23 +397,34 @@ __global__ void __launch_bounds__(256) snapkv_select_kernel(const SnapkvSelectPa
     for (int pass = 0; pass < 4; ++pass) {
       const int shift = 24 - 8 * pass;
       const uint32_t hi_mask = pass == 0 ? 0u : (0xffffffffu << (32 - 8 * pass));
-      hist[tid] = 0;
+      for (int i = tid; i < kSelWaves * 256; i += kSelThreads) (&hist[0][0])[i] = 0;
       __syncthreads();
-      for (int j = tid; j < n; j += 256) {
-        const uint32_t key = sk_key(sk_pooled(v, n, j, p.pool));
-        if ((key & hi_mask) == (prefix & hi_mask)) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+      for (int base = 0; base < n; base += kSelPer * kSelThreads) {
+        uint32_t k[kSelPer];  // the keys first, so their reads overlap
+#pragma unroll
+        for (int e = 0; e < kSelPer; ++e) {
+          const int j = base + e * kSelThreads + tid;
+          k[e] = j < n ? key_at(j) : 0u;
+        }
+#pragma unroll
+        for (int e = 0; e < kSelPer; ++e) {
+          const bool act = base + e * kSelThreads + tid < n && (k[e] & hi_mask) == (prefix & hi_mask);
+          sk_hist_add(hist[w], act, (k[e] >> shift) & 255u, lane);
+        }
       }
       __syncthreads();
-      if (tid == 0) {
-        // Walk the digits from the top until the running count reaches keep.
-        uint32_t run = above;
-        int d = 255;
-        for (; d > 0; --d) {
-          if (run + hist[d] >= static_cast<uint32_t>(keep)) break;
-          run += hist[d];
-        }
-        s_above = run;
-        s_prefix = prefix | (static_cast<uint32_t>(d) << shift);
+      // Threads 0..255 own digits 255..0; a scan from the top digit finds the
+      // one where the running count reaches keep.
+      uint32_t cnt = 0;
+      const uint32_t d = 255u - static_cast<uint32_t>(tid);
+      if (tid < 256)
+        for (int x = 0; x < kSelWaves; ++x) cnt += hist[x][d];
+      uint32_t total;
+      const uint32_t excl = sk_block_scan(cnt, wsum, total, lane, w);
+      if (tid < 256 && above + excl < static_cast<uint32_t>(keep) &&
+          above + excl + cnt >= static_cast<uint32_t>(keep)) {
+        s_prefix = prefix | (d << shift);
+        s_above = above + excl;
       }
       __syncthreads();
       prefix = s_prefix;
@@ -318,44 +435,44 @@ __global__ void __launch_bounds__(256) snapkv_select_kernel(const SnapkvSelectPa
   const uint32_t tau = prefix;
   const uint32_t need_eq = keep > 0 ? static_cast<uint32_t>(keep) - above : 0;
 
-  // Ordered compaction over 256-position slices: keep key > tau, and key ==
-  // tau while fewer than need_eq of those were kept; positions come out
-  // ascending, so ties go to the smaller position.
-  if (tid == 0) {
-    s_out = 0;
-    s_eq_seen = 0;
-  }
-  __syncthreads();
-  for (int base = 0; base < n && keep > 0; base += 256) {
-    const int j = base + tid;
-    bool gt = false, eq = false;
-    if (j < n) {
-      const uint32_t key = sk_key(sk_pooled(v, n, j, p.pool));
-      gt = key > tau;
-      eq = key == tau;
+  // Ordered compaction, kSelStep positions per step, kSelPer consecutive ones
+  // per thread: keep key > tau, and key == tau while fewer than need_eq of
+  // those were kept before it; positions come out ascending, so ties go to
+  // the smaller position.
+  uint32_t out_base = 0, eq_base = 0;
+  for (int base = 0; base < n && keep > 0; base += kSelStep) {
+    const int j0 = base + tid * kSelPer;
+    bool gt[kSelPer], eq[kSelPer];
+    uint32_t n_eq = 0;
+#pragma unroll
+    for (int e = 0; e < kSelPer; ++e) {
+      const int j = j0 + e;
+      const uint32_t k = j < n ? key_at(j) : 0u;
+      gt[e] = j < n && k > tau;
+      eq[e] = j < n && k == tau;
+      n_eq += eq[e];
     }
-    const uint64_t eq_mask = __ballot(eq);
-    if ((tid & 63) == 0) w_eq[w] = __popcll(eq_mask);
-    __syncthreads();
-    uint32_t eq_before = s_eq_seen + __popcll(eq_mask & below);
-    for (int x = 0; x < w; ++x) eq_before += w_eq[x];
-    const bool take = gt || (eq && eq_before < need_eq);
-    const uint64_t take_mask = __ballot(take);
-    if ((tid & 63) == 0) w_take[w] = __popcll(take_mask);
-    __syncthreads();
-    uint32_t pos = s_out + __popcll(take_mask & below);
-    for (int x = 0; x < w; ++x) pos += w_take[x];
-    if (take) out[pos] = j;
-    __syncthreads();
-    if (tid == 0) {
-      s_out += w_take[0] + w_take[1] + w_take[2] + w_take[3];
-      s_eq_seen += w_eq[0] + w_eq[1] + w_eq[2] + w_eq[3];
+    uint32_t eq_total;
+    uint32_t eq_before = eq_base + sk_block_scan(n_eq, wsum, eq_total, lane, w);
+    bool take[kSelPer];
+    uint32_t n_take = 0;
+#pragma unroll
+    for (int e = 0; e < kSelPer; ++e) {
+      take[e] = gt[e] || (eq[e] && eq_before < need_eq);
+      eq_before += eq[e];
+      n_take += take[e];
     }
-    __syncthreads();
+    uint32_t take_total;
+    uint32_t pos = out_base + sk_block_scan(n_take, wsum, take_total, lane, w);
+#pragma unroll
+    for (int e = 0; e < kSelPer; ++e)
+      if (take[e]) out[pos++] = j0 + e;
+    out_base += take_total;
+    eq_base += eq_total;
   }
   // The observation window, always kept.
   const int kept = keep > 0 ? keep : 0;
-  for (int j = n + tid; j < S; j += 256) out[kept + (j - n)] = j;
+  for (int j = n + tid; j < S; j += kSelThreads) out[kept + (j - n)] = j;
   if (tid == 0 && (row % p.rows_per_seq) == 0) p.counts[b] = kept + (S - n);
 }
 
@@ -416,7 +533,10 @@ hipError_t launch_snapkv_votes(const SnapkvParams& p, int head_dim, bool bf16, i
 
 hipError_t launch_snapkv_select(const SnapkvSelectParams& p, hipStream_t s) {
   if (p.rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(snapkv_select_kernel, dim3(p.rows), dim3(256), 0, s, p);
+  if (p.stride <= kSelLdsKeys && p.pool / 2 <= kSelHalo)
+    hipLaunchKernelGGL(snapkv_select_kernel<true>, dim3(p.rows), dim3(kSelThreads), 0, s, p);
+  else
+    hipLaunchKernelGGL(snapkv_select_kernel<false>, dim3(p.rows), dim3(kSelThreads), 0, s, p);
   return hipGetLastError();
 }
 

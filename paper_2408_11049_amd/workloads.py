@@ -9,7 +9,8 @@ not used.
 
 Seeds: workload ``base`` uses generator streams ``base*10 + s`` with
 s = 0 Q, 1 K, 2 V, 3 lengths, 4 page placement, 5 outlier channels,
-6 logits, 7 planted tokens and drafts, 8 appended K/V rows.
+6 logits, 7 planted tokens and drafts, 8 appended K/V rows, 9 the bench's
+SnapKV observation queries.
 
 Padding that a correct kernel never reads (tokens past kv_lens[b] in a
 contiguous cache, slots past the end in a sequence's last page, pages owned by

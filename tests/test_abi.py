@@ -297,6 +297,8 @@ def test_kv_append_pointer_rules(lib):
     ap = lib.md_kv_append
     assert ap(None, 3, FAKE, FAKE, FAKE, None, None) == md.MD_ERR_INVALID_ARG
     assert ap(ctypes.byref(c), 3, FAKE, FAKE, FAKE, FAKE, None) == md.MD_ERR_INVALID_ARG  # lens_out == pos0
+    assert ap(ctypes.byref(c), 3, FAKE, FAKE, FAKE, FAKE + 4, None) == md.MD_ERR_INVALID_ARG  # overlap
+    assert ap(ctypes.byref(c), 3, FAKE, FAKE, FAKE + 4, FAKE, None) == md.MD_ERR_INVALID_ARG
     assert ap(ctypes.byref(c), 3, FAKE + 8, FAKE, FAKE, None, None) == md.MD_ERR_INVALID_ARG
     assert ap(ctypes.byref(c), 3, FAKE, FAKE, None, None, None) == md.MD_ERR_INVALID_ARG
     assert ap(ctypes.byref(c), 3, FAKE, FAKE, FAKE + 2, None, None) == md.MD_ERR_INVALID_ARG

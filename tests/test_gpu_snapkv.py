@@ -67,6 +67,7 @@ SELECT = [
     (2, 300, 8, 40, 1, [308, 100], 1),
     (1, 70, 32, 64, 5, [32], 2),           # prompt == window: nothing to select
     (2, 1000, 32, 33, 3, [1032, 900], 2),  # one prefix position kept
+    (2, 40000, 32, 2049, 5, [40032, 20000], 2),  # rows longer than the LDS key buffer
 ]
 
 
