@@ -21,7 +21,10 @@
 //       top keep, ordered compaction, plus the window.
 // In the pass kernels all G*n_obs rows of a unit share each 32-key tile,
 // loaded once into LDS as whole 256 B rows; each wave owns a quarter of the
-// rows (16-row MFMA tiles) and computes S^T = K Q^T on v_mfma_f32_16x16x32_bf16.
+// rows (16-row MFMA tiles) and computes S = Q K^T on v_mfma_f32_16x16x32_bf16,
+// so each lane holds four rows of one key: a key's vote sums inside the lane
+// and across the wave's four lane groups, and the softmax statistics of a
+// row stay in its lanes until the chunk ends.
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
@@ -74,26 +77,29 @@ snapkv_pass_kernel(const SnapkvParams p) {
   const int v_end = min(U, v_begin + p.chunk_len);
   const int n_tiles = v_end > v_begin ? (v_end - v_begin + kSkTile - 1) / kSkTile : 0;
 
-  // Rows of this wave: r = (wave * TW + t) * 16 + l16, r = o * G + g.
-  int row_pos[TW];
+  // Rows of this wave's tile t: r = (wave * TW + t) * 16 + i, r = o * G + g.
+  // Q is the MFMA A operand (lane l16 loads row i = l16), so the C tile of
+  // S = Q K^T gives each lane rows 4 * grp + e (e = item) of key l16.
   sk_u32x4 qreg[TW][SH::KCB];
-  float lse2[TW];
+  int row_pos[TW][4];  // query position of the lane's rows (-1: padding)
+  float lse2[TW][4];   // PASS 1: their log2-sum-exp (+inf for padding: p = 0)
   for (int t = 0; t < TW; ++t) {
-    const int r = (wave * TW + t) * 16 + l16;
-    const bool real = r < p.R;
-    const int o = real ? r / p.G : 0, g = real ? r % p.G : 0;
-    row_pos[t] = real ? S - p.n_obs + o : -1;
+    const int rq = (wave * TW + t) * 16 + l16;
     for (int cb = 0; cb < SH::KCB; ++cb) qreg[t][cb] = sk_u32x4{0, 0, 0, 0};
-    if (real) {
+    if (rq < p.R) {
+      const int o = rq / p.G, g = rq % p.G;
       const unsigned char* qp = static_cast<const unsigned char*>(p.q) +
                                 ((static_cast<int64_t>(b) * p.n_obs + o) * p.Hq + hk * p.G + g) *
                                     D * SH::ES;
       for (int cb = 0; cb < SH::KCB; ++cb)
         qreg[t][cb] = *reinterpret_cast<const sk_u32x4*>(qp + cb * 64 + grp * 16);
     }
-    // PASS 1: rows that are not real get lse = +inf, so their p is exactly 0.
-    lse2[t] = INFINITY;
-    if (PASS == 1 && real) lse2[t] = p.lse2[static_cast<int64_t>(unit) * p.R + r];
+    for (int e = 0; e < 4; ++e) {
+      const int r = (wave * TW + t) * 16 + 4 * grp + e;
+      row_pos[t][e] = r < p.R ? S - p.n_obs + r / p.G : -1;
+      lse2[t][e] = INFINITY;
+      if (PASS == 1 && r < p.R) lse2[t][e] = p.lse2[static_cast<int64_t>(unit) * p.R + r];
+    }
   }
 
   const unsigned char* kbase = static_cast<const unsigned char*>(p.k);
@@ -130,11 +136,12 @@ snapkv_pass_kernel(const SnapkvParams p) {
     }
   };
 
-  float m_run[TW], l_run[TW];
-  for (int t = 0; t < TW; ++t) {
-    m_run[t] = -INFINITY;
-    l_run[t] = 0.f;
-  }
+  float m_run[TW][4], l_run[TW][4];
+  for (int t = 0; t < TW; ++t)
+    for (int e = 0; e < 4; ++e) {
+      m_run[t][e] = -INFINITY;
+      l_run[t][e] = 0.f;
+    }
 
   sk_u32x4 xr[SH::NLD];
   load_tile(xr, 0);
@@ -145,7 +152,7 @@ snapkv_pass_kernel(const SnapkvParams p) {
     load_tile(xr, tile + 1);  // next tile in flight while this one is used
     const int v0 = v_begin + tile * kSkTile;
 
-    // S^T = K Q^T for this wave's row tiles.
+    // S = Q K^T for this wave's row tiles and the tile's two 16-key blocks.
     sk_f32x4 sacc[TW][2];
     for (int tb = 0; tb < 2; ++tb) {
       for (int t = 0; t < TW; ++t) sacc[t][tb] = sk_f32x4{0.f, 0.f, 0.f, 0.f};
@@ -155,50 +162,48 @@ snapkv_pass_kernel(const SnapkvParams p) {
         for (int t = 0; t < TW; ++t) {
           if constexpr (BF16) {
             sacc[t][tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(sk_bf16x8, kk), __builtin_bit_cast(sk_bf16x8, qreg[t][cb]),
+                __builtin_bit_cast(sk_bf16x8, qreg[t][cb]), __builtin_bit_cast(sk_bf16x8, kk),
                 sacc[t][tb], 0, 0, 0);
           } else {
             for (int jj = 0; jj < 4; ++jj)
               sacc[t][tb] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                  __uint_as_float(kk[jj]), __uint_as_float(qreg[t][cb][jj]), sacc[t][tb], 0, 0, 0);
+                  __uint_as_float(qreg[t][cb][jj]), __uint_as_float(kk[jj]), sacc[t][tb], 0, 0, 0);
           }
         }
       }
     }
 
     if constexpr (PASS == 0) {
-      // Online max and sum of 2^(s*scale*log2e) per row (this lane's 8 keys).
-      for (int t = 0; t < TW; ++t) {
-        float x8[8];
-        float mx = -INFINITY;
-        for (int tb = 0; tb < 2; ++tb)
-          for (int e = 0; e < 4; ++e) {
-            const int j = v0 + tb * 16 + grp * 4 + e;
-            const bool vis = j < v_end && j <= row_pos[t];
-            x8[tb * 4 + e] = vis ? sacc[t][tb][e] * p.scale_log2 : -INFINITY;
-            mx = fmaxf(mx, x8[tb * 4 + e]);
+      // Online max and sum of 2^(s*scale*log2e) per row, over this lane's two
+      // keys (one per block); the rescale runs only when the max moves.
+      const int ja = v0 + l16, jb = v0 + 16 + l16;
+      for (int t = 0; t < TW; ++t)
+        for (int e = 0; e < 4; ++e) {
+          const int pos = row_pos[t][e];
+          const float x0 = (ja < v_end && ja <= pos) ? sacc[t][0][e] * p.scale_log2 : -INFINITY;
+          const float x1 = (jb < v_end && jb <= pos) ? sacc[t][1][e] * p.scale_log2 : -INFINITY;
+          const float mx = fmaxf(x0, x1);
+          if (mx > m_run[t][e]) {
+            l_run[t][e] *= __builtin_amdgcn_exp2f(m_run[t][e] - mx);
+            m_run[t][e] = mx;
           }
-        const float m_new = fmaxf(m_run[t], mx);
-        const float m_use = m_new == -INFINITY ? 0.f : m_new;
-        float s = 0.f;
-        for (int jj = 0; jj < 8; ++jj) s += __builtin_amdgcn_exp2f(x8[jj] - m_use);
-        l_run[t] = l_run[t] * __builtin_amdgcn_exp2f(m_run[t] - m_use) + s;
-        m_run[t] = m_new;
-      }
+          const float m_use = m_run[t][e] == -INFINITY ? 0.f : m_run[t][e];
+          l_run[t][e] += __builtin_amdgcn_exp2f(x0 - m_use) + __builtin_amdgcn_exp2f(x1 - m_use);
+        }
     } else {
-      // p = 2^(s*scale*log2e - lse2) summed over every row, per key.
-      float col[8];
-      for (int jj = 0; jj < 8; ++jj) col[jj] = 0.f;
+      // p = 2^(s*scale*log2e - lse2) summed over every row, per key: inside
+      // the lane over its rows, then over the four row groups of the wave.
+      float col[2] = {0.f, 0.f};
       for (int t = 0; t < TW; ++t)
         for (int tb = 0; tb < 2; ++tb)
           for (int e = 0; e < 4; ++e)
-            col[tb * 4 + e] += __builtin_amdgcn_exp2f(sacc[t][tb][e] * p.scale_log2 - lse2[t]);
-      // Sum over the 16 rows of each 16-lane group.
-      for (int off = 1; off < 16; off <<= 1)
-        for (int jj = 0; jj < 8; ++jj) col[jj] += __shfl_xor(col[jj], off);
-      if (l16 == 0)
-        for (int tb = 0; tb < 2; ++tb)
-          for (int e = 0; e < 4; ++e) red[wave][tb * 16 + grp * 4 + e] = col[tb * 4 + e];
+            col[tb] += __builtin_amdgcn_exp2f(sacc[t][tb][e] * p.scale_log2 - lse2[t][e]);
+      for (int tb = 0; tb < 2; ++tb) {
+        col[tb] += __shfl_xor(col[tb], 16);
+        col[tb] += __shfl_xor(col[tb], 32);
+      }
+      if (grp == 0)
+        for (int tb = 0; tb < 2; ++tb) red[wave][tb * 16 + l16] = col[tb];
       __syncthreads();
       if (threadIdx.x < kSkTile) {
         const int j = v0 + threadIdx.x;
@@ -213,21 +218,25 @@ snapkv_pass_kernel(const SnapkvParams p) {
   }
 
   if constexpr (PASS == 0) {
-    // Combine the 4 lanes of each row, then write (m, l) for this chunk.
-    for (int t = 0; t < TW; ++t) {
-      float m_all = fmaxf(m_run[t], __shfl_xor(m_run[t], 16));
-      m_all = fmaxf(m_all, __shfl_xor(m_all, 32));
-      const float m_use = m_all == -INFINITY ? 0.f : m_all;
-      float l = l_run[t] * __builtin_amdgcn_exp2f(m_run[t] - m_use);
-      l += __shfl_xor(l, 16);
-      l += __shfl_xor(l, 32);
-      const int r = (wave * TW + t) * 16 + l16;
-      if (grp == 0 && r < p.R) {
-        const int64_t at = (static_cast<int64_t>(unit) * p.n_chunks + chunk) * p.R + r;
-        p.part_m[at] = m_all;
-        p.part_l[at] = l;
+    // Combine each row over the 16 lanes holding its keys, then write (m, l)
+    // for this chunk.
+    for (int t = 0; t < TW; ++t)
+      for (int e = 0; e < 4; ++e) {
+        float m = m_run[t][e], l = l_run[t][e];
+        for (int off = 1; off < 16; off <<= 1) {
+          const float mo = __shfl_xor(m, off), lo = __shfl_xor(l, off);
+          const float mn = fmaxf(m, mo);
+          const float m_use = mn == -INFINITY ? 0.f : mn;
+          l = l * __builtin_amdgcn_exp2f(m - m_use) + lo * __builtin_amdgcn_exp2f(mo - m_use);
+          m = mn;
+        }
+        const int r = (wave * TW + t) * 16 + 4 * grp + e;
+        if (l16 == 0 && r < p.R) {
+          const int64_t at = (static_cast<int64_t>(unit) * p.n_chunks + chunk) * p.R + r;
+          p.part_m[at] = m;
+          p.part_l[at] = l;
+        }
       }
-    }
   }
 }
 
