@@ -308,6 +308,66 @@ def main():
         ts.append(a_ev.elapsed_time(b_ev) * 1e3)
     t_commit = float(np.median(ts))
     bytes_append = 2 * 2 * w.B * L * w.Hkv * w.d * w.esize  # K and V rows, read + write
+
+    # A whole speculative step as an engine issues it: gamma draft steps (one
+    # token's K/V appended, then a one-token draft over the 2049-position
+    # lists plus the 1024-slot ring), then the gamma+1 verified tokens' K/V,
+    # verification, greedy acceptance and the commit.  Timed from the same
+    # restored state each time, eagerly and as one HIP graph replay.
+    sd_lists0 = torch.full((w.B, w.Hkv, budget + ring), -1, dtype=torch.int32, device=dev)
+    sd_lists0[:, :, :budget] = idx_t
+    sd_lists = sd_lists0.clone()
+    sd_len = torch.full((w.B,), budget + ring, dtype=torch.int32, device=dev)
+    sd_lens = pos0.clone()
+    pos_i = [(pos0 + i).contiguous() for i in range(w.gamma)]
+    kvl_i = [torch.empty_like(pos0) for _ in range(w.gamma)]
+    k1 = [k_new[:, i:i + 1].contiguous() for i in range(w.gamma)]
+    v1 = [v_new[:, i:i + 1].contiguous() for i in range(w.gamma)]
+    out_sd1 = torch.empty_like(q1)
+    ws_i1 = torch.empty((max(int(lib.md_workspace_bytes_indexed(md.ctypes.byref(md.make_args(
+        q1, c["k"], c["v"], c["kv_lens"], **common)), budget + ring)), 256),), dtype=torch.uint8,
+        device=dev)
+    ws_vsd = ws(0, c["q"])
+    sd_out = torch.empty_like(pos0)
+
+    def sd_step():
+        for i in range(w.gamma):
+            md.md_kv_append(c["k"], c["v"], k1[i], v1[i], pos_i[i], page_table=c["page_table"],
+                            lens_out=kvl_i[i])
+            md.md_draft_attn_indexed(q1, c["k"], c["v"], kvl_i[i], sd_lists, sd_len, out=out_sd1,
+                                     return_lse=False, workspace=ws_i1, **common)
+        md.md_kv_append(c["k"], c["v"], k_new, v_new, sd_lens, page_table=c["page_table"],
+                        lens_out=sd_out)
+        md.md_verify_attn(c["q"], c["k"], c["v"], sd_out, out=out_v, lse=lse_v, workspace=ws_vsd,
+                          **common)
+        md.md_greedy_accept(logits, draft_tok, accepted=acc, tokens=toks, want_target=False,
+                            workspace=ws_acc)
+        md.md_kv_commit(sd_lens, acc, L, idx=sd_lists, ring_start=budget, ring_len=ring)
+
+    def sd_timed(run, n=8):
+        ts = []
+        for _ in range(n):
+            sd_lens.copy_(pos0)
+            sd_lists.copy_(sd_lists0)
+            do_flush()
+            a_ev, b_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a_ev.record(stream); run(); b_ev.record(stream)
+            torch.cuda.synchronize()
+            ts.append(a_ev.elapsed_time(b_ev) * 1e3)
+        return float(np.median(ts))
+
+    sd_step()
+    torch.cuda.synchronize()
+    t_sd_eager = sd_timed(sd_step)
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(graph, stream=side):
+            sd_step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    t_sd_graph = sd_timed(graph.replay)
     bytes_logits = logits.numel() * logits.element_size()
     # A plain 1 GiB copy of known size: its FETCH_SIZE / WRITE_SIZE readings
     # calibrate the HBM byte counters of a rocprofv3 --pmc run of this script.
@@ -370,6 +430,9 @@ def main():
             "t_kv_commit_us (lengths + 1024-slot ring)": round(t_commit, 2),
             "t_sd_full_us (gamma*t_draft(1) + append + verify + accept + commit)": round(
                 w.gamma * t_draft1 + t_append + float(np.mean(tv)) + t_accept + t_commit, 2),
+            "t_sd_step_eager_us (gamma x (append 1 + listed draft 1) + append + verify + accept + commit)":
+                round(t_sd_eager, 2),
+            "t_sd_step_graph_us (the same step, one HIP graph replay)": round(t_sd_graph, 2),
             "verify_kv_bytes": bytes_v, "draft_kv_bytes": bytes_d,
             "verify_gbs": round(verify_gbs, 1),
             "draft_gbs": round(bytes_d / (np.mean(td) * 1e-6) / 1e9, 1),
