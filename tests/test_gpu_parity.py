@@ -17,6 +17,7 @@ import pytest
 import torch
 
 import oracle
+import paper_2408_11049_amd as md
 from gpu_util import TOL, compare, run_gpu, run_gpu_indexed, run_oracle, sample_units, say, unit_rows
 from paper_2408_11049_amd import workloads as wl
 
@@ -190,3 +191,51 @@ def test_full_size_sampled(name):
     finally:
         del c
         torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("paged", [False, True], ids=["contiguous", "paged16"])
+def test_head_major_layout(paged):
+    """The cache given head-major ([.., kv head, token, d] under the same
+    [blk, tok, head, d] view, through its strides): verify, draft and the
+    listed draft against the oracle on a token-major copy of the same values,
+    and an append into it lands where the strides say."""
+    B, L, Hq, Hkv, d, ps = 3, 4, 8, 2, 128, 16
+    lens = np.array([300, 77, 1030])
+    c = wl.make_case(B=B, q_len=L, Hq=Hq, Hkv=Hkv, d=d, kv_lens=lens, dtype="bf16",
+                     page_size=ps if paged else 0, seed=41, device=DEV, nan_pad=False,
+                     S_alloc=None if paged else 1040)
+    # Head-major storage holding the same logical values.
+    k_hm = c["k"].permute(0, 2, 1, 3).contiguous().permute(0, 2, 1, 3)
+    v_hm = c["v"].permute(0, 2, 1, 3).contiguous().permute(0, 2, 1, 3)
+    assert k_hm.stride(2) == k_hm.shape[1] * d and k_hm.stride(1) == d
+    say(f"[parity] head-major {'paged' if paged else 'contiguous'}: strides {k_hm.stride()}")
+    kw = dict(max_kv_len=c["max_kv_len"], page_table=c["page_table"])
+    q, kh, vh = wl.to_host_bits(c["q"]), wl.to_host_bits(c["k"]), wl.to_host_bits(c["v"])
+    pt = c["page_table_np"]
+    o, l = md.md_verify_attn(c["q"], k_hm, v_hm, c["kv_lens"], **kw)
+    torch.cuda.synchronize()
+    ro, rl = oracle.verify(q, kh, vh, c["kv_lens_np"], page_table=pt)
+    compare(o.float().cpu().numpy().astype(np.float64), l.cpu().numpy().astype(np.float64), ro, rl,
+            "bf16", "head-major/verify")
+    o, l = md.md_draft_attn(c["q"], k_hm, v_hm, c["kv_lens"], 4, 64, **kw)
+    torch.cuda.synchronize()
+    ro, rl = oracle.draft(q, kh, vh, c["kv_lens_np"], 4, 64, page_table=pt)
+    compare(o.float().cpu().numpy().astype(np.float64), l.cpu().numpy().astype(np.float64), ro, rl,
+            "bf16", "head-major/draft")
+    idx, n = wl.index_lists(B, Hkv, lens, L, 100, 41)
+    o, l = md.md_draft_attn_indexed(c["q"], k_hm, v_hm, c["kv_lens"], torch.from_numpy(idx).to(DEV),
+                                    torch.from_numpy(n).to(DEV), **kw)
+    torch.cuda.synchronize()
+    ro, rl = oracle.indexed(q, kh, vh, c["kv_lens_np"], idx, n, page_table=pt)
+    compare(o.float().cpu().numpy().astype(np.float64), l.cpu().numpy().astype(np.float64), ro, rl,
+            "bf16", "head-major/listed draft")
+    # Append two tokens after position 10 of every sequence, through the strides.
+    k_new, v_new = wl.new_kv_rows(B, 2, Hkv, d, "bf16", seed=42, device=DEV)
+    pos0 = torch.full((B,), 10, dtype=torch.int32, device=DEV)
+    md.md_kv_append(k_hm, v_hm, k_new, v_new, pos0, page_table=c["page_table"])
+    torch.cuda.synchronize()
+    for b in range(B):
+        for i in range(2):
+            j = 10 + i
+            blk, tok = (int(pt[b, j // ps]), j % ps) if paged else (b, j)
+            assert torch.equal(k_hm[blk, tok], k_new[b, i]) and torch.equal(v_hm[blk, tok], v_new[b, i])
