@@ -24,6 +24,7 @@ kv_lens [B] int32 counting the L speculated tokens; lse [B, L, Hq] fp32.
 from __future__ import annotations
 
 import ctypes
+import functools
 import os
 from typing import Optional
 
@@ -175,6 +176,22 @@ def _check(status: int):
     raise ValueError(f"magicdec: {msg} (status {status})")
 
 
+def _stream_scoped(fn):
+    """Run a binding call with its `stream` (when given) as torch's current
+    stream, so every tensor the binding allocates for the call (outputs,
+    workspace) belongs to the stream the call's kernels run on: the caching
+    allocator then never hands such a block to other work before those
+    kernels are done, even when the binding drops it on return."""
+    @functools.wraps(fn)
+    def wrapped(*args, stream=None, **kw):
+        if stream is None:
+            return fn(*args, stream=None, **kw)
+        import torch
+        with torch.cuda.stream(stream):
+            return fn(*args, stream=stream, **kw)
+    return wrapped
+
+
 def _stream_handle(t, stream):
     import torch
     if stream is None:
@@ -244,6 +261,7 @@ def md_workspace_bytes(q, k, v, kv_lens, *, mode=MD_MODE_VERIFY, n_sink=0, windo
     return int(lib.md_workspace_bytes(ctypes.byref(a), mode, n_sink, window))
 
 
+@_stream_scoped
 def _attention(mode, q, k, v, kv_lens, n_sink, window, *, max_kv_len=None, page_table=None,
                sm_scale=0.0, out=None, lse=None, return_lse=True, workspace=None, stream=None,
                idx=None, idx_len=None):
@@ -343,6 +361,7 @@ def md_snapkv_workspace_bytes(q_obs, k, prompt_lens, **kw) -> int:
         ctypes.byref(make_snapkv_args(q_obs, k, prompt_lens, **kw))))
 
 
+@_stream_scoped
 def md_snapkv_votes(q_obs, k, prompt_lens, *, max_prompt_len=None, page_table=None,
                     sm_scale=0.0, votes=None, workspace=None, stream=None):
     """Raw SnapKV votes [B, Hkv, stride] fp32 of every prefix position
@@ -362,6 +381,7 @@ def md_snapkv_votes(q_obs, k, prompt_lens, *, max_prompt_len=None, page_table=No
     return votes
 
 
+@_stream_scoped
 def md_snapkv_select(votes, prompt_lens, n_obs, budget, *, pool=5, idx=None, idx_len=None,
                      stream=None):
     """Pool the votes [B, Hkv, stride] and keep budget positions per (sequence,
@@ -380,6 +400,7 @@ def md_snapkv_select(votes, prompt_lens, n_obs, budget, *, pool=5, idx=None, idx
     return idx, idx_len
 
 
+@_stream_scoped
 def md_merge_lse(o_parts, lse_parts, *, out_dtype=None, out=None, lse=None, stream=None):
     """o_parts [n_parts, n_rows, d] fp32, lse_parts [n_parts, n_rows] fp32 -> (o, lse)."""
     import torch
@@ -429,6 +450,7 @@ def make_kv_cache(k, v, *, num_seqs=None, page_table=None) -> MdKvCache:
     return c
 
 
+@_stream_scoped
 def md_kv_append(k, v, k_new, v_new, pos0, *, page_table=None, lens_out=None, stream=None):
     """Write k_new/v_new [B, n_new, Hkv, d] at positions pos0[b] + i of the cache
     (in place).  Returns lens_out [B] int32 = pos0 + n_new."""
@@ -449,6 +471,7 @@ def md_kv_append(k, v, k_new, v_new, pos0, *, page_table=None, lens_out=None, st
     return lens_out
 
 
+@_stream_scoped
 def md_greedy_accept(logits, draft, *, accepted=None, tokens=None, target=None,
                      want_target=True, workspace=None, stream=None):
     """logits [B, gamma + 1, vocab] float32/bfloat16, draft [B, gamma] int32 ->
@@ -478,6 +501,7 @@ def md_greedy_accept(logits, draft, *, accepted=None, tokens=None, target=None,
     return accepted, tokens, target
 
 
+@_stream_scoped
 def md_kv_commit(lens, accepted, q_len, *, idx=None, ring_start=0, ring_len=None, stream=None):
     """lens [B] int32 in place: C -> C + accepted + 1; with idx [B, Hkv, stride]
     the kept positions also enter each list's ring [ring_start, ring_start + ring_len)."""
@@ -493,6 +517,7 @@ def md_kv_commit(lens, accepted, q_len, *, idx=None, ring_start=0, ring_len=None
     return lens
 
 
+@_stream_scoped
 def md_streaming_list(prompt_lens, num_kv_heads, n_sink, window, *, idx=None, idx_len=None,
                       stream=None):
     """Sink-plus-window draft lists [B, Hkv, n_sink + window] and idx_len [B]."""
