@@ -131,15 +131,18 @@ attn_partial_kernel(const AttnParams p) {
   const int grp = lane >> 4;
 
   const int chunk = blockIdx.x % p.n_chunks;
-  const int unit = p.lpt ? lpt_unit(p, blockIdx.x, reinterpret_cast<int*>(lds))
-                         : static_cast<int>(blockIdx.x / p.n_chunks);
+  // Wave-uniform by construction; readfirstlane lets the compiler keep the
+  // unit's address arithmetic in scalar registers.
+  const int unit = __builtin_amdgcn_readfirstlane(
+      p.lpt ? lpt_unit(p, blockIdx.x, reinterpret_cast<int*>(lds))
+            : static_cast<int>(blockIdx.x / p.n_chunks));
   const int hk = unit % p.Hkv;
   const int b = unit / p.Hkv;
   const int L = p.L;
 
   // ---- the unit's visible range (a1/a5 of the method's hot path)
   UnitGeom u;
-  u.S = min(p.kv_lens[b], p.max_kv_len);
+  u.S = __builtin_amdgcn_readfirstlane(min(p.kv_lens[b], p.max_kv_len));
   if (u.S < 0) u.S = 0;
   int U = u.S;
   u.seg0 = u.S;
@@ -255,9 +258,44 @@ attn_partial_kernel(const AttnParams p) {
   // instruction -- full-row accesses stream markedly faster from HBM than
   // the 64 B-per-row pattern of the MFMA operand layout.  One address per
   // token serves both.  r: where this lane's token (lane & 31) lives.
+  // Full verify tiles (every tile of a unit but its last): the TPI tokens of
+  // load n are tokens v0 + n*TPI .. of one sequence -- and, with pages of at
+  // least TPI tokens, of one page, whose id lane n*TPI holds -- so the row
+  // group's address is wave-uniform and each lane adds a fixed 32-bit offset
+  // (its row within the group, its 16 B chunk within the row).  The loads
+  // then need no per-lane address arithmetic.
+  const bool fast_verify =
+      !IDX && p.mode == MD_MODE_VERIFY && (!PAGED || (1 << p.page_shift) >= SH::TPI);
+  const uint32_t lane_off = static_cast<uint32_t>(
+      (lane / SH::LPT) * p.s_tok * SH::ES + (lane % SH::LPT) * 16);
+  auto load_tile_full = [&](TileRegs& T, int v0, TokRef r) {
+    T.ok = (1u << SH::NV) - 1u;
+    T.tok = r.tok;
+    for (int n = 0; n < SH::NV; ++n) {
+      int64_t base;  // element offset of token v0 + n*TPI in kv head hk (uniform)
+      if constexpr (PAGED) {
+        const int pid = __builtin_amdgcn_readlane(r.pid, n * SH::TPI);
+        const bool pg_ok = pid >= 0 && pid < p.num_pages;
+        base = pg_ok ? static_cast<int64_t>(pid) * p.s_blk +
+                           static_cast<int64_t>((v0 + n * SH::TPI) & pmask) * p.s_tok + head_off
+                     : 0;  // a page outside the pool: element 0, the row reads as zero
+        if (!pg_ok) T.ok &= ~(1u << n);
+      } else {
+        base = static_cast<int64_t>(b) * p.s_blk + static_cast<int64_t>(v0 + n * SH::TPI) * p.s_tok +
+               head_off;
+      }
+      T.k[n] = ld16(kbase + base * SH::ES + lane_off);
+      T.v[n] = ld16(vbase + base * SH::ES + lane_off);
+    }
+  };
+
   auto load_tile = [&](TileRegs& T, int tile, TokRef r) {
     const int v0 = u.v_begin + tile * kTile;
     const bool live = tile < n_tiles;
+    if (fast_verify && live && v0 + kTile <= u.v_end) {
+      load_tile_full(T, v0, r);
+      return;
+    }
     T.ok = 0;
     T.tok = r.tok;
     for (int n = 0; n < SH::NV; ++n) {
