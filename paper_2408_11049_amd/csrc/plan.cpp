@@ -91,14 +91,18 @@ Plan make_plan(const md_attn_args* a, int mode, int n_sink, int window, int num_
   p.n_rows = static_cast<int64_t>(a->num_seqs) * L * a->num_q_heads;
   p.n_units = static_cast<int64_t>(a->num_seqs) * a->num_kv_heads;
 
-  // Resident workgroups: two of kWaves waves per compute unit.  When the units
-  // alone cover every slot, one chunk per unit avoids the merge pass; else
-  // split each unit's range until about two workgroups wait per slot, but
-  // never below kMinChunkTokens tokens per chunk.
-  const int64_t slots = static_cast<int64_t>(num_cus > 0 ? num_cus : 256) * 2;
+  // One workgroup of kWaves waves (one per SIMD) per compute unit is enough
+  // to stream at full rate.  When the units alone cover every compute unit,
+  // one chunk per unit avoids the merge pass; else each unit's range is split
+  // just until they do, never below kMinChunkTokens tokens per chunk.  (Every
+  // chunk pays a pipeline fill, a cross-wave merge and a partial write:
+  // measured on MI355X, splitting further -- two or four workgroups per
+  // compute unit -- was 5-15% slower on long caches and slower still on
+  // short draft ranges.)
+  const int64_t slots = num_cus > 0 ? num_cus : 256;
   int64_t n_chunks = 1;
   if (p.n_units > 0 && p.n_units < slots) {
-    n_chunks = ceil_div(2 * slots, p.n_units);
+    n_chunks = ceil_div(slots, p.n_units);
     int64_t cap = ceil_div(U, kMinChunkTokens);
     if (n_chunks > cap) n_chunks = cap;
     if (n_chunks < 1) n_chunks = 1;
