@@ -125,6 +125,37 @@ def cpu_baseline(c, w, budget_s=15.0, batch=32):
                       f"random order, verify + draft, {total_t:.1f} s of fp64 oracle time"}
 
 
+def cpu_oracle_extras(c, w, logits, draft_tok, q_obs, n_obs, t_accept_us, t_votes_us):
+    """The oracle beside the steps around verification: greedy acceptance
+    over the whole logits tensor, and SnapKV votes of a few sampled (prompt,
+    kv head) units scaled to the whole batch."""
+    import numpy as np
+
+    import oracle
+    import oracle.sdstep as sd
+    from paper_2408_11049_amd import workloads as wl
+
+    host_logits = wl.to_host_bits(logits)
+    host_draft = draft_tok.cpu().numpy()
+    t0 = time.perf_counter()
+    sd.greedy_accept(host_logits, host_draft)
+    t_acc = time.perf_counter() - t0
+    units = [(0, 0), (w.B // 2, w.Hkv // 2), (w.B - 1, w.Hkv - 1)]
+    G = w.Hq // w.Hkv
+    t_votes = 0.0
+    for b, hk in units:
+        q = wl.to_host_bits(q_obs[b: b + 1, :, hk * G: (hk + 1) * G])
+        _, k, _, S = wl.gather_unit(c, b, hk)
+        t0 = time.perf_counter()
+        oracle.snapkv_votes(q, k, S, pool=5)
+        t_votes += time.perf_counter() - t0
+    t_votes_all = t_votes / len(units) * w.B * w.Hkv
+    return {"greedy_accept_s (numpy, one thread, whole logits)": round(t_acc, 3),
+            "greedy_accept_gpu_speedup": round(t_acc / (t_accept_us * 1e-6), 1),
+            "snapkv_votes_s (fp64 C, one thread, 3 sampled units scaled to all)": round(t_votes_all, 2),
+            "snapkv_votes_gpu_speedup": round(t_votes_all / (t_votes_us * 1e-6), 1)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -390,9 +421,11 @@ def main():
                 "algorithmic_bytes_per_launch": bytes_v}
 
     cpu = None
+    oracle_extras = None
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (fp64 oracle on a bounded sample)")
         cpu = cpu_baseline(c, w)
+        oracle_extras = cpu_oracle_extras(c, w, logits, draft_tok, q_obs, n_obs, t_accept, t_votes)
 
     rec = {
         "metric": "K/V HBM GB/s (% of peak) and µs per verify+draft attention step",
@@ -439,6 +472,7 @@ def main():
             "read_ceiling_gbs": round(ceiling, 1),
             "pct_of_read_ceiling": round(100 * value / ceiling, 2),
             "wall_ms_per_step_incl_flush": round(wall * 1e3 / K, 4),
+            "cpu_oracle_extras": oracle_extras,
             "paper_context": "2.51x end-to-end speedup, Llama-3.1-8B SnapKV self-speculation, "
                              "8xH100 (Table 2): context only, not comparable",
         },
