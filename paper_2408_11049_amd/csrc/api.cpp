@@ -114,6 +114,15 @@ int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void*
   p.chunk_len = pl.chunk_len;
   p.num_seqs = a->num_seqs;
   p.lpt = longest_first(mode, pl.n_chunks, a->num_seqs, a->max_kv_len);
+  p.hp = pl.hp;
+  int64_t n_blocks = pl.n_groups * pl.n_chunks;
+  if (p.lpt && pl.hp == 2) {
+    // One workgroup per unit; the kernel pairs heads (and idles the surplus
+    // half) only when the lengths leave nothing for longest-first to balance.
+    p.hp = 1;
+    p.hp_auto = 1;
+    n_blocks = pl.n_units;
+  }
   p.o = a->o;
   p.lse = a->lse;
   p.n_rows = pl.n_rows;
@@ -124,7 +133,7 @@ int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void*
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int depth = prefetch_depth(pl.NT, mode);
   hipError_t e = launch_attn_partial(p, a->head_dim, bf16, pl.NT, paged, depth,
-                                     occupancy(pl.NT, depth, mode), pl.n_units * pl.n_chunks, s);
+                                     occupancy(pl.NT, depth, mode), n_blocks, s);
   if (e != hipSuccess) return hip_fail(e);
   if (pl.n_chunks > 1) {
     e = launch_merge_lse(pl.n_chunks, pl.n_rows, a->head_dim, bf16, p.part_o, p.part_lse, a->o,

@@ -8,9 +8,11 @@
 // kernel therefore streams every visible K/V element of a (sequence, kv head)
 // unit from HBM exactly once, for all G*(gamma+1) query rows that share it.
 //
-// One workgroup = one (unit, chunk); its kWaves waves take interleaved
-// 32-token tiles of the chunk and run independent online softmaxes, merged
-// through LDS at the end.  Per tile and wave:
+// One workgroup = one chunk of hp units (hp adjacent kv heads of a sequence,
+// so that the waves of a workgroup read neighbouring runs of each token row);
+// the kWaves / hp waves of a unit take interleaved 32-token tiles of the
+// chunk and run independent online softmaxes, merged through LDS at the end.
+// Per tile and wave:
 //   K  16 B loads straight into the MFMA A-operand layout (8 bf16 channels of
 //      one token per lane), Q held as the B operand for the whole chunk:
 //      S^T[token, row] = K Q^T on v_mfma_f32_16x16x32_bf16.
@@ -84,20 +86,47 @@ __device__ __forceinline__ int real_token(const UnitGeom& u, int v) {
 // Longest-processing-time-first dispatch.  Workgroups start roughly in
 // blockIdx order (round-robin over the XCDs), so with ragged lengths the
 // units that happen to start last set the finish time.  With p.lpt (one chunk
-// per unit, B <= kLptMaxSeqs), workgroup r instead takes the r-th unit in the
-// order (length descending, sequence ascending, kv head ascending): every
-// workgroup ranks the B clamped lengths in LDS (B compares per thread) and
-// picks the sequence of rank r / Hkv.  The order is a bijection, so each unit
-// is still computed once, with the same arithmetic.
+// per unit, B <= kLptMaxSeqs), workgroup r instead takes the r-th head group
+// in the order (length descending, sequence ascending, kv head ascending):
+// every workgroup ranks the B clamped lengths in LDS (B compares per thread)
+// and picks the sequence of rank r / gps, gps = Hkv / hp head groups per
+// sequence.  The order is a bijection, so each unit is still computed once,
+// with the same arithmetic.
+//
+// With p.hp_auto the grid has one workgroup per unit and the kernel chooses
+// hp here: head pairs stream faster, but there are half as many of them, too
+// few for longest-first to even out unequal lengths.  Pairs are taken when
+// the longest clamped length is within 1/16 of the mean (the workgroups past
+// the pairs then return at once); otherwise one head per workgroup.  Returns
+// the head group, or -1 for a workgroup with nothing to do.
 template <typename P>
-__device__ __forceinline__ int lpt_unit(const P& p, int r, int* sl) {
+__device__ __forceinline__ int lpt_group(const P& p, int r, int* sl, int& hp) {
   const int B = p.num_seqs;
   for (int t = threadIdx.x; t < B; t += kWaves * 64) {
     const int s = min(p.kv_lens[t], p.max_kv_len);
     sl[t] = s < 0 ? 0 : s;
   }
   __syncthreads();
-  const int want = r / p.Hkv;
+  if (p.hp_auto) {
+    if (threadIdx.x < 64) {
+      int mx = 0;
+      long long sum = 0;
+      for (int t = threadIdx.x; t < B; t += 64) {
+        mx = max(mx, sl[t]);
+        sum += sl[t];
+      }
+      for (int o = 32; o >= 1; o >>= 1) {
+        mx = max(mx, __shfl_xor(mx, o));
+        sum += __shfl_xor(sum, o);
+      }
+      if (threadIdx.x == 0) sl[kLptMaxSeqs + 1] = 16LL * mx * B <= 17LL * sum ? 2 : 1;
+    }
+    __syncthreads();
+    hp = sl[kLptMaxSeqs + 1];
+  }
+  const int gps = p.Hkv / hp;
+  if (r >= B * gps) return -1;  // uniform over the workgroup: it returns as a whole
+  const int want = r / gps;
   for (int t = threadIdx.x; t < B; t += kWaves * 64) {
     const int lt = sl[t];
     int rank = 0;
@@ -110,7 +139,7 @@ __device__ __forceinline__ int lpt_unit(const P& p, int r, int* sl) {
   __syncthreads();
   const int b = sl[kLptMaxSeqs];
   __syncthreads();  // the LDS is reused by the tiles
-  return b * p.Hkv + r % p.Hkv;
+  return b * gps + r % gps;
 }
 
 template <int D, bool BF16, int NT, bool PAGED, bool IDX, int P, int OCC>
@@ -131,13 +160,28 @@ attn_partial_kernel(const AttnParams p) {
   const int grp = lane >> 4;
 
   const int chunk = blockIdx.x % p.n_chunks;
+  // The workgroup's head group: hp adjacent kv heads hk0 .. hk0+hp-1 of
+  // sequence b.  Wave w serves kv head hk0 + w % hp and is slot w / hp of
+  // that head's wph = kWaves / hp waves, which interleave its tiles.
   // Wave-uniform by construction; readfirstlane lets the compiler keep the
   // unit's address arithmetic in scalar registers.
-  const int unit = __builtin_amdgcn_readfirstlane(
-      p.lpt ? lpt_unit(p, blockIdx.x, reinterpret_cast<int*>(lds))
-            : static_cast<int>(blockIdx.x / p.n_chunks));
-  const int hk = unit % p.Hkv;
-  const int b = unit / p.Hkv;
+  int hp_sel = p.hp;
+  int group_sel;
+  if (p.lpt) {
+    group_sel = lpt_group(p, static_cast<int>(blockIdx.x), reinterpret_cast<int*>(lds), hp_sel);
+    if (group_sel < 0) return;
+  } else {
+    group_sel = static_cast<int>(blockIdx.x / p.n_chunks);
+  }
+  const int hp = __builtin_amdgcn_readfirstlane(hp_sel);
+  const int group = __builtin_amdgcn_readfirstlane(group_sel);
+  const int wph = kWaves / hp;
+  const int gps = p.Hkv / hp;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const int wslot = wave_u / hp;
+  const int b = group / gps;
+  const int hk0 = (group % gps) * hp;
+  const int hk = hk0 + wave_u % hp;
   const int L = p.L;
 
   // ---- the unit's visible range (a1/a5 of the method's hot path)
@@ -331,7 +375,7 @@ attn_partial_kernel(const AttnParams p) {
   unsigned char* vt_lds = kt_lds + SH::KTILE;
 
   // One tile: K and V rows to LDS, after which the tile's registers are
-  // refilled with tile `tile + P*kWaves` (so P tiles stay in flight through
+  // refilled with tile `tile + P*wph` (so P tiles stay in flight through
   // the compute below); then S^T = K Q^T, the online softmax and
   // O^T += V^T P^T, all operands read back from LDS.
   // Per-unit facts for the mask fast path: the smallest and largest query
@@ -371,8 +415,8 @@ attn_partial_kernel(const AttnParams p) {
     // run P tiles further ahead still, so waiting for one never waits on a
     // K/V load that is not already needed.
     {
-      const int ahead = tile + P * kWaves;
-      const TokRef far = load_ref(ahead + P * kWaves);
+      const int ahead = tile + P * wph;
+      const TokRef far = load_ref(ahead + P * wph);
       load_tile(T, ahead, ref_slot);
       ref_slot = far;
     }
@@ -516,16 +560,16 @@ attn_partial_kernel(const AttnParams p) {
   TokRef ref_ring[P];
   {
     TokRef ref0[P];
-    for (int s = 0; s < P; ++s) ref0[s] = load_ref(wave + s * kWaves);
-    for (int s = 0; s < P; ++s) ref_ring[s] = load_ref(wave + (s + P) * kWaves);
-    for (int s = 0; s < P; ++s) load_tile(ring[s], wave + s * kWaves, ref0[s]);
+    for (int s = 0; s < P; ++s) ref0[s] = load_ref(wslot + s * wph);
+    for (int s = 0; s < P; ++s) ref_ring[s] = load_ref(wslot + (s + P) * wph);
+    for (int s = 0; s < P; ++s) load_tile(ring[s], wslot + s * wph, ref0[s]);
   }
   // Every ring slot is processed unconditionally (a tile past the chunk is
   // fully masked: it leaves m, l and O unchanged), so no slot becomes a
   // conditionally-updated loop-carried value that would force a full wait.
-  for (int base = wave; base < n_tiles; base += P * kWaves) {
+  for (int base = wslot; base < n_tiles; base += P * wph) {
 #pragma unroll
-    for (int s = 0; s < P; ++s) process(ring[s], base + s * kWaves, ref_ring[s]);
+    for (int s = 0; s < P; ++s) process(ring[s], base + s * wph, ref_ring[s]);
   }
 
   // ---- row sums: add the 4 lanes that share a row
@@ -534,7 +578,8 @@ attn_partial_kernel(const AttnParams p) {
     l_run[rt] += __shfl_xor(l_run[rt], 32);
   }
 
-  // ---- merge the kWaves waves of the workgroup (LDS reused after the loop)
+  // ---- merge the waves of each unit (LDS reused after the loop): wave w
+  // holds unit hk0 + w % hp, so unit hs's waves are j * hp + hs, j < wph.
   __syncthreads();
   float* sm_m = reinterpret_cast<float*>(lds + kMergeO);
   float* sm_l = sm_m + kWaves * ROWS;
@@ -546,17 +591,21 @@ attn_partial_kernel(const AttnParams p) {
     }
   }
   __syncthreads();
+  // The unit's running max M and total L_total of row r over its waves.
+  auto row_stats = [&](int hs, int r, float& M, float& Lt) {
+    M = -INFINITY;
+    Lt = 0.f;
+    for (int j = 0; j < wph; ++j) M = fmaxf(M, sm_m[(j * hp + hs) * ROWS + r]);
+    if (M != -INFINITY)
+      for (int j = 0; j < wph; ++j) {
+        const float mw = sm_m[(j * hp + hs) * ROWS + r];
+        if (mw != -INFINITY) Lt += sm_l[(j * hp + hs) * ROWS + r] * fast_exp2(mw - M);
+      }
+  };
   // Each wave rescales its own O by 2^(m_w - M) / L_total.
   for (int rt = 0; rt < NT; ++rt) {
-    const int r = rt * 16 + l16;
-    float M = -INFINITY;
-    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, sm_m[w * ROWS + r]);
-    float Lt = 0.f;
-    if (M != -INFINITY)
-      for (int w = 0; w < kWaves; ++w) {
-        float mw = sm_m[w * ROWS + r];
-        if (mw != -INFINITY) Lt += sm_l[w * ROWS + r] * fast_exp2(mw - M);
-      }
+    float M, Lt;
+    row_stats(wave_u % hp, rt * 16 + l16, M, Lt);
     float f = 0.f;
     if (m_run[rt] != -INFINITY && Lt > 0.f) f = fast_exp2(m_run[rt] - M) / Lt;
     for (int c = 0; c < SH::CB16; ++c) acc[rt][c] *= f;
@@ -564,30 +613,30 @@ attn_partial_kernel(const AttnParams p) {
 
   const bool direct = p.n_chunks == 1;
   const int tid = threadIdx.x;
+  constexpr int kGroupsPerRow = D / 8;
+  constexpr int kItemsPerUnit = 16 * kGroupsPerRow;  // (row of a row tile, 8 channels)
   for (int rt = 0; rt < NT; ++rt) {
     // Wave w writes its scaled O^T rows (lane: row l16, channels c*16+4grp..+3).
     for (int c = 0; c < SH::CB16; ++c)
       *reinterpret_cast<f32x4*>(mo + (wave * 16 + l16) * D + c * 16 + grp * 4) = acc[rt][c];
     __syncthreads();
-    // Thread -> (row, 8 channels); sum the waves in a fixed order.
-    constexpr int kGroupsPerRow = D / 8;
-    const int rr = tid / kGroupsPerRow;
-    const int c0 = (tid % kGroupsPerRow) * 8;
-    const int r = rt * 16 + rr;
-    if (rr < 16 && r < p.R) {
+    // Thread -> (unit hs, row, 8 channels); sum the unit's waves in a fixed order.
+    for (int item = tid; item < hp * kItemsPerUnit; item += kWaves * 64) {
+      const int hs = item / kItemsPerUnit;
+      const int rr = (item % kItemsPerUnit) / kGroupsPerRow;
+      const int c0 = (item % kGroupsPerRow) * 8;
+      const int r = rt * 16 + rr;
+      if (r >= p.R) continue;
       float o8[8];
       for (int j = 0; j < 8; ++j) o8[j] = 0.f;
-      for (int w = 0; w < kWaves; ++w)
+      for (int jw = 0; jw < wph; ++jw) {
+        const int w = jw * hp + hs;
         for (int j = 0; j < 8; ++j) o8[j] += mo[(w * 16 + rr) * D + c0 + j];
-      const int i = r / p.G, h = hk * p.G + r % p.G;
+      }
+      const int i = r / p.G, h = (hk0 + hs) * p.G + r % p.G;
       const int64_t row_g = (static_cast<int64_t>(b) * L + i) * p.Hq + h;
-      float M = -INFINITY, Lt = 0.f;
-      for (int w = 0; w < kWaves; ++w) M = fmaxf(M, sm_m[w * ROWS + r]);
-      if (M != -INFINITY)
-        for (int w = 0; w < kWaves; ++w) {
-          float mw = sm_m[w * ROWS + r];
-          if (mw != -INFINITY) Lt += sm_l[w * ROWS + r] * fast_exp2(mw - M);
-        }
+      float M, Lt;
+      row_stats(hs, r, M, Lt);
       const float lse = (Lt > 0.f) ? (M + fast_log2(Lt)) * 0.69314718055994530942f : -INFINITY;
       if (direct) {
         if constexpr (BF16) {

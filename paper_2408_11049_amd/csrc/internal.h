@@ -16,8 +16,10 @@ namespace md {
 // that kv head are packed into 16-row MFMA tiles and stream the unit's K/V
 // once.  The unit's visible key range (the whole causal prefix for verify;
 // sinks followed by the window for draft, read as one virtual range) is cut
-// into n_chunks chunks of chunk_len tokens; each chunk is one workgroup of
-// kWaves waves, which interleave kTile-token tiles.  With n_chunks > 1 the
+// into n_chunks chunks of chunk_len tokens.  A workgroup of kWaves waves
+// takes one chunk of hp units of the same sequence (hp adjacent kv heads):
+// kWaves / hp waves per unit, which interleave kTile-token tiles.  With
+// n_chunks > 1 the
 // chunks write normalised partial results and a merge pass combines them
 // by log-sum-exp (the split-KV decomposition named in the paper's Sec. 2).
 constexpr int kWaves = 4;
@@ -38,6 +40,8 @@ struct Plan {
   int32_t chunk_len = 0;
   int64_t n_rows = 0;    // B * L * Hq
   int64_t n_units = 0;   // B * Hkv
+  int32_t hp = 1;        // units (adjacent kv heads) per workgroup
+  int64_t n_groups = 0;  // n_units / hp; the grid is n_groups * n_chunks
   size_t part_o_bytes = 0;   // workspace: [n_chunks][n_rows][d] fp32 partial O
   size_t part_lse_bytes = 0; // workspace: [n_chunks][n_rows] fp32 partial lse
   size_t workspace_bytes = 0;

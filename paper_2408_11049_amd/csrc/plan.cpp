@@ -2,6 +2,7 @@
 // Pure host arithmetic: no HIP call is made here, so every error path can be
 // exercised on a machine without a GPU.
 #include <limits.h>
+#include <stdlib.h>
 
 #include <algorithm>
 
@@ -80,6 +81,32 @@ int validate_attn(const md_attn_args* a, int mode, int n_sink, int window) {
   return MD_OK;
 }
 
+// Kv heads per workgroup.  In the token-major cache the kv heads of a token
+// are adjacent, so a workgroup that serves two heads of a sequence (two waves
+// each) reads 2 x 256 B runs of every token row (bf16, d = 128) side by side
+// instead of one: on MI355X a load-only model of the verify stream read the
+// B = 64, S = 32768 cache at 7.03 TB/s this way against 6.62 TB/s with one
+// head per workgroup, and the verify kernel gained 5-6% on the large-batch
+// workloads.  Pairs halve the number of workgroups, though: a streaming
+// draft's short range then needs twice the chunks and their merge, which
+// costs more than the pairing gains unless the pairs alone fill the device.
+// A listed draft reads a different list per head -- no adjacent rows -- and
+// keeps one head per workgroup.  MD_HEADS_PER_WG (1 or 2) overrides, for
+// measurement.
+static int heads_per_workgroup(const md_attn_args* a, int mode, int64_t slots) {
+  static const int forced = [] {
+    const char* s = getenv("MD_HEADS_PER_WG");
+    const int v = s ? atoi(s) : 0;
+    return (v == 1 || v == 2) ? v : 0;
+  }();
+  if (a->num_kv_heads % 2) return 1;
+  if (forced) return forced;
+  const int64_t pairs = static_cast<int64_t>(a->num_seqs) * a->num_kv_heads / 2;
+  if (mode == MD_MODE_VERIFY) return 2;
+  if (mode == MD_MODE_DRAFT) return pairs >= slots ? 2 : 1;
+  return 1;
+}
+
 Plan make_plan(const md_attn_args* a, int mode, int n_sink, int window, int num_cus) {
   Plan p;
   const int L = a->q_len;
@@ -92,17 +119,19 @@ Plan make_plan(const md_attn_args* a, int mode, int n_sink, int window, int num_
   p.n_units = static_cast<int64_t>(a->num_seqs) * a->num_kv_heads;
 
   // One workgroup of kWaves waves (one per SIMD) per compute unit is enough
-  // to stream at full rate.  When the units alone cover every compute unit,
-  // one chunk per unit avoids the merge pass; else each unit's range is split
-  // just until they do, never below kMinChunkTokens tokens per chunk.  (Every
+  // to stream at full rate.  When the workgroups alone cover every compute
+  // unit, one chunk per unit avoids the merge pass; else each unit's range is
+  // split just until they do, never below kMinChunkTokens tokens per chunk.  (Every
   // chunk pays a pipeline fill, a cross-wave merge and a partial write:
   // measured on MI355X, splitting further -- two or four workgroups per
   // compute unit -- was 5-15% slower on long caches and slower still on
   // short draft ranges.)
   const int64_t slots = num_cus > 0 ? num_cus : 256;
+  p.hp = heads_per_workgroup(a, mode, slots);
+  p.n_groups = p.n_units / p.hp;
   int64_t n_chunks = 1;
-  if (p.n_units > 0 && p.n_units < slots) {
-    n_chunks = ceil_div(slots, p.n_units);
+  if (p.n_groups > 0 && p.n_groups < slots) {
+    n_chunks = ceil_div(slots, p.n_groups);
     int64_t cap = ceil_div(U, kMinChunkTokens);
     if (n_chunks > cap) n_chunks = cap;
     if (n_chunks < 1) n_chunks = 1;

@@ -44,6 +44,7 @@ SMALL = [
     ("bf16_page1", 2, 3, 4, 2, 64, [37, 20], "bf16", 1, 2, 9),
     ("bf16_page64", 2, 3, 4, 2, 128, [300, 129], "bf16", 64, 2, 40),
     ("f32_rows40_split", 1, 5, 8, 1, 128, [2600], "f32", 0, 16, 100),
+    ("bf16_head_pairs_split_paged", 2, 5, 16, 4, 128, [4000, 2500], "bf16", 16, 16, 496),
 ]
 
 
@@ -129,13 +130,17 @@ def test_indexed_against_oracle(case):
         assert torch.equal(o2, o) and torch.equal(l2, l), "an unlisted key was read"
 
 
-def test_longest_first_dispatch_ragged():
+@pytest.mark.parametrize("lo", [600, 5800], ids=["ragged_single_heads", "even_head_pairs"])
+def test_longest_first_dispatch(lo):
     """A verify launch that takes units longest first (one chunk per unit:
-    64 sequences x 8 kv heads, ragged lengths up to 6000, a paged cache):
-    whole output against the oracle, NaN padding included."""
+    64 sequences x 8 kv heads, lengths up to 6000, a paged cache): whole
+    output against the oracle, NaN padding included.  With lengths 600..6000
+    each workgroup serves one kv head; with 5800..6000 (every length within
+    1/16 of the mean) the kernel pairs the heads and half the workgroups
+    return without work."""
     B, L, Hq, Hkv, d = 64, 4, 8, 8, 64
     rng = np.random.default_rng(64)
-    lens = rng.integers(600, 6001, size=B)
+    lens = rng.integers(lo, 6001, size=B)
     lens[rng.integers(B)] = 6000
     say(f"[parity] longest-first verify: B={B} Hkv={Hkv} lens {lens.min()}..{lens.max()}")
     c = wl.make_case(B=B, q_len=L, Hq=Hq, Hkv=Hkv, d=d, kv_lens=lens, dtype="bf16", page_size=16,
