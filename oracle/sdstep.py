@@ -1,6 +1,7 @@
 """Oracle for the steps around each verification: greedy acceptance with a
 bonus token, writing the verified tokens' K/V into the cache, committing the
-accepted length, and the rolling list of a StreamingLLM-style draft cache.
+accepted length, the rolling list of a StreamingLLM-style draft cache, and
+gathering a static selection into a draft cache of its own.
 
 TEST INFRASTRUCTURE ONLY: only ``tests/``, ``__graft_entry__.smoke()`` and the
 ``cpu_baseline`` leg of ``bench.py`` may use this module.  It shares no code
@@ -85,6 +86,34 @@ def kv_append(cache, new, pos0, page_size=0, page_table=None):
             blk, tok = cache_slot(b, int(pos0[b]) + i, page_size, page_table)
             out[blk, tok] = new[b, i]
     return out
+
+
+def kv_gather(dst, src, idx, idx_len, src_lens, *, src_page_size=0, src_page_table=None,
+              dst_page_size=0, dst_page_table=None):
+    """A static selection gathered into a draft cache of its own: a static KV
+    selection collects its sparse cache once, before generation, so drafting
+    then reads it like any cache (Sec. 4.2).  src and dst hold one of K or V,
+    as in kv_append.  For every sequence b, kv head h and
+    j < n_b = min(idx_len[b], stride) (idx [B, Hkv, stride]), row j of head h
+    of dst takes row p = idx[b, h, j] of head h of src if 0 <= p < src_lens[b],
+    and zeros otherwise.  Values move unchanged.
+
+    Returns (updated copy of dst, n [B])."""
+    out = np.array(dst, copy=True)
+    idx = np.asarray(idx)
+    B, Hkv, stride = idx.shape
+    n = np.clip(np.asarray(idx_len, np.int64), 0, stride)
+    for b in range(B):
+        for h in range(Hkv):
+            for j in range(int(n[b])):
+                p = int(idx[b, h, j])
+                dblk, dtok = cache_slot(b, j, dst_page_size, dst_page_table)
+                if 0 <= p < int(src_lens[b]):
+                    sblk, stok = cache_slot(b, p, src_page_size, src_page_table)
+                    out[dblk, dtok, h] = src[sblk, stok, h]
+                else:
+                    out[dblk, dtok, h] = 0
+    return out, n
 
 
 def kv_commit(lens, accepted):

@@ -18,6 +18,12 @@ real module and ``test_oracle_mutants.py`` on copies with a planted mistake.
   commit/ring_*    C' = C + a + 1; after any sequence of steps the rolling
                    list holds exactly the sinks and the last W committed
                    positions, each once (the StreamingLLM cache, Sec. 5.1).
+  gather_*         a hand-worked gather (unusable entries and an over-long
+                   idx_len included); paged == contiguous read back through
+                   an independent gather; and attention over the gathered
+                   cache with the speculated rows appended equals the listed
+                   draft over the full cache (the fp64 attention oracles,
+                   pinned on their own).
 """
 import itertools
 
@@ -180,5 +186,92 @@ def pin_ring_window(mod=None):
             C = s.kv_commit(C, acc)
 
 
+def pin_gather_by_hand(mod=None):
+    s = _m(mod)
+    # src[b, t, h, 0] = 100 b + 10 t + h + 1 (no zeros, so a zero row shows).
+    src = np.zeros((2, 4, 2, 1), np.float32)
+    for b in range(2):
+        for t in range(4):
+            for h in range(2):
+                src[b, t, h, 0] = 100 * b + 10 * t + h + 1
+    idx = np.array([[[3, 0, 2], [-1, 2, 5]],
+                    [[1, 0, 9], [2, 3, 0]]], np.int32)
+    src_lens = [4, 3]
+    want = np.full((2, 4, 2, 1), -7.0, np.float32)
+    # sequence 0: three entries; -1 and 5 (>= 4) are unusable -> zeros
+    want[0, 0, :, 0] = [31, 0]
+    want[0, 1, :, 0] = [1, 22]
+    want[0, 2, :, 0] = [21, 0]
+    # sequence 1: two entries; position 3 is not below src_lens = 3 -> zero
+    want[1, 0, :, 0] = [111, 122]
+    want[1, 1, :, 0] = [101, 0]
+    for idx_len in ([3, 2], [5, 2]):  # idx_len past the stride is clamped
+        got, n = s.kv_gather(np.full((2, 4, 2, 1), -7.0, np.float32), src, idx, idx_len, src_lens)
+        assert np.array_equal(got, want), (idx_len, got[..., 0])
+        assert list(n) == [3, 2], n
+
+
+def pin_gather_paged_contiguous(mod=None):
+    s = _m(mod)
+    rng = np.random.default_rng(16)
+    B, Hkv, d, ps, S_alloc, D_alloc, stride = 3, 2, 4, 4, 16, 8, 8
+    src = rng.standard_normal((B, S_alloc, Hkv, d)).astype(np.float32)
+    spages = rng.permutation(B * (S_alloc // ps)).reshape(B, S_alloc // ps)
+    src_p = np.zeros((B * S_alloc // ps, ps, Hkv, d), np.float32)
+    for b in range(B):
+        for j in range(S_alloc):
+            src_p[spages[b, j // ps], j % ps] = src[b, j]
+    dpages = rng.permutation(B * (D_alloc // ps)).reshape(B, D_alloc // ps)
+    idx = rng.integers(-2, S_alloc + 2, size=(B, Hkv, stride)).astype(np.int32)
+    idx_len, src_lens = np.array([8, 3, 0]), np.array([16, 9, 5])
+    dst = rng.standard_normal((B, D_alloc, Hkv, d)).astype(np.float32)
+    dst_p = np.zeros((B * D_alloc // ps, ps, Hkv, d), np.float32)
+    for b in range(B):
+        for j in range(D_alloc):
+            dst_p[dpages[b, j // ps], j % ps] = dst[b, j]
+    c2, n = s.kv_gather(dst, src, idx, idx_len, src_lens)
+    p2, _ = s.kv_gather(dst_p, src_p, idx, idx_len, src_lens, src_page_size=ps,
+                        src_page_table=spages, dst_page_size=ps, dst_page_table=dpages)
+    for b in range(B):
+        for j in range(D_alloc):
+            for h in range(Hkv):
+                if j < n[b]:
+                    p = idx[b, h, j]
+                    want = src[b, p, h] if 0 <= p < src_lens[b] else np.zeros(d, np.float32)
+                else:
+                    want = dst[b, j, h]
+                assert np.array_equal(_gather(c2, b, j, 0, None)[h], want), (b, j, h)
+                assert np.array_equal(_gather(p2, b, j, ps, dpages)[h], want), (b, j, h)
+
+
+def pin_gather_listed_draft_equivalence(mod=None):
+    import oracle
+
+    s = _m(mod)
+    rng = np.random.default_rng(17)
+    B, L, Hq, Hkv, d, S_alloc, stride = 2, 3, 4, 2, 16, 48, 12
+    S = np.array([40, 25], np.int32)
+    q = rng.standard_normal((B, L, Hq, d)).astype(np.float32)
+    k = rng.standard_normal((B, S_alloc, Hkv, d)).astype(np.float32)
+    v = rng.standard_normal((B, S_alloc, Hkv, d)).astype(np.float32)
+    n = np.array([10, 6], np.int32)
+    idx = np.full((B, Hkv, stride), -1, np.int32)
+    for b in range(B):
+        for h in range(Hkv):
+            idx[b, h, : n[b]] = np.sort(rng.choice(S[b] - L, size=n[b], replace=False))
+    ro, rl = oracle.indexed(q, k, v, S, idx, n)
+    kc, nk = s.kv_gather(np.zeros((B, 16, Hkv, d), np.float32), k, idx, n, S - L)
+    vc, _ = s.kv_gather(np.zeros((B, 16, Hkv, d), np.float32), v, idx, n, S - L)
+    spec_k = np.stack([k[b, S[b] - L: S[b]] for b in range(B)])
+    spec_v = np.stack([v[b, S[b] - L: S[b]] for b in range(B)])
+    kc = s.kv_append(kc, spec_k, nk)
+    vc = s.kv_append(vc, spec_v, nk)
+    go, gl = oracle.attention(oracle.VERIFY, q, kc, vc, (nk + L).astype(np.int32))
+    assert np.allclose(go, ro, rtol=0, atol=1e-12), np.max(np.abs(go - ro))
+    assert np.allclose(gl, rl, rtol=0, atol=1e-12), np.max(np.abs(gl - rl))
+
+
 ALL_SDSTEP_PINS = [pin_accept_eq1, pin_accept_cases, pin_argmax_brute, pin_argmax_bf16,
-                   pin_append_paged_contiguous, pin_commit_lengths, pin_ring_window]
+                   pin_append_paged_contiguous, pin_commit_lengths, pin_ring_window,
+                   pin_gather_by_hand, pin_gather_paged_contiguous,
+                   pin_gather_listed_draft_equivalence]

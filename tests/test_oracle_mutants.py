@@ -101,6 +101,15 @@ SDSTEP_MUTANTS = [
     ("streaming: window one short", "range(max(n_sink, C - window), C)",
      "range(max(n_sink, C - window + 1), C)"),
     ("streaming: sinks dropped", "for j in range(min(n_sink, C)):", "for j in range(0):"),
+    ("gather: the next head's row", "out[dblk, dtok, h] = src[sblk, stok, h]",
+     "out[dblk, dtok, h] = src[sblk, stok, (h + 1) % Hkv]"),
+    ("gather: unusable entries copied", "if 0 <= p < int(src_lens[b]):", "if 0 <= p < src.shape[1]:"),
+    ("gather: destination row shifted", "dblk, dtok = cache_slot(b, j, dst_page_size",
+     "dblk, dtok = cache_slot(b, j + 1, dst_page_size"),
+    ("gather: source position off by one", "sblk, stok = cache_slot(b, p, src_page_size",
+     "sblk, stok = cache_slot(b, p + 1, src_page_size"),
+    ("gather: idx_len not clamped", "n = np.clip(np.asarray(idx_len, np.int64), 0, stride)",
+     "n = np.asarray(idx_len, np.int64)"),
 ]
 
 
