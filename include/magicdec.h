@@ -354,6 +354,41 @@ int md_streaming_list(int32_t num_seqs, int32_t num_kv_heads, const int32_t* pro
                       void* stream);
 
 /*
+ * Gather a static selection into a draft cache of its own, once, before
+ * generation (Sec. 4.2: a static KV selection collects its sparse cache up
+ * front, so drafting pays no search).  A draft step then streams the
+ * gathered rows contiguously instead of reading each listed row of the full
+ * cache (md_draft_attn_indexed).  For every sequence b, kv head h and
+ * j < n_b = min(max(idx_len[b], 0), idx_stride): row j of head h of dst gets
+ * the K and V rows of head h at position p = idx[b][h][j] of src when
+ * 0 <= p < src_lens[b], and zeros otherwise.
+ *   dst, src   caches with equal num_seqs, num_kv_heads, head_dim and dtype
+ *              (contiguous or paged, independently); their memory must not
+ *              overlap
+ *   idx        device int32 [B, Hkv, idx_stride] (md_snapkv_select's lists)
+ *   idx_len    device int32 [B]
+ *   src_lens   device int32 [B]: how many positions of src are valid
+ *   dst_lens   device int32 [B] out, or NULL: set to n_b; must not overlap
+ *              idx_len or src_lens
+ * Values move bit for bit.  Rows past dst's capacity (or its table), and
+ * pages outside [0, num_pages), are not written.
+ * Drafting over dst: md_kv_append the step's rows at position dst_lens[b] of
+ * dst (as of the full cache), then md_verify_attn over dst with kv_lens =
+ * dst_lens + q_len; md_kv_commit then advances dst_lens like the full
+ * cache's lengths.  The gathered rows come first and every query sees them,
+ * the speculated rows last and causally: md_draft_attn_indexed over
+ * (src, idx) for lists of usable entries.  An unusable entry gathers a zero
+ * row, which takes part in that attention (score 0, value 0) where
+ * md_draft_attn_indexed skips the entry.
+ * Errors: MD_ERR_INVALID_ARG for NULL or misaligned pointers, a malformed or
+ * mismatched cache, idx_stride < 1, dst_lens overlapping idx_len or
+ * src_lens; MD_ERR_HIP.
+ */
+int md_kv_gather(const md_kv_cache* dst, const md_kv_cache* src, const int32_t* idx,
+                 int32_t idx_stride, const int32_t* idx_len, const int32_t* src_lens,
+                 int32_t* dst_lens, void* stream);
+
+/*
  * ---- Speculative-decoding cost model (Sec. 3.1 Eq. 1-2; Sec. 4.1 Eq. 3-4) ----
  *
  * Host-only arithmetic (no device, no stream), for choosing the speculation

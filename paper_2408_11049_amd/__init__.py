@@ -14,6 +14,7 @@ CPU fallback: if the library is missing, every call raises.
     md_greedy_accept(logits, draft, ...)          -> (accepted, tokens, target)
     md_kv_commit(lens, accepted, q_len, ...)      (in place)
     md_streaming_list(prompt_lens, Hkv, n_sink, window) -> (idx, idx_len)
+    md_kv_gather(dst_k, dst_v, src_k, src_v, idx, idx_len, src_lens, ...) -> dst_lens
     md_sd_expected_tokens / md_sd_latency_ratio / md_sd_best_gamma /
     md_sd_alpha_from_omega                        (host-only cost model, Eq. 1-4)
 
@@ -39,7 +40,7 @@ EXPORTED = ["md_verify_attn", "md_draft_attn", "md_draft_attn_indexed", "md_merg
             "md_workspace_bytes", "md_workspace_bytes_indexed", "md_snapkv_votes",
             "md_snapkv_workspace_bytes", "md_snapkv_select", "md_kv_append",
             "md_greedy_accept", "md_greedy_accept_workspace_bytes", "md_kv_commit",
-            "md_streaming_list", "md_sd_expected_tokens", "md_sd_latency_ratio",
+            "md_streaming_list", "md_kv_gather", "md_sd_expected_tokens", "md_sd_latency_ratio",
             "md_sd_best_gamma", "md_sd_alpha_from_omega",
             "md_status_str", "md_last_hip_error", "md_attn_args_size",
             "md_bench_stream_read", "md_bench_copy", "md_bench_fill"]
@@ -135,6 +136,9 @@ def load_library(path: str = LIB_PATH):
     lib.md_kv_commit.restype = ctypes.c_int
     lib.md_streaming_list.argtypes = [i32, i32, vp, i32, i32, vp, vp, vp]
     lib.md_streaming_list.restype = ctypes.c_int
+    lib.md_kv_gather.argtypes = [ctypes.POINTER(MdKvCache), ctypes.POINTER(MdKvCache), vp, i32,
+                                 vp, vp, vp, vp]
+    lib.md_kv_gather.restype = ctypes.c_int
     f64 = ctypes.c_double
     lib.md_sd_expected_tokens.argtypes = [i32, f64]
     lib.md_sd_expected_tokens.restype = f64
@@ -534,6 +538,27 @@ def md_streaming_list(prompt_lens, num_kv_heads, n_sink, window, *, idx=None, id
     return idx, idx_len
 
 
+@_stream_scoped
+def md_kv_gather(dst_k, dst_v, src_k, src_v, idx, idx_len, src_lens, *, dst_page_table=None,
+                 src_page_table=None, dst_lens=None, stream=None):
+    """Gather each (sequence, kv head)'s listed rows idx [B, Hkv, stride] of the
+    src cache into rows 0.. of the dst cache (in place), zeros for entries
+    outside [0, src_lens[b]).  Returns dst_lens [B] int32 = min(idx_len, stride)."""
+    import torch
+    lib = load_library()
+    B, Hkv, stride = idx.shape
+    if idx.dtype != torch.int32 or not idx.is_contiguous():
+        raise ValueError("idx must be contiguous int32 [B, Hkv, stride]")
+    dst = make_kv_cache(dst_k, dst_v, num_seqs=B, page_table=dst_page_table)
+    src = make_kv_cache(src_k, src_v, num_seqs=B, page_table=src_page_table)
+    if dst_lens is None:
+        dst_lens = torch.empty((B,), dtype=torch.int32, device=idx.device)
+    _check(lib.md_kv_gather(ctypes.byref(dst), ctypes.byref(src), _ptr(idx), stride,
+                            _ptr(idx_len), _ptr(src_lens), _ptr(dst_lens),
+                            _stream_handle(idx, stream)))
+    return dst_lens
+
+
 def md_sd_expected_tokens(gamma: int, alpha: float) -> float:
     """Eq. 1: expected tokens per verification (NaN for invalid arguments)."""
     return load_library().md_sd_expected_tokens(int(gamma), float(alpha))
@@ -573,3 +598,4 @@ kv_append = md_kv_append
 greedy_accept = md_greedy_accept
 kv_commit = md_kv_commit
 streaming_list = md_streaming_list
+kv_gather = md_kv_gather

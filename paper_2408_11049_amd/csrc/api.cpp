@@ -16,6 +16,28 @@ namespace md {
 
 namespace {
 
+CacheView cache_view(const md_kv_cache* c) {
+  CacheView v{};
+  v.k = static_cast<unsigned char*>(c->k);
+  v.v = static_cast<unsigned char*>(c->v);
+  v.s_blk = c->kv_stride_blk;
+  v.s_tok = c->kv_stride_tok;
+  v.s_head = c->kv_stride_head;
+  v.page_table = c->page_table;
+  v.page_shift = 0;
+  if (c->page_size)
+    while ((1 << v.page_shift) < c->page_size) ++v.page_shift;
+  v.max_pages = c->max_pages_per_seq;
+  v.num_pages = c->num_pages;
+  v.capacity = c->capacity;
+  return v;
+}
+
+bool overlaps(const void* a, const void* b, size_t n) {
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return x < y + n && y < x + n;
+}
+
 thread_local std::string g_last_hip_error;
 
 int hip_fail(hipError_t e) {
@@ -335,6 +357,49 @@ int md_kv_append(const md_kv_cache* c, int32_t n_new, const void* k_new, const v
   p.row_vecs = c->head_dim * es / 16;
   p.n_items = 2 * static_cast<int64_t>(c->num_seqs) * n_new * c->num_kv_heads * p.row_vecs;
   const hipError_t e = md::launch_kv_append(p, c->page_size != 0, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? MD_OK : md::hip_fail(e);
+}
+
+int md_kv_gather(const md_kv_cache* dst, const md_kv_cache* src, const int32_t* idx,
+                 int32_t idx_stride, const int32_t* idx_len, const int32_t* src_lens,
+                 int32_t* dst_lens, void* stream) {
+  int st = md::validate_kv_cache(dst, 0);
+  if (st != MD_OK) return st;
+  st = md::validate_kv_cache(src, 0);
+  if (st != MD_OK) return st;
+  if (dst->num_seqs != src->num_seqs || dst->num_kv_heads != src->num_kv_heads ||
+      dst->head_dim != src->head_dim || dst->dtype != src->dtype || idx_stride < 1)
+    return MD_ERR_INVALID_ARG;
+  if (dst->num_seqs == 0) return MD_OK;
+  if (!dst->k || !dst->v || !src->k || !src->v || !idx || !idx_len || !src_lens)
+    return MD_ERR_INVALID_ARG;
+  if (!md::aligned16(dst->k) || !md::aligned16(dst->v) || !md::aligned16(src->k) ||
+      !md::aligned16(src->v) || (reinterpret_cast<uintptr_t>(idx) & 3u) ||
+      (reinterpret_cast<uintptr_t>(idx_len) & 3u) || (reinterpret_cast<uintptr_t>(src_lens) & 3u) ||
+      (reinterpret_cast<uintptr_t>(dst_lens) & 3u))
+    return MD_ERR_INVALID_ARG;
+  const size_t nb = static_cast<size_t>(dst->num_seqs) * 4;
+  // every thread reads idx_len[b] and src_lens[b] while one writes dst_lens[b]
+  if (dst_lens && (md::overlaps(dst_lens, idx_len, nb) || md::overlaps(dst_lens, src_lens, nb)))
+    return MD_ERR_INVALID_ARG;
+  const int es = dst->dtype == MD_BF16 ? 2 : 4;
+  md::GatherParams p{};
+  p.dst = md::cache_view(dst);
+  p.src = md::cache_view(src);
+  p.idx = idx;
+  p.idx_stride = idx_stride;
+  p.idx_len = idx_len;
+  p.src_lens = src_lens;
+  p.dst_lens = dst_lens;
+  p.B = dst->num_seqs;
+  p.Hkv = dst->num_kv_heads;
+  p.row_vecs = dst->head_dim * es / 16;
+  p.esize = es;
+  const double items = 2.0 * p.B * idx_stride * p.Hkv * p.row_vecs;
+  if (items > 9.0e18) return MD_ERR_INVALID_ARG;
+  p.n_items = 2 * static_cast<int64_t>(p.B) * idx_stride * p.Hkv * p.row_vecs;
+  const hipError_t e = md::launch_kv_gather(p, src->page_size != 0, dst->page_size != 0,
+                                            static_cast<hipStream_t>(stream));
   return e == hipSuccess ? MD_OK : md::hip_fail(e);
 }
 

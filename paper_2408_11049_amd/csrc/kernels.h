@@ -107,6 +107,31 @@ struct AppendParams {
   int64_t n_items;             // 2 * B * n_new * Hkv * row_vecs
 };
 
+// One cache as the gather kernel addresses it (element strides).
+struct CacheView {
+  unsigned char* k;
+  unsigned char* v;
+  int64_t s_blk, s_tok, s_head;
+  const int32_t* page_table;  // [B, max_pages] (paged)
+  int32_t page_shift;
+  int32_t max_pages;
+  int64_t num_pages;
+  int64_t capacity;           // tokens per sequence (contiguous)
+};
+
+struct GatherParams {
+  CacheView dst, src;
+  const int32_t* idx;       // [B, Hkv, idx_stride]
+  int32_t idx_stride;
+  const int32_t* idx_len;   // [B]
+  const int32_t* src_lens;  // [B]
+  int32_t* dst_lens;        // [B] or nullptr
+  int32_t B, Hkv;
+  int32_t row_vecs;         // 16-byte vectors per row (d * element size / 16)
+  int32_t esize;
+  int64_t n_items;          // 2 (K, V) * B * idx_stride * Hkv * row_vecs
+};
+
 struct AcceptParams {
   const void* logits;          // [rows][vocab]
   int32_t vocab, n_chunks, chunk_len;  // chunk_len: elements, a multiple of 8
@@ -119,6 +144,7 @@ struct AcceptParams {
   int32_t* target;             // [B, L] or nullptr
 };
 
+hipError_t launch_kv_gather(const GatherParams& p, bool src_paged, bool dst_paged, hipStream_t s);
 hipError_t launch_kv_append(const AppendParams& p, bool paged, hipStream_t s);
 hipError_t launch_greedy_accept(const AcceptParams& p, bool bf16, bool vec, hipStream_t s);
 hipError_t launch_kv_commit(int B, int q_len, int32_t* lens, const int32_t* accepted, int Hkv,

@@ -12,7 +12,9 @@
 //   kv_commit       C' = C + a + 1, recording the kept positions in the
 //                   rolling ring of a listed draft cache;
 //   streaming_list  the sink-plus-window lists a StreamingLLM-style draft
-//                   cache starts from at prefill.
+//                   cache starts from at prefill;
+//   kv_gather       a static selection's listed rows copied, once, into a
+//                   draft cache of its own.
 //
 // All of them are bound by HBM or by launch latency; none is a contraction.
 #include <hip/hip_runtime.h>
@@ -71,6 +73,82 @@ hipError_t launch_kv_append(const AppendParams& p, bool paged, hipStream_t s) {
     hipLaunchKernelGGL(kv_append_kernel<true>, dim3(blocks), dim3(256), 0, s, p);
   else
     hipLaunchKernelGGL(kv_append_kernel<false>, dim3(blocks), dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- gather --
+
+// Where logical position j of sequence b lives in cache c: (block, token),
+// or false when it lies outside the cache (past the capacity or the table,
+// or on a page outside the pool).
+template <bool PAGED>
+__device__ __forceinline__ bool cache_row(const CacheView& c, int b, int64_t j, int64_t& blk,
+                                          int64_t& tok) {
+  if (j < 0) return false;
+  if (PAGED) {
+    const int64_t pg = j >> c.page_shift;
+    if (pg >= c.max_pages) return false;
+    blk = c.page_table[static_cast<int64_t>(b) * c.max_pages + pg];
+    if (blk < 0 || blk >= c.num_pages) return false;
+    tok = j & ((int64_t{1} << c.page_shift) - 1);
+  } else {
+    if (j >= c.capacity) return false;
+    blk = b;
+    tok = j;
+  }
+  return true;
+}
+
+// One 16-byte vector per item, items ordered (vector, kv head, list slot,
+// sequence, K/V): the kv heads of one destination row are written side by
+// side (one whole token row), each read from its own listed source row.
+template <bool SRC_PAGED, bool DST_PAGED>
+__global__ void __launch_bounds__(256) kv_gather_kernel(const GatherParams p) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * 256;
+  for (int64_t item = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; item < p.n_items;
+       item += stride) {
+    int64_t r = item;
+    const int c = static_cast<int>(r % p.row_vecs);
+    r /= p.row_vecs;
+    const int hk = static_cast<int>(r % p.Hkv);
+    r /= p.Hkv;
+    const int j = static_cast<int>(r % p.idx_stride);
+    r /= p.idx_stride;
+    const int b = static_cast<int>(r % p.B);
+    const bool is_v = r >= p.B;
+
+    const int n = min(max(p.idx_len[b], 0), p.idx_stride);
+    if (!is_v && j == 0 && hk == 0 && c == 0 && p.dst_lens) p.dst_lens[b] = n;
+    if (j >= n) continue;
+    int64_t dblk, dtok;
+    if (!cache_row<DST_PAGED>(p.dst, b, j, dblk, dtok)) continue;
+    const int32_t pos = p.idx[(static_cast<int64_t>(b) * p.Hkv + hk) * p.idx_stride + j];
+    u32x4 val = u32x4{0u, 0u, 0u, 0u};
+    int64_t sblk, stok;
+    if (pos >= 0 && pos < p.src_lens[b] && cache_row<SRC_PAGED>(p.src, b, pos, sblk, stok)) {
+      const int64_t so =
+          (sblk * p.src.s_blk + stok * p.src.s_tok + hk * p.src.s_head) * p.esize + c * 16;
+      val = __builtin_nontemporal_load(
+          reinterpret_cast<const u32x4*>((is_v ? p.src.v : p.src.k) + so));
+    }
+    const int64_t dof =
+        (dblk * p.dst.s_blk + dtok * p.dst.s_tok + hk * p.dst.s_head) * p.esize + c * 16;
+    *reinterpret_cast<u32x4*>((is_v ? p.dst.v : p.dst.k) + dof) = val;
+  }
+}
+
+hipError_t launch_kv_gather(const GatherParams& p, bool src_paged, bool dst_paged, hipStream_t s) {
+  const int64_t want = (p.n_items + 255) / 256;
+  const uint32_t blocks = static_cast<uint32_t>(want < (1 << 20) ? want : (1 << 20));
+  const dim3 g(blocks), blk(256);
+  if (src_paged && dst_paged)
+    hipLaunchKernelGGL((kv_gather_kernel<true, true>), g, blk, 0, s, p);
+  else if (src_paged)
+    hipLaunchKernelGGL((kv_gather_kernel<true, false>), g, blk, 0, s, p);
+  else if (dst_paged)
+    hipLaunchKernelGGL((kv_gather_kernel<false, true>), g, blk, 0, s, p);
+  else
+    hipLaunchKernelGGL((kv_gather_kernel<false, false>), g, blk, 0, s, p);
   return hipGetLastError();
 }
 

@@ -307,6 +307,47 @@ def test_kv_append_pointer_rules(lib):
     assert ap(ctypes.byref(good_cache(num_seqs=0)), 5, None, None, None, None, None) == md.MD_OK
 
 
+GATHER_BAD = [
+    ("heads differ", {}, {"num_kv_heads": 4}),
+    ("head_dim differs", {}, {"head_dim": 64, "kv_stride_head": 64}),
+    ("dtype differs", {}, {"dtype": md.MD_F32}),
+    ("sequences differ", {}, {"num_seqs": 3}),
+    ("bad destination", {"capacity": 0}, {}),
+    ("bad source", {}, {"kv_stride_tok": 100}),
+    ("misaligned destination", {"k": FAKE + 4}, {}),
+    ("null source", {}, {"v": None}),
+]
+
+
+@pytest.mark.parametrize("name,dst_over,src_over", GATHER_BAD, ids=[b[0] for b in GATHER_BAD])
+def test_kv_gather_rejects(lib, name, dst_over, src_over):
+    d, s = good_cache(**dst_over), good_cache(**src_over)
+    st = lib.md_kv_gather(ctypes.byref(d), ctypes.byref(s), FAKE, 16, FAKE + 64, FAKE + 128,
+                          FAKE + 192, None)
+    assert st == md.MD_ERR_INVALID_ARG
+
+
+def test_kv_gather_pointer_rules(lib):
+    d, s = good_cache(), good_cache()
+    g = lib.md_kv_gather
+    assert g(None, ctypes.byref(s), FAKE, 16, FAKE, FAKE, None, None) == md.MD_ERR_INVALID_ARG
+    assert g(ctypes.byref(d), None, FAKE, 16, FAKE, FAKE, None, None) == md.MD_ERR_INVALID_ARG
+    assert g(ctypes.byref(d), ctypes.byref(s), FAKE, 0, FAKE, FAKE, None, None) == md.MD_ERR_INVALID_ARG
+    assert g(ctypes.byref(d), ctypes.byref(s), None, 16, FAKE, FAKE, None, None) == md.MD_ERR_INVALID_ARG
+    assert g(ctypes.byref(d), ctypes.byref(s), FAKE, 16, None, FAKE, None, None) == md.MD_ERR_INVALID_ARG
+    assert g(ctypes.byref(d), ctypes.byref(s), FAKE, 16, FAKE, None, None, None) == md.MD_ERR_INVALID_ARG
+    assert g(ctypes.byref(d), ctypes.byref(s), FAKE + 2, 16, FAKE, FAKE, None, None) == md.MD_ERR_INVALID_ARG
+    # dst_lens overlapping idx_len or src_lens (two sequences: 8 bytes each)
+    assert g(ctypes.byref(d), ctypes.byref(s), FAKE, 16, FAKE + 64, FAKE + 128, FAKE + 68,
+             None) == md.MD_ERR_INVALID_ARG
+    assert g(ctypes.byref(d), ctypes.byref(s), FAKE, 16, FAKE + 64, FAKE + 128, FAKE + 124,
+             None) == md.MD_ERR_INVALID_ARG
+    # nothing to gather: no launch, no pointer read
+    e = good_cache(num_seqs=0)
+    assert g(ctypes.byref(e), ctypes.byref(good_cache(num_seqs=0)), None, 16, None, None, None,
+             None) == md.MD_OK
+
+
 def test_greedy_accept_args(lib):
     ga = lib.md_greedy_accept
     ws = lib.md_greedy_accept_workspace_bytes(64, 4, 128256)
