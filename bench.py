@@ -399,6 +399,78 @@ def main():
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
     t_sd_graph = sd_timed(graph.replay)
+
+    # The same selection gathered once into a draft cache of its own
+    # (md_kv_gather): a draft step is then verify attention over the 2049
+    # gathered rows plus its own speculated rows, appended to that cache.
+    cap_c = budget + L + w.gamma
+    ck = torch.empty((w.B, cap_c, w.Hkv, w.d), dtype=c["k"].dtype, device=dev)
+    cv = torch.empty_like(ck)
+    glen = torch.empty_like(pos0)
+
+    def gather():
+        md.md_kv_gather(ck, cv, c["k"], c["v"], idx_t, n_t, pos0, dst_lens=glen,
+                        src_page_table=c["page_table"])
+
+    t_gather = timed(gather, n=5)
+    gather()
+    torch.cuda.synchronize()
+    common_c = dict(max_kv_len=cap_c)
+    glen1, glenL = (glen + 1).contiguous(), (glen + L).contiguous()
+
+    def ws_c(q, lens_c):
+        n = md.md_workspace_bytes(q, ck, cv, lens_c, mode=md.MD_MODE_VERIFY, **common_c)
+        return torch.empty((max(n, 256),), dtype=torch.uint8, device=dev) if n else None
+
+    ws_g1, ws_gL = ws_c(q1, glen1), ws_c(c["q"], glenL)
+    t_draft_g1 = timed(lambda: md.md_verify_attn(q1, ck, cv, glen1, out=out_sd1, return_lse=False,
+                                                 workspace=ws_g1, **common_c))
+    t_draft_gL = timed(lambda: md.md_verify_attn(c["q"], ck, cv, glenL, out=out_d,
+                                                 return_lse=False, workspace=ws_gL, **common_c))
+    g_lens = glen.clone()
+    g_pos_i = [(glen + i).contiguous() for i in range(w.gamma)]
+    g_kvl_i = [torch.empty_like(pos0) for _ in range(w.gamma)]
+    g_out = torch.empty_like(pos0)
+
+    def sd_step_gathered():
+        for i in range(w.gamma):
+            md.md_kv_append(ck, cv, k1[i], v1[i], g_pos_i[i], lens_out=g_kvl_i[i])
+            md.md_verify_attn(q1, ck, cv, g_kvl_i[i], out=out_sd1, return_lse=False,
+                              workspace=ws_g1, **common_c)
+        md.md_kv_append(c["k"], c["v"], k_new, v_new, sd_lens, page_table=c["page_table"],
+                        lens_out=sd_out)
+        md.md_kv_append(ck, cv, k_new, v_new, g_lens, lens_out=g_out)
+        md.md_verify_attn(c["q"], c["k"], c["v"], sd_out, out=out_v, lse=lse_v, workspace=ws_vsd,
+                          **common)
+        md.md_greedy_accept(logits, draft_tok, accepted=acc, tokens=toks, want_target=False,
+                            workspace=ws_acc)
+        md.md_kv_commit(sd_lens, acc, L)
+        md.md_kv_commit(g_lens, acc, L)
+
+    def sd_timed_g(run, n=8):
+        ts = []
+        for _ in range(n):
+            sd_lens.copy_(pos0)
+            g_lens.copy_(glen)
+            do_flush()
+            a_ev, b_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a_ev.record(stream); run(); b_ev.record(stream)
+            torch.cuda.synchronize()
+            ts.append(a_ev.elapsed_time(b_ev) * 1e3)
+        return float(np.median(ts))
+
+    sd_step_gathered()
+    torch.cuda.synchronize()
+    t_sdg_eager = sd_timed_g(sd_step_gathered)
+    graph_g = torch.cuda.CUDAGraph()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(graph_g, stream=side):
+            sd_step_gathered()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    t_sdg_graph = sd_timed_g(graph_g.replay)
+    bytes_gather = 2 * bytes_idx - 2 * w.B * L * w.Hkv * 2 * w.d * w.esize  # rows read + written
     bytes_logits = logits.numel() * logits.element_size()
     # A plain 1 GiB copy of known size: its FETCH_SIZE / WRITE_SIZE readings
     # calibrate the HBM byte counters of a rocprofv3 --pmc run of this script.
@@ -466,6 +538,15 @@ def main():
             "t_sd_step_eager_us (gamma x (append 1 + listed draft 1) + append + verify + accept + commit)":
                 round(t_sd_eager, 2),
             "t_sd_step_graph_us (the same step, one HIP graph replay)": round(t_sd_graph, 2),
+            "t_kv_gather_us (the 2049 listed rows into a draft cache, once per prompt)":
+                round(t_gather, 2),
+            "kv_gather_bytes (read + write)": bytes_gather,
+            "t_draft_gathered_qlen1_us (verify over the gathered 2049 rows + 1)": round(t_draft_g1, 2),
+            "t_draft_gathered_us (q_len gamma+1)": round(t_draft_gL, 2),
+            "draft_gathered_gbs": round(bytes_idx / (t_draft_gL * 1e-6) / 1e9, 1),
+            "t_sd_step_gathered_eager_us (the step with drafts over the gathered cache)":
+                round(t_sdg_eager, 2),
+            "t_sd_step_gathered_graph_us": round(t_sdg_graph, 2),
             "verify_kv_bytes": bytes_v, "draft_kv_bytes": bytes_d,
             "verify_gbs": round(verify_gbs, 1),
             "draft_gbs": round(bytes_d / (np.mean(td) * 1e-6) / 1e9, 1),

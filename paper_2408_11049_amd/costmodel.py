@@ -9,9 +9,10 @@ cold cache:
   T_T        verify at q_len = 1 (plain decoding: one token per sequence),
   T_V(g)     verify at q_len = g + 1 (g speculated tokens plus the last one),
   T_D        one-token draft over a StreamingLLM cache of 16 sinks + 496
-             window (budget 512, Table 1), and over a listed SnapKV-style cache
-             of 2049 positions (Sec. 5.2); static selections cost nothing per
-             step (T_select = 0 in Eq. 3).
+             window (budget 512, Table 1), over a listed SnapKV-style cache
+             of 2049 positions (Sec. 5.2), and over the same 2049 rows
+             gathered once into a draft cache of their own (md_kv_gather);
+             static selections cost nothing per step (T_select = 0 in Eq. 3).
 
 Those times go through the library's cost model (md_sd_best_gamma, Eq. 4 over
 gamma) for a set of acceptance rates, giving the best speculation length, the
@@ -62,7 +63,7 @@ def _timer(dev, flush, lib, sh):
 
 def measure(B, S, max_gamma=8, reps=5, device="cuda:0", seed=7):
     """Times in microseconds: t_target, t_verify[g - 1] for g = 1 .. max_gamma,
-    t_draft_streaming, t_draft_listed."""
+    t_draft_streaming, t_draft_listed, t_draft_gathered."""
     import torch
 
     import paper_2408_11049_amd as md
@@ -100,10 +101,17 @@ def measure(B, S, max_gamma=8, reps=5, device="cuda:0", seed=7):
     idx, n_t = torch.from_numpy(idx_np).to(dev), torch.from_numpy(n_np).to(dev)
     t_listed = timed(lambda: md.md_draft_attn_indexed(qs[1], k, v, lens, idx, n_t, out=outs[1],
                                                       return_lse=False, max_kv_len=S), reps)
-    del c, k, v, flush
+    ck = torch.empty((B, LISTED + 1) + tuple(k.shape[2:]), dtype=k.dtype, device=dev)
+    cv = torch.empty_like(ck)
+    glen = md.md_kv_gather(ck, cv, k, v, idx, n_t, (lens - 1).contiguous())
+    # the drafted token's row, as the draft step appends it
+    glen1 = md.md_kv_append(ck, cv, k[:, S - 1:S].contiguous(), v[:, S - 1:S].contiguous(), glen)
+    t_gathered = timed(lambda: md.md_verify_attn(qs[1], ck, cv, glen1, out=outs[1],
+                                                 return_lse=False, max_kv_len=LISTED + 1), reps)
+    del c, k, v, ck, cv, flush
     torch.cuda.empty_cache()
     return dict(B=B, S=S, t_target=t_target, t_verify=t_verify, t_draft_streaming=t_stream,
-                t_draft_listed=t_listed)
+                t_draft_listed=t_listed, t_draft_gathered=t_gathered)
 
 
 def analyse(m, alphas=ALPHAS):
@@ -112,7 +120,8 @@ def analyse(m, alphas=ALPHAS):
     import paper_2408_11049_amd as md
 
     out = {"tv1_over_tt": m["t_verify"][0] / m["t_target"]}
-    for name, td in (("streaming", m["t_draft_streaming"]), ("listed", m["t_draft_listed"])):
+    for name, td in (("streaming", m["t_draft_streaming"]), ("listed", m["t_draft_listed"]),
+                     ("gathered", m["t_draft_gathered"])):
         for a in alphas:
             g, r = md.md_sd_best_gamma(a, m["t_target"], td, m["t_verify"])
             out[f"{name}@{a}"] = {"gamma": g, "ratio": r, "speedup": 1.0 / r}
@@ -139,20 +148,21 @@ def main(argv=None):
         m["model"] = analyse(m)
         rows.append(m)
         print(json.dumps(m), flush=True)
-    print("\n| B | S | T_T us | T_V(1)/T_T | T_V(4)/T_T | T_D 512 us | T_D 2049 us | "
-          + " | ".join(f"listed a={a}: g, x" for a in ALPHAS) + " |")
-    print("|" + "---|" * (7 + len(ALPHAS)))
+    print("\n| B | S | T_T us | T_V(1)/T_T | T_V(4)/T_T | T_D 512 us | T_D 2049 listed us | "
+          "T_D 2049 gathered us | " + " | ".join(f"gathered a={a}: g, x" for a in ALPHAS) + " |")
+    print("|" + "---|" * (8 + len(ALPHAS)))
     for m in rows:
         cells = [str(m["B"]), str(m["S"]), f"{m['t_target']:.1f}",
                  f"{m['t_verify'][0] / m['t_target']:.3f}",
                  f"{m['t_verify'][3] / m['t_target']:.3f}" if len(m["t_verify"]) >= 4 else "-",
-                 f"{m['t_draft_streaming']:.1f}", f"{m['t_draft_listed']:.1f}"]
+                 f"{m['t_draft_streaming']:.1f}", f"{m['t_draft_listed']:.1f}",
+                 f"{m['t_draft_gathered']:.1f}"]
         for a in ALPHAS:
-            e = m["model"][f"listed@{a}"]
+            e = m["model"][f"gathered@{a}"]
             cells.append(f"{e['gamma']}, {e['speedup']:.2f}")
         print("| " + " | ".join(cells) + " |")
     print("\nS_inflection (smallest measured S with attention-only speedup > 1):")
-    for name in ("streaming", "listed"):
+    for name in ("streaming", "listed", "gathered"):
         for a in ALPHAS:
             parts = []
             for B in sorted({m["B"] for m in rows}):

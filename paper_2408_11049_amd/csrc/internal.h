@@ -26,6 +26,7 @@ constexpr int kWaves = 4;
 constexpr int kTile = 32;            // tokens per wave iteration
 constexpr int kMinChunkTokens = 1024;  // every wave gets >= 8 tiles of a chunk
 constexpr int kMaxRows = 64;         // G*L bound: at most four 16-row tiles
+constexpr int kPairMinChunkTokens = 4096;  // head pairs on split ranges: chunks at least this long
 // Longest-first dispatch (single-chunk verify plans): every workgroup ranks
 // the sequences by length, so it is kept to small batches of long caches.
 constexpr int kLptMaxSeqs = 256;

@@ -81,19 +81,42 @@ int validate_attn(const md_attn_args* a, int mode, int n_sink, int window) {
   return MD_OK;
 }
 
+// The range split for n_groups workgroups' worth of units: one chunk each
+// when they alone cover every compute unit, else each range is cut just until
+// they do, never below kMinChunkTokens tokens per chunk.
+static void split_units(int64_t U, int64_t n_groups, int64_t slots, int64_t* n_chunks_out,
+                        int64_t* chunk_len_out) {
+  int64_t n_chunks = 1;
+  if (n_groups > 0 && n_groups < slots) {
+    n_chunks = ceil_div(slots, n_groups);
+    const int64_t cap = ceil_div(U, kMinChunkTokens);
+    if (n_chunks > cap) n_chunks = cap;
+    if (n_chunks < 1) n_chunks = 1;
+  }
+  int64_t chunk_len = ceil_div(ceil_div(U, n_chunks), kTile) * kTile;
+  if (chunk_len < kTile) chunk_len = kTile;
+  n_chunks = ceil_div(U, chunk_len);
+  if (n_chunks < 1) n_chunks = 1;
+  *n_chunks_out = n_chunks;
+  *chunk_len_out = chunk_len;
+}
+
 // Kv heads per workgroup.  In the token-major cache the kv heads of a token
 // are adjacent, so a workgroup that serves two heads of a sequence (two waves
 // each) reads 2 x 256 B runs of every token row (bf16, d = 128) side by side
 // instead of one: on MI355X a load-only model of the verify stream read the
 // B = 64, S = 32768 cache at 7.03 TB/s this way against 6.62 TB/s with one
-// head per workgroup, and the verify kernel gained 5-6% on the large-batch
-// workloads.  Pairs halve the number of workgroups, though: a streaming
-// draft's short range then needs twice the chunks and their merge, which
-// costs more than the pairing gains unless the pairs alone fill the device.
-// A listed draft reads a different list per head -- no adjacent rows -- and
-// keeps one head per workgroup.  MD_HEADS_PER_WG (1 or 2) overrides, for
-// measurement.
-static int heads_per_workgroup(const md_attn_args* a, int mode, int64_t slots) {
+// head per workgroup.  Pairs halve the workgroups, though, so a range that
+// must be split to fill the device is cut into twice as many chunks, each
+// paying a pipeline fill and its share of the merge.  Measured over verify
+// and draft calls of B = 1 .. 64 and S = 2048 .. 131072 (Llama-3.1-8B heads):
+// pairs gain 5-13% where they alone fill the device and 2-3% where their
+// chunks stay at 4096 tokens or more, and lose up to a third on short split
+// ranges (one-token verify at B = 1, S = 4096: 35 us against 26).  So pairs
+// are taken in those two cases only.  A listed draft reads a different list
+// per head -- no adjacent rows -- and keeps one head per workgroup.
+// MD_HEADS_PER_WG (1 or 2) overrides, for measurement.
+static int heads_per_workgroup(const md_attn_args* a, int mode, int64_t U, int64_t slots) {
   static const int forced = [] {
     const char* s = getenv("MD_HEADS_PER_WG");
     const int v = s ? atoi(s) : 0;
@@ -101,10 +124,12 @@ static int heads_per_workgroup(const md_attn_args* a, int mode, int64_t slots) {
   }();
   if (a->num_kv_heads % 2) return 1;
   if (forced) return forced;
+  if (mode == MD_MODE_DRAFT_INDEXED) return 1;
   const int64_t pairs = static_cast<int64_t>(a->num_seqs) * a->num_kv_heads / 2;
-  if (mode == MD_MODE_VERIFY) return 2;
-  if (mode == MD_MODE_DRAFT) return pairs >= slots ? 2 : 1;
-  return 1;
+  if (pairs >= slots) return 2;
+  int64_t n_chunks, chunk_len;
+  split_units(U, pairs, slots, &n_chunks, &chunk_len);
+  return chunk_len >= kPairMinChunkTokens ? 2 : 1;
 }
 
 Plan make_plan(const md_attn_args* a, int mode, int n_sink, int window, int num_cus) {
@@ -127,19 +152,10 @@ Plan make_plan(const md_attn_args* a, int mode, int n_sink, int window, int num_
   // compute unit -- was 5-15% slower on long caches and slower still on
   // short draft ranges.)
   const int64_t slots = num_cus > 0 ? num_cus : 256;
-  p.hp = heads_per_workgroup(a, mode, slots);
+  p.hp = heads_per_workgroup(a, mode, U, slots);
   p.n_groups = p.n_units / p.hp;
-  int64_t n_chunks = 1;
-  if (p.n_groups > 0 && p.n_groups < slots) {
-    n_chunks = ceil_div(slots, p.n_groups);
-    int64_t cap = ceil_div(U, kMinChunkTokens);
-    if (n_chunks > cap) n_chunks = cap;
-    if (n_chunks < 1) n_chunks = 1;
-  }
-  int64_t chunk_len = ceil_div(ceil_div(U, n_chunks), kTile) * kTile;
-  if (chunk_len < kTile) chunk_len = kTile;
-  n_chunks = ceil_div(U, chunk_len);
-  if (n_chunks < 1) n_chunks = 1;
+  int64_t n_chunks, chunk_len;
+  split_units(U, p.n_groups, slots, &n_chunks, &chunk_len);
   p.n_chunks = static_cast<int32_t>(n_chunks);
   p.chunk_len = static_cast<int32_t>(chunk_len);
   if (p.n_chunks > 1) {

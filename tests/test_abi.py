@@ -219,6 +219,31 @@ def test_workspace_zero_when_units_fill_the_device(lib):
     assert lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1) == 0
 
 
+def _split_bytes(n_chunks, n_rows, d):
+    up = lambda x: (x + 255) // 256 * 256
+    return up(n_chunks * n_rows * d * 4) + up(n_chunks * n_rows * 4)
+
+
+@pytest.mark.parametrize("B,S,hp", [
+    (1, 131072, 1),   # pairs would cut 128k tokens into 64 chunks of 2048: one head per group
+    (4, 65536, 2),    # 16 pairs x 16 chunks of 4096 tokens: pairs
+    (16, 4096, 1),    # 64 pairs x 4 chunks of 1024: one head
+    (16, 16384, 2),   # 64 pairs x 4 chunks of 4096: pairs
+])
+def test_plan_pairs_heads_only_where_they_pay(lib, B, S, hp):
+    """The verify split as md_workspace_bytes reveals it (256 compute units on
+    this host): the workgroups are B * 8 / hp, and the range is cut into
+    ceil(256 / workgroups) chunks, at least 1024 tokens each."""
+    a = good_args(num_seqs=B, num_kv_heads=8, num_q_heads=32, q_len=5, max_kv_len=S,
+                  kv_stride_tok=8 * 128, kv_stride_blk=S * 8 * 128)
+    groups = B * 8 // hp
+    n_chunks = min(-(-256 // groups), -(-S // 1024))
+    chunk = -(-(-(-S // n_chunks)) // 32) * 32
+    n_chunks = -(-S // chunk)
+    got = lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1)
+    assert got == _split_bytes(n_chunks, B * 5 * 32, 128), (got, n_chunks)
+
+
 def test_workspace_draft_smaller_than_verify(lib):
     a = good_args(num_seqs=2, num_kv_heads=1, num_q_heads=8, q_len=4, max_kv_len=1 << 17,
                   kv_stride_tok=128, kv_stride_blk=(1 << 17) * 128)

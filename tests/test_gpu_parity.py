@@ -44,7 +44,7 @@ SMALL = [
     ("bf16_page1", 2, 3, 4, 2, 64, [37, 20], "bf16", 1, 2, 9),
     ("bf16_page64", 2, 3, 4, 2, 128, [300, 129], "bf16", 64, 2, 40),
     ("f32_rows40_split", 1, 5, 8, 1, 128, [2600], "f32", 0, 16, 100),
-    ("bf16_head_pairs_split_paged", 2, 5, 16, 4, 128, [4000, 2500], "bf16", 16, 16, 496),
+    ("bf16_hkv4_split_paged", 2, 5, 16, 4, 128, [4000, 2500], "bf16", 16, 16, 496),
 ]
 
 
