@@ -39,6 +39,7 @@ sys.path.insert(0, ROOT)
 WORKLOAD = "llama8b_b64_s32k_paged"
 HBM_PEAK_GBS = 8000.0
 PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "attn_verify_llama8b_b64_s32k_paged_counters.md")
+PROFILE_MFMA = os.path.join(ROOT, "profiles", "attn_mfma_llama8b_b64_s32k_paged.md")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2408_11049_amd", "csrc", "attn.hip")
 
 
@@ -78,6 +79,24 @@ def read_counters():
     if sha != m_sha.group(1):
         return None
     return float(m_f.group(1)) + float(m_w.group(1))
+
+
+def read_mfma():
+    """The verify kernel's MFMA utilisation from the committed rocprofv3 counter
+    summary (MfmaUtil, bf16 MFMA TFLOP/s), or None if absent or taken on a
+    different kernel source."""
+    if not os.path.exists(PROFILE_MFMA):
+        return None
+    text = open(PROFILE_MFMA).read()
+    m_sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
+    m_u = re.search(r"verify_mfma_util_pct:\s*([0-9.eE+]+)", text)
+    m_t = re.search(r"verify_mfma_tflops:\s*([0-9.eE+]+)", text)
+    if not (m_sha and m_u and m_t):
+        return None
+    if hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest() != m_sha.group(1):
+        return None
+    return {"util_pct": float(m_u.group(1)), "bf16_tflops": float(m_t.group(1)),
+            "peak_tflops": 2500.0, "source": "profiles/attn_mfma_llama8b_b64_s32k_paged.md"}
 
 
 def cpu_baseline(c, w, budget_s=15.0, batch=32):
@@ -490,7 +509,8 @@ def main():
                 "unit": "GB/s", "frac": round(verify_gbs / HBM_PEAK_GBS, 4),
                 "traffic": traffic,
                 "kernel": "md::attn_partial_kernel<128, true, 2, true, false, 1, 1> (md_verify_attn)",
-                "algorithmic_bytes_per_launch": bytes_v}
+                "algorithmic_bytes_per_launch": bytes_v,
+                "mfma": read_mfma()}
 
     cpu = None
     oracle_extras = None
