@@ -18,7 +18,8 @@
  *     NULL is the null stream).  Buffers must stay alive and unmodified until
  *     the stream reaches the call.  Nothing synchronises with the host.
  *   - Calls are thread-safe and re-entrant.  The only global state is a
- *     per-device cache of the compute-unit count.
+ *     per-device cache of the compute-unit count and the MD_* tuning
+ *     overrides, read once from the environment.
  *   - Errors are return codes (md_status).  Argument errors are detected on
  *     the host before any HIP call, so a failed call has launched nothing.
  *   - Device-side contract violations are not detected: kv_lens[b] < q_len

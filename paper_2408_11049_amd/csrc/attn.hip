@@ -13,16 +13,19 @@
 // the kWaves / hp waves of a unit take interleaved 32-token tiles of the
 // chunk and run independent online softmaxes, merged through LDS at the end.
 // Per tile and wave:
-//   K  16 B loads straight into the MFMA A-operand layout (8 bf16 channels of
-//      one token per lane), Q held as the B operand for the whole chunk:
-//      S^T[token, row] = K Q^T on v_mfma_f32_16x16x32_bf16.
+//   load     K and V as whole token rows (256 B for bf16, d = 128: 16 lanes
+//            per row, nontemporal 16 B loads, one address per token), staged
+//            through the wave's private LDS tiles.
+//   scores   K read back as the MFMA A operand (a token per lane), Q held as
+//            the B operand for the whole chunk: S^T[token, row] = K Q^T on
+//            v_mfma_f32_16x16x32_bf16.
 //   softmax  each lane owns one query row and 8 of the tile's tokens; the
-//      row max needs two cross-lane steps, the row sum is reduced only once
-//      at the end.
-//   V  16 B coalesced loads (whole 256 B token rows), staged through a
-//      wave-private LDS tile and read back transposed as the A operand of
-//      O^T[channel, row] += V^T P^T, whose output layout puts each lane's
-//      row in the same place as its softmax state (no shuffles to rescale).
+//            row max needs two cross-lane steps, the row sum is reduced only
+//            once at the end.
+//   values   V read back transposed (ds_read_b64_tr_b16) as the A operand of
+//            O^T[channel, row] += V^T P^T, whose output layout puts each
+//            lane's row in the same place as its softmax state (no shuffles
+//            to rescale).
 // The next tile's K/V (and page ids, two tiles ahead) are in flight while
 // the current one is computed.
 #include <hip/hip_runtime.h>
@@ -184,7 +187,7 @@ attn_partial_kernel(const AttnParams p) {
   const int hk = hk0 + wave_u % hp;
   const int L = p.L;
 
-  // ---- the unit's visible range (a1/a5 of the method's hot path)
+  // ---- the unit's visible range: the causal prefix, sinks then windows, or the list
   UnitGeom u;
   u.S = __builtin_amdgcn_readfirstlane(min(p.kv_lens[b], p.max_kv_len));
   if (u.S < 0) u.S = 0;
