@@ -22,11 +22,19 @@
  *     overrides, read once from the environment.
  *   - Errors are return codes (md_status).  Argument errors are detected on
  *     the host before any HIP call, so a failed call has launched nothing.
- *   - Device-side contract violations are not detected: kv_lens[b] < q_len
- *     yields rows with an empty key set (O = 0, lse = -inf); kv_lens[b] is
- *     clamped to max_kv_len; page ids outside [0, num_pages) are never
- *     dereferenced (those tokens read as zero).  Results are then meaningless
- *     but memory stays in bounds.
+ *   - Device-side contract violations leave memory in bounds but results
+ *     meaningless: kv_lens[b] < q_len yields rows with an empty key set
+ *     (O = 0, lse = -inf); kv_lens[b] is clamped to max_kv_len; page ids
+ *     outside [0, num_pages) are never dereferenced (those tokens read as
+ *     zero).  They are reported only to a caller that passes an error word
+ *     (md_attn_args.err_word, for debugging): each attention call then ORs
+ *     into it MD_ERRW_SHORT_LEN if some kv_lens[b] < q_len (negative
+ *     included), MD_ERRW_LONG_LEN if some kv_lens[b] > max_kv_len, and
+ *     MD_ERRW_BAD_PAGE if a position the call reads (below the clamped
+ *     length; for a listed draft, a usable list entry or a speculated
+ *     position) has a page id outside [0, num_pages).  The library never
+ *     clears the word.  The checks read the lengths and the page ids once
+ *     more, before the K/V stream; without the word they cost nothing.
  */
 #ifndef MAGICDEC_H_
 #define MAGICDEC_H_
@@ -49,6 +57,13 @@ typedef enum {
 typedef enum { MD_F32 = 0, MD_BF16 = 1 } md_dtype;
 
 typedef enum { MD_MODE_VERIFY = 0, MD_MODE_DRAFT = 1, MD_MODE_DRAFT_INDEXED = 2 } md_mode;
+
+/* Bits of md_attn_args.err_word (device-side contract checks). */
+typedef enum {
+  MD_ERRW_SHORT_LEN = 1, /* some kv_lens[b] < q_len */
+  MD_ERRW_LONG_LEN = 2,  /* some kv_lens[b] > max_kv_len */
+  MD_ERRW_BAD_PAGE = 4   /* a position read has a page id outside [0, num_pages) */
+} md_err_bits;
 
 /*
  * One attention call over a batch of B sequences for one layer.
@@ -104,6 +119,7 @@ typedef struct {
   float* lse;
   void* workspace;            /* device scratch, >= md_workspace_bytes(), 256-byte aligned */
   size_t workspace_bytes;
+  int32_t* err_word;          /* device int32 or NULL: contract checks (md_err_bits, above) */
 } md_attn_args;
 
 /*

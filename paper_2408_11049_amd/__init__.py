@@ -35,6 +35,7 @@ LIB_PATH = os.path.join(_HERE, "libmagicdec.so")
 MD_OK, MD_ERR_INVALID_ARG, MD_ERR_UNSUPPORTED, MD_ERR_WORKSPACE, MD_ERR_HIP = range(5)
 MD_F32, MD_BF16 = 0, 1
 MD_MODE_VERIFY, MD_MODE_DRAFT, MD_MODE_DRAFT_INDEXED = 0, 1, 2
+MD_ERRW_SHORT_LEN, MD_ERRW_LONG_LEN, MD_ERRW_BAD_PAGE = 1, 2, 4
 
 EXPORTED = ["md_verify_attn", "md_draft_attn", "md_draft_attn_indexed", "md_merge_lse",
             "md_workspace_bytes", "md_workspace_bytes_indexed", "md_snapkv_votes",
@@ -60,6 +61,7 @@ class MdAttnArgs(ctypes.Structure):
         ("kv_lens", ctypes.c_void_p), ("max_kv_len", ctypes.c_int32),
         ("o", ctypes.c_void_p), ("lse", ctypes.c_void_p),
         ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
+        ("err_word", ctypes.c_void_p),
     ]
 
 
@@ -217,7 +219,8 @@ def _dtype_code(t):
 
 
 def make_args(q, k, v, kv_lens, *, max_kv_len: Optional[int] = None, page_table=None,
-              sm_scale: float = 0.0, out=None, lse=None, workspace=None) -> MdAttnArgs:
+              sm_scale: float = 0.0, out=None, lse=None, workspace=None,
+              err_word=None) -> MdAttnArgs:
     """Fill md_attn_args from tensors (no data is read or moved)."""
     if q.dim() != 4 or k.dim() != 4 or v.dim() != 4:
         raise ValueError("q, k, v must be 4-D")
@@ -256,6 +259,11 @@ def make_args(q, k, v, kv_lens, *, max_kv_len: Optional[int] = None, page_table=
     a.lse = lse.data_ptr() if lse is not None else None
     if workspace is not None:
         a.workspace, a.workspace_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
+    if err_word is not None:
+        import torch
+        if err_word.dtype != torch.int32 or err_word.numel() < 1:
+            raise ValueError("err_word must be a device int32 tensor")
+        a.err_word = err_word.data_ptr()
     return a
 
 
@@ -268,7 +276,7 @@ def md_workspace_bytes(q, k, v, kv_lens, *, mode=MD_MODE_VERIFY, n_sink=0, windo
 @_stream_scoped
 def _attention(mode, q, k, v, kv_lens, n_sink, window, *, max_kv_len=None, page_table=None,
                sm_scale=0.0, out=None, lse=None, return_lse=True, workspace=None, stream=None,
-               idx=None, idx_len=None):
+               idx=None, idx_len=None, err_word=None):
     import torch
     lib = load_library()
     if kv_lens.dtype != torch.int32:
@@ -278,7 +286,7 @@ def _attention(mode, q, k, v, kv_lens, n_sink, window, *, max_kv_len=None, page_
     if lse is None and return_lse:
         lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
     a = make_args(q, k, v, kv_lens, max_kv_len=max_kv_len, page_table=page_table,
-                  sm_scale=sm_scale, out=out, lse=lse)
+                  sm_scale=sm_scale, out=out, lse=lse, err_word=err_word)
     if mode == MD_MODE_DRAFT_INDEXED:
         need = int(lib.md_workspace_bytes_indexed(ctypes.byref(a), idx.shape[2]))
     else:

@@ -137,6 +137,7 @@ int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void*
   p.num_seqs = a->num_seqs;
   p.lpt = longest_first(mode, pl.n_chunks, a->num_seqs, a->max_kv_len);
   p.hp = pl.hp;
+  p.err = a->err_word;
   int64_t n_blocks = pl.n_groups * pl.n_chunks;
   if (p.lpt && pl.hp == 2) {
     // One workgroup per unit; the kernel pairs heads (and idles the surplus

@@ -145,6 +145,50 @@ __device__ __forceinline__ int lpt_group(const P& p, int r, int* sl, int& hp) {
   return b * gps + r % gps;
 }
 
+// Contract checks for a caller that passes an error word (debug use), ahead
+// of the K/V stream; they change no result.  The lengths are checked once per
+// sequence (its first head group's first chunk).  Paged: the page id of every
+// position this workgroup reads -- one position per page and segment of a
+// shared range, checked by the sequence's first head group; every usable
+// list entry and speculated position of a listed draft, by the first wave of
+// each head.
+template <bool PAGED, bool IDX, typename P, typename U>
+__device__ void check_contract(const P& p, const U& u, int b, int chunk, bool first_group,
+                               bool first_wave, const int32_t* idxrow, int lane) {
+  uint32_t bits = 0;
+  if (chunk == 0 && first_group && threadIdx.x == 0) {
+    const int raw = p.kv_lens[b];
+    if (raw < p.L) bits |= MD_ERRW_SHORT_LEN;
+    if (raw > p.max_kv_len) bits |= MD_ERRW_LONG_LEN;
+  }
+  if constexpr (PAGED) {
+    const bool mine = IDX ? first_wave : first_group;
+    const int start = IDX ? lane : static_cast<int>(threadIdx.x);
+    const int step = IDX ? 64 : kWaves * 64;
+    const int pmask = (1 << p.page_shift) - 1;
+    if (mine) {
+      for (int v = u.v_begin + start; v < u.v_end; v += step) {
+        int t;
+        if constexpr (IDX) {
+          if (v < u.seg0) {
+            t = idxrow[v];
+            if (t < 0 || t >= u.S - p.L) continue;  // an unusable entry is skipped, not read
+          } else {
+            t = v - u.seg0 + u.seg1_start;
+          }
+        } else {
+          t = real_token(u, v);
+          if (v != u.v_begin && v != u.seg0 && (t & pmask) != 0) continue;  // page already covered
+        }
+        const int pg = t >> p.page_shift;
+        const int pid = pg < p.max_pages ? p.page_table[static_cast<int64_t>(b) * p.max_pages + pg] : -1;
+        if (pid < 0 || pid >= p.num_pages) bits |= MD_ERRW_BAD_PAGE;
+      }
+    }
+  }
+  if (bits) atomicOr(reinterpret_cast<unsigned int*>(p.err), bits);
+}
+
 template <int D, bool BF16, int NT, bool PAGED, bool IDX, int P, int OCC>
 __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(OCC)))
 attn_partial_kernel(const AttnParams p) {
@@ -556,6 +600,9 @@ attn_partial_kernel(const AttnParams p) {
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   };
+
+  if (p.err)
+    check_contract<PAGED, IDX>(p, u, b, chunk, hk0 == 0, wslot == 0, idxrow, lane);
 
   // Prologue: this wave's first P tiles in flight; the token locations of
   // the P tiles after them.

@@ -40,6 +40,7 @@ struct AttnParams {
   const int32_t* idx;         // indexed draft: [B, Hkv, idx_stride] prompt positions
   const int32_t* idx_len;     // indexed draft: [B] list lengths
   int32_t idx_stride;
+  int32_t* err;               // md_attn_args.err_word, or nullptr
 };
 
 // depth: K/V tiles each wave keeps in flight (1..3; bf16 instances).

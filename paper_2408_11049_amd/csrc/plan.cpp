@@ -63,7 +63,8 @@ int validate_attn(const md_attn_args* a, int mode, int n_sink, int window) {
     return MD_ERR_INVALID_ARG;
   if ((reinterpret_cast<uintptr_t>(a->kv_lens) & 3u) ||
       (a->lse && (reinterpret_cast<uintptr_t>(a->lse) & 3u)) ||
-      (paged && (reinterpret_cast<uintptr_t>(a->page_table) & 3u)))
+      (paged && (reinterpret_cast<uintptr_t>(a->page_table) & 3u)) ||
+      (reinterpret_cast<uintptr_t>(a->err_word) & 3u))
     return MD_ERR_INVALID_ARG;
   // Every token row must start on a 16-byte boundary for the 128-bit loads.
   const int64_t per16 = a->dtype == MD_BF16 ? 8 : 4;

@@ -100,6 +100,7 @@ BAD = [
     ("misaligned q", dict(q=FAKE + 8), md.MD_ERR_INVALID_ARG),
     ("misaligned k", dict(k=FAKE + 2), md.MD_ERR_INVALID_ARG),
     ("misaligned o", dict(o=FAKE + 4), md.MD_ERR_INVALID_ARG),
+    ("misaligned error word", dict(err_word=FAKE + 2), md.MD_ERR_INVALID_ARG),
     ("token stride not 16 B", dict(kv_stride_tok=2 * 128 + 4), md.MD_ERR_INVALID_ARG),
     ("head stride overlaps", dict(kv_stride_head=64), md.MD_ERR_INVALID_ARG),
     ("negative stride", dict(kv_stride_blk=-8), md.MD_ERR_INVALID_ARG),
