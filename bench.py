@@ -108,7 +108,7 @@ def cpu_baseline(c, w, budget_s=15.0, batch=32):
     import oracle
     from paper_2408_11049_amd import workloads as wl
 
-    threads = os.cpu_count() or 1
+    threads = oracle.default_threads()
 
     def run(units):
         qs, ks, vs, lens = [], [], [], []
@@ -139,7 +139,14 @@ def cpu_baseline(c, w, budget_s=15.0, batch=32):
         total_t += dt
         total_b += by
         done += min(batch, len(units) - done)
+    model = None
+    if os.path.exists("/proc/cpuinfo"):
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
     return {"value": total_b / total_t / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "cpu_model": model,
             "sample": f"{done} of {len(units)} (sequence, kv head) units of {WORKLOAD} in seeded "
                       f"random order, verify + draft, {total_t:.1f} s of fp64 oracle time"}
 

@@ -44,6 +44,16 @@ def open_library(path):
     return lib
 
 
+def default_threads():
+    """Worker threads for the oracle: the CPUs this process may run on, at most
+    16 (one GPU's share of the cores on a shared GPU host)."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
 def _load():
     global _lib
     if _lib is None:
@@ -99,7 +109,7 @@ def attention(mode, q, k, v, kv_lens, *, n_sink=0, window=1, scale=None, page_ta
         probs_len = int(probs_len if probs_len is not None else (kv_lens.max() if B else 0))
         probs = np.zeros((B, q_len, Hq, probs_len), dtype=np.float64)
     if nthreads is None:
-        nthreads = os.cpu_count() or 1
+        nthreads = default_threads()
     rc = lib.oracle_attention(mode, B, q_len, Hq, Hkv, d, dt, float(scale), _ptr(q), _ptr(k),
                               _ptr(v), s_blk, s_tok, s_head, page_size, _ptr(pt), max_pages,
                               _ptr(kv_lens), n_sink, window, _ptr(o), _ptr(lse), _ptr(probs),
@@ -144,7 +154,7 @@ def indexed(q, k, v, kv_lens, idx, idx_len, *, scale=None, page_table=None, want
         probs_len = int(probs_len if probs_len is not None else (kv_lens.max() if B else 0))
         probs = np.zeros((B, q_len, Hq, probs_len), dtype=np.float64)
     if nthreads is None:
-        nthreads = os.cpu_count() or 1
+        nthreads = default_threads()
     rc = lib.oracle_attention_indexed(B, q_len, Hq, Hkv, d, dt, float(scale), _ptr(q), _ptr(k),
                                       _ptr(v), s_blk, s_tok, s_head, page_size, _ptr(pt),
                                       max_pages, _ptr(kv_lens), _ptr(idx), _ptr(idx_len),

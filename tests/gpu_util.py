@@ -65,20 +65,3 @@ def compare(got_o, got_l, ref_o, ref_l, dtype, what):
     assert lerr <= tol, f"{what}: max abs lse error {lerr:.3e} > {tol:g}"
     return err, lerr
 
-
-def sample_units(case, n, seed):
-    """(b, hk) units to check one by one at full size: first, last, and seeded picks
-    (including the longest and shortest sequences when lengths differ)."""
-    B, Hkv = case["B"], case["Hkv"]
-    lens = case["kv_lens_np"]
-    picks = {(0, 0), (B - 1, Hkv - 1), (int(np.argmax(lens)), Hkv // 2), (int(np.argmin(lens)), 1 % Hkv)}
-    rng = np.random.default_rng(seed)
-    n = min(n, B * Hkv)
-    while len(picks) < n:
-        picks.add((int(rng.integers(B)), int(rng.integers(Hkv))))
-    return sorted(picks)
-
-
-def unit_rows(o, b, hk, G):
-    """[L, G, d] slice of a [B, L, Hq, d] array for kv head hk."""
-    return o[b, :, hk * G:(hk + 1) * G]
