@@ -19,9 +19,9 @@ namespace md {
 // into n_chunks chunks of chunk_len tokens.  A workgroup of kWaves waves
 // takes one chunk of hp units of the same sequence (hp adjacent kv heads):
 // kWaves / hp waves per unit, which interleave kTile-token tiles.  With
-// n_chunks > 1 the
-// chunks write normalised partial results and a merge pass combines them
-// by log-sum-exp (the split-KV decomposition named in the paper's Sec. 2).
+// n_chunks > 1 the chunks write normalised partial results and a merge pass
+// combines them by log-sum-exp (the split-KV decomposition named in the
+// paper's Sec. 2).
 constexpr int kWaves = 4;
 constexpr int kTile = 32;            // tokens per wave iteration
 constexpr int kMinChunkTokens = 1024;  // every wave gets >= 8 tiles of a chunk
