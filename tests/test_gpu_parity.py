@@ -130,16 +130,19 @@ def test_indexed_against_oracle(case):
         assert torch.equal(o2, o) and torch.equal(l2, l), "an unlisted key was read"
 
 
+@pytest.mark.parametrize("B,Hkv,Hq", [(64, 8, 8), (65, 8, 8), (256, 2, 8)],
+                         ids=["b64_hkv8", "b65_hkv8", "b256_hkv2"])
 @pytest.mark.parametrize("lo", [600, 5800], ids=["ragged_single_heads", "even_head_pairs"])
-def test_longest_first_dispatch(lo):
-    """A verify launch that takes units longest first (one chunk per unit:
-    64 sequences x 8 kv heads, lengths up to 6000, a paged cache): whole
-    output against the oracle, NaN padding included.  With lengths 600..6000
-    each workgroup serves one kv head; with 5800..6000 (every length within
-    1/16 of the mean) the kernel pairs the heads and half the workgroups
-    return without work."""
-    B, L, Hq, Hkv, d = 64, 4, 8, 8, 64
-    rng = np.random.default_rng(64)
+def test_longest_first_dispatch(lo, B, Hkv, Hq):
+    """A verify launch that takes units longest first (one chunk per unit,
+    enough head pairs to fill the device, lengths up to 6000, a paged cache):
+    whole output against the oracle, NaN padding included.  With lengths
+    600..6000 each workgroup serves one kv head; with 5800..6000 (every length
+    within 1/16 of the mean) the kernel pairs the heads and the workgroups
+    past the pairs return without work -- including an odd batch (65) and two
+    kv heads per sequence (one pair each)."""
+    L, d = 4, 64
+    rng = np.random.default_rng(64 + B + Hkv)
     lens = rng.integers(lo, 6001, size=B)
     lens[rng.integers(B)] = 6000
     say(f"[parity] longest-first verify: B={B} Hkv={Hkv} lens {lens.min()}..{lens.max()}")
