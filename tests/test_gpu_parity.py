@@ -45,6 +45,10 @@ SMALL = [
     ("bf16_page64", 2, 3, 4, 2, 128, [300, 129], "bf16", 64, 2, 40),
     ("f32_rows40_split", 1, 5, 8, 1, 128, [2600], "f32", 0, 16, 100),
     ("bf16_hkv4_split_paged", 2, 5, 16, 4, 128, [4000, 2500], "bf16", 16, 16, 496),
+    # 64 head pairs split into 4 chunks of >= 4096 tokens: pairs with a merge
+    ("bf16_head_pairs_split4_paged", 16, 4, 16, 8, 64,
+     [17000, 16500, 16900, 16400, 16800, 17000, 16600, 16950,
+      16700, 16850, 16450, 16999, 16550, 16650, 16750, 16890], "bf16", 16, 16, 240),
 ]
 
 
