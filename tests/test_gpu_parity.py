@@ -49,6 +49,11 @@ SMALL = [
     ("bf16_head_pairs_split4_paged", 16, 4, 16, 8, 64,
      [17000, 16500, 16900, 16400, 16800, 17000, 16600, 16950,
       16700, 16850, 16450, 16999, 16550, 16650, 16750, 16890], "bf16", 16, 16, 240),
+    # one past the longest-first batch limit: head pairs, no ranking
+    ("bf16_b257_pairs_no_lpt", 257, 4, 32, 8, 128, [100 + (i * 37) % 300 for i in range(257)],
+     "bf16", 16, 16, 64),
+    # one long sequence: 8 units split into 32 chunks of 4096, merged
+    ("bf16_b1_s128k_32chunks", 1, 5, 32, 8, 128, [131072], "bf16", 0, 64, 1984),
 ]
 
 
