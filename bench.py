@@ -176,7 +176,26 @@ def cpu_oracle_extras(c, w, logits, draft_tok, q_obs, n_obs, t_accept_us, t_vote
         oracle.snapkv_votes(q, k, S, pool=5)
         t_votes += time.perf_counter() - t0
     t_votes_all = t_votes / len(units) * w.B * w.Hkv
-    return {"greedy_accept_s (numpy, one thread, whole logits)": round(t_acc, 3),
+    # The oracle on one thread over the two smallest workloads: the whole of
+    # tiny_f32, and two of llama8b_b32_s8k's 32 sequences (all 8 kv heads).
+    one = {}
+    for name, B in (("tiny_f32", None), ("llama8b_b32_s8k", 2)):
+        ww = wl.WORKLOADS[name]
+        cc = wl.make_case(B=B or ww.B, q_len=ww.q_len, Hq=ww.Hq, Hkv=ww.Hkv, d=ww.d,
+                          kv_lens=[ww.S] * (B or ww.B), dtype=ww.dtype, seed=ww.seed_base,
+                          device="cpu", nan_pad=False)
+        q, k, v = (wl.to_host_bits(cc[x]) for x in ("q", "k", "v"))
+        lens = cc["kv_lens_np"]
+        t0 = time.perf_counter()
+        oracle.verify(q, k, v, lens, nthreads=1)
+        oracle.draft(q, k, v, lens, ww.n_sink, ww.window, nthreads=1)
+        dt = time.perf_counter() - t0
+        by = kv_bytes(ww, lens, "verify", ww.q_len) + kv_bytes(ww, lens, "draft", ww.q_len)
+        one[f"oracle_one_thread_{name}"] = {
+            "gbs": round(by / dt / 1e9, 4), "s": round(dt, 3),
+            "sample": "whole workload" if B is None else f"{B} of {ww.B} sequences"}
+    return {**one,
+            "greedy_accept_s (numpy, one thread, whole logits)": round(t_acc, 3),
             "greedy_accept_gpu_speedup": round(t_acc / (t_accept_us * 1e-6), 1),
             "snapkv_votes_s (fp64 C, one thread, 3 sampled units scaled to all)": round(t_votes_all, 2),
             "snapkv_votes_gpu_speedup": round(t_votes_all / (t_votes_us * 1e-6), 1)}
