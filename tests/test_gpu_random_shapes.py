@@ -1,0 +1,72 @@
+"""Seeded random problems across the parameter space, each against the fp64
+oracle: dtype, head_dim, kv heads, GQA group, q_len, batch, ragged lengths,
+page size, mode (verify, draft, listed draft).  They reach combinations of the
+plan's choices (head pairs, longest-first dispatch, split counts, row tiles)
+that the hand-picked cases do not name one by one."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2408_11049_amd as md
+from gpu_util import compare, run_gpu, run_oracle, say
+from paper_2408_11049_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+N_CASES = 32
+WORK_BOUND = 3e8  # sum of S_b * Hq * q_len * d per case: keeps the oracle to well under a second
+
+
+def draw(i):
+    """Problem i: sizes from a generator seeded by i (independent of the others)."""
+    rng = np.random.default_rng(1000 + i)
+    dtype = str(rng.choice(["bf16", "bf16", "f32"]))
+    d = int(rng.choice([64, 128]))
+    Hkv = int(rng.choice([1, 2, 3, 4, 8]))
+    while True:
+        G = int(rng.choice([1, 2, 4, 8]))
+        L = int(rng.integers(1, 17))
+        if G * L <= 64:
+            break
+    B = int(rng.choice([1, 2, 5, 17, 40, 64, 65]))
+    s_max = int(rng.choice([64, 600, 3000, 9000]))
+    lens = rng.integers(L, s_max + 1, size=B)
+    while lens.sum() * G * Hkv * L * d > WORK_BOUND and lens.max() > L:
+        lens = np.maximum(L, lens // 2)
+    page = int(rng.choice([0, 0, 1, 8, 16, 64]))
+    mode = int(rng.choice([oracle.VERIFY, oracle.DRAFT, oracle.INDEXED]))
+    n_sink = int(rng.integers(0, 20))
+    window = int(rng.integers(1, 600))
+    budget = int(rng.integers(0, 700))
+    return dict(dtype=dtype, d=d, Hkv=Hkv, Hq=G * Hkv, L=L, B=B, lens=lens.astype(np.int32),
+                page=page, mode=mode, n_sink=n_sink, window=window, budget=budget)
+
+
+@pytest.mark.parametrize("i", range(N_CASES))
+def test_random_problem(i):
+    p = draw(i)
+    name = ["verify", "draft", "listed draft"][p["mode"]]
+    say(f"[random {i}] {name} {p['dtype']} d={p['d']} B={p['B']} L={p['L']} Hq={p['Hq']} "
+        f"Hkv={p['Hkv']} page={p['page']} lens {p['lens'].min()}..{p['lens'].max()} "
+        f"sink={p['n_sink']} window={p['window']} budget={p['budget']}")
+    c = wl.make_case(B=p["B"], q_len=p["L"], Hq=p["Hq"], Hkv=p["Hkv"], d=p["d"], kv_lens=p["lens"],
+                     dtype=p["dtype"], page_size=p["page"], seed=2000 + i, device=DEV,
+                     S_alloc=None if p["page"] else int(p["lens"].max()) + 3)
+    if p["mode"] == oracle.INDEXED:
+        idx, n = wl.index_lists(p["B"], p["Hkv"], p["lens"], p["L"], p["budget"], 3000 + i)
+        o = torch.full_like(c["q"], float("nan"))
+        lse = torch.full(c["q"].shape[:3], float("nan"), dtype=torch.float32, device=DEV)
+        md.md_draft_attn_indexed(c["q"], c["k"], c["v"], c["kv_lens"], torch.from_numpy(idx).to(DEV),
+                                 torch.from_numpy(n).to(DEV), max_kv_len=c["max_kv_len"],
+                                 page_table=c["page_table"], out=o, lse=lse)
+        torch.cuda.synchronize()
+        go = o.float().cpu().numpy().astype(np.float64)
+        gl = lse.cpu().numpy().astype(np.float64)
+        ro, rl = oracle.indexed(wl.to_host_bits(c["q"]), wl.to_host_bits(c["k"]),
+                                wl.to_host_bits(c["v"]), p["lens"], idx, n,
+                                page_table=c["page_table_np"])
+    else:
+        go, gl = run_gpu(p["mode"], c, p["n_sink"], p["window"])
+        ro, rl = run_oracle(p["mode"], c, p["n_sink"], p["window"])
+    compare(go, gl, ro, rl, p["dtype"], f"random {i} ({name})")
