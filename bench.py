@@ -18,9 +18,15 @@ reported beside them.
 
 `value` is K/V HBM GB/s: the algorithmic K/V bytes of verify + draft (every
 visible K and V element once) divided by the step time.  `roofline` is for
-the dominant kernel (the verify attention kernel, a single launch here).
+the dominant kernel (the verify attention kernel, a single launch here), with
+the HBM traffic and MFMA utilisation read from the committed rocprofv3
+summaries under profiles/ (null when the kernel source changed since).
 `cpu_baseline` is the fp64 oracle timed on a bounded sample of the same
-workload on this host's cores (a reported baseline, not a target).
+workload on this host's cores (a reported baseline, not a target).  `detail`
+adds the one-token and warm timings, the listed and gathered SnapKV-style
+drafts, the SnapKV selection, append, acceptance and commit, whole
+engine-shaped speculative steps (eager and as a HIP graph), the read ceiling
+and the oracle beside the step kernels.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
 """
