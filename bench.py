@@ -105,6 +105,25 @@ def read_mfma():
             "peak_tflops": 2500.0, "source": "profiles/attn_mfma_llama8b_b64_s32k_paged.md"}
 
 
+def input_sha256(c, piece=1 << 28):
+    """SHA-256 of each seeded input tensor's bytes (the whole K and V pools
+    included), so that two runs can be shown to have timed the same data.
+    Tensors are copied to the host a piece at a time."""
+    import torch
+
+    out = {}
+    for name in ("q", "k", "v", "kv_lens", "page_table"):
+        t = c.get(name)
+        if t is None:
+            continue
+        flat = t.detach().contiguous().view(-1).view(torch.uint8)
+        h = hashlib.sha256()
+        for s in range(0, flat.numel(), piece):
+            h.update(flat[s:s + piece].cpu().numpy().tobytes())
+        out[name] = h.hexdigest()
+    return out
+
+
 def cpu_baseline(c, w, budget_s=15.0, batch=32):
     """The fp64 oracle (as it stands) on a bounded sample of the same workload:
     verify + draft over (sequence, kv head) units in seeded random order,
@@ -232,6 +251,7 @@ def main():
     w = wl.WORKLOADS[WORKLOAD]
     log(f"[bench] generating {WORKLOAD} on {torch.cuda.get_device_name(dev)}")
     c = wl.make_workload(w, device=dev)
+    inputs = input_sha256(c)
     lens = c["kv_lens_np"]
     L = w.q_len
     out_v = torch.empty_like(c["q"])
@@ -575,6 +595,7 @@ def main():
                    "page_size": w.page_size, "cache": "cold (1 GiB flush before each call)"},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "inputs_sha256": inputs,
         "detail": {
             "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
             "t_verify_us": round(float(np.mean(tv)), 2),

@@ -98,7 +98,8 @@ int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void*
     if ((reinterpret_cast<uintptr_t>(idx) & 3u) || (reinterpret_cast<uintptr_t>(idx_len) & 3u))
       return MD_ERR_INVALID_ARG;
   }
-  const Plan pl = make_plan(a, mode, n_sink, window, device_cu_count());
+  const int num_cus = device_cu_count();
+  const Plan pl = make_plan(a, mode, n_sink, window, num_cus);
   const bool bf16 = a->dtype == MD_BF16;
   const bool paged = a->page_size != 0;
 
@@ -141,9 +142,10 @@ int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void*
   int64_t n_blocks = pl.n_groups * pl.n_chunks;
   if (p.lpt && pl.hp == 2) {
     // One workgroup per unit; the kernel pairs heads (and idles the surplus
-    // half) only when the lengths leave nothing for longest-first to balance.
+    // half) only when longest-first can still balance the pairs.
     p.hp = 1;
     p.hp_auto = 1;
+    p.slots = num_cus > 0 ? num_cus : 256;
     n_blocks = pl.n_units;
   }
   p.o = a->o;

@@ -97,11 +97,17 @@ __device__ __forceinline__ int real_token(const UnitGeom& u, int v) {
 // with the same arithmetic.
 //
 // With p.hp_auto the grid has one workgroup per unit and the kernel chooses
-// hp here: head pairs stream faster, but there are half as many of them, too
-// few for longest-first to even out unequal lengths.  Pairs are taken when
-// the longest clamped length is within 1/16 of the mean (the workgroups past
-// the pairs then return at once); otherwise one head per workgroup.  Returns
-// the head group, or -1 for a workgroup with nothing to do.
+// hp here: head pairs stream faster, but there are half as many of them, and
+// each is twice as long -- at one pair per compute unit, too few and too
+// coarse for longest-first to even out unequal lengths.  Pairs are taken when
+// the longest clamped length is within 1/16 of the mean, or when there are at
+// least two pairs per compute unit and the longest pair is no more than a
+// compute unit's mean share of the work (the workgroups past the pairs then
+// return at once); otherwise one head per workgroup.  Measured on MI355X
+// (Llama-3.1-8B heads, lengths uniform in a range): at B = 64 single heads
+// beat pairs by 6-33% on ragged lengths; at B = 128 and 256 pairs beat
+// single heads by 4-7%.  Returns the head group, or -1 for a workgroup with
+// nothing to do.
 template <typename P>
 __device__ __forceinline__ int lpt_group(const P& p, int r, int* sl, int& hp) {
   const int B = p.num_seqs;
@@ -122,7 +128,12 @@ __device__ __forceinline__ int lpt_group(const P& p, int r, int* sl, int& hp) {
         mx = max(mx, __shfl_xor(mx, o));
         sum += __shfl_xor(sum, o);
       }
-      if (threadIdx.x == 0) sl[kLptMaxSeqs + 1] = 16LL * mx * B <= 17LL * sum ? 2 : 1;
+      if (threadIdx.x == 0) {
+        const bool even = 16LL * mx * B <= 17LL * sum;
+        const bool many = static_cast<long long>(B) * p.Hkv >= 4LL * p.slots &&
+                          2LL * mx * p.slots <= static_cast<long long>(p.Hkv) * sum;
+        sl[kLptMaxSeqs + 1] = (even || many) ? 2 : 1;
+      }
     }
     __syncthreads();
     hp = sl[kLptMaxSeqs + 1];

@@ -36,7 +36,8 @@ struct AttnParams {
   int32_t lpt;                // 1: workgroups take sequences longest first (see attn.hip)
   int32_t hp;                 // kv heads per workgroup (1 or 2; divides Hkv)
   int32_t hp_auto;            // longest-first launch of one workgroup per unit that
-                              // pairs heads when the lengths are even (see attn.hip)
+                              // pairs heads when the lengths allow (see attn.hip)
+  int32_t slots;              // compute units of the device (hp_auto's balance test)
   const int32_t* idx;         // indexed draft: [B, Hkv, idx_stride] prompt positions
   const int32_t* idx_len;     // indexed draft: [B] list lengths
   int32_t idx_stride;

@@ -139,17 +139,19 @@ def test_indexed_against_oracle(case):
         assert torch.equal(o2, o) and torch.equal(l2, l), "an unlisted key was read"
 
 
-@pytest.mark.parametrize("B,Hkv,Hq", [(64, 8, 8), (65, 8, 8), (256, 2, 8)],
-                         ids=["b64_hkv8", "b65_hkv8", "b256_hkv2"])
-@pytest.mark.parametrize("lo", [600, 5800], ids=["ragged_single_heads", "even_head_pairs"])
+@pytest.mark.parametrize("B,Hkv,Hq", [(64, 8, 8), (65, 8, 8), (256, 2, 8), (128, 8, 8)],
+                         ids=["b64_hkv8", "b65_hkv8", "b256_hkv2", "b128_hkv8"])
+@pytest.mark.parametrize("lo", [600, 5800], ids=["ragged", "even"])
 def test_longest_first_dispatch(lo, B, Hkv, Hq):
     """A verify launch that takes units longest first (one chunk per unit,
     enough head pairs to fill the device, lengths up to 6000, a paged cache):
     whole output against the oracle, NaN padding included.  With lengths
-    600..6000 each workgroup serves one kv head; with 5800..6000 (every length
-    within 1/16 of the mean) the kernel pairs the heads and the workgroups
-    past the pairs return without work -- including an odd batch (65) and two
-    kv heads per sequence (one pair each)."""
+    600..6000 and at most one pair per compute unit (B = 64, 65; 256 with two
+    kv heads) each workgroup serves one kv head; with 5800..6000 (every length
+    within 1/16 of the mean), or with two pairs per compute unit (B = 128,
+    eight kv heads) and ragged lengths, the kernel pairs the heads and the
+    workgroups past the pairs return without work -- including an odd batch
+    (65) and two kv heads per sequence (one pair each)."""
     L, d = 4, 64
     rng = np.random.default_rng(64 + B + Hkv)
     lens = rng.integers(lo, 6001, size=B)
