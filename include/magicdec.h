@@ -128,8 +128,10 @@ typedef struct {
  * Errors: MD_ERR_INVALID_ARG for a NULL args/q/k/v/o/kv_lens, a NULL or
  * superfluous page_table, bad sizes, a non power-of-two page size, a table too
  * narrow for max_kv_len, max_kv_len < q_len, misaligned pointers or strides;
- * MD_ERR_UNSUPPORTED for head_dim not in {64,128} or G*L > 64;
- * MD_ERR_WORKSPACE; MD_ERR_HIP.
+ * MD_ERR_UNSUPPORTED for head_dim not in {64,128}, G*L > 64, or sizes past
+ * the kernels' 32-bit indexing: kv_stride_tok > 2^28 elements,
+ * num_seqs * num_kv_heads > 2^31 - 1, num_seqs * q_len * num_q_heads >
+ * 4 (2^31 - 1); MD_ERR_WORKSPACE; MD_ERR_HIP.
  */
 int md_verify_attn(const md_attn_args* a, void* stream);
 
@@ -175,7 +177,8 @@ int md_draft_attn_indexed(const md_attn_args* a, const int32_t* idx, const int32
  *   lse       [n_rows] fp32 or NULL
  * All device pointers, 16-byte aligned.  Errors: MD_ERR_INVALID_ARG for
  * n_parts < 1, n_rows < 0, NULL or misaligned pointers, a bad dtype;
- * MD_ERR_UNSUPPORTED for head_dim not in {64,128}; MD_ERR_HIP.
+ * MD_ERR_UNSUPPORTED for head_dim not in {64,128} or n_rows > 4 (2^31 - 1);
+ * MD_ERR_HIP.
  */
 int md_merge_lse(int32_t n_parts, int64_t n_rows, int32_t head_dim, int32_t out_dtype,
                  const float* o_parts, const float* lse_parts, void* o, float* lse,
@@ -235,8 +238,8 @@ typedef struct {
 /* Votes of every (sequence, kv head) prefix position.  Errors:
  * MD_ERR_INVALID_ARG for NULL or misaligned pointers, bad sizes, a votes
  * stride below max_prompt_len - n_obs, max_prompt_len < n_obs;
- * MD_ERR_UNSUPPORTED for head_dim not in {64,128} or G * n_obs > 256;
- * MD_ERR_WORKSPACE; MD_ERR_HIP. */
+ * MD_ERR_UNSUPPORTED for head_dim not in {64,128}, G * n_obs > 256 or
+ * num_seqs * num_kv_heads > 2^31 - 1; MD_ERR_WORKSPACE; MD_ERR_HIP. */
 int md_snapkv_votes(const md_snapkv_args* a, void* stream);
 size_t md_snapkv_workspace_bytes(const md_snapkv_args* a);
 

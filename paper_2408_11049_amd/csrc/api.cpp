@@ -212,6 +212,7 @@ int md_merge_lse(int32_t n_parts, int64_t n_rows, int32_t head_dim, int32_t out_
   if (n_parts < 1 || n_rows < 0) return MD_ERR_INVALID_ARG;
   if (out_dtype != MD_F32 && out_dtype != MD_BF16) return MD_ERR_INVALID_ARG;
   if (head_dim != 64 && head_dim != 128) return MD_ERR_UNSUPPORTED;
+  if ((n_rows + 3) / 4 > INT32_MAX) return MD_ERR_UNSUPPORTED;  // four rows per workgroup
   if (n_rows == 0) return MD_OK;
   if (!o_parts || !lse_parts || !o) return MD_ERR_INVALID_ARG;
   if (!md::aligned16(o_parts) || !md::aligned16(lse_parts) || !md::aligned16(o) || (lse && !md::aligned16(lse)))
@@ -225,19 +226,13 @@ size_t md_workspace_bytes(const md_attn_args* a, int32_t mode, int32_t n_sink, i
   if (!a) return 0;
   if (mode != MD_MODE_VERIFY && mode != MD_MODE_DRAFT) return 0;
   if (mode == MD_MODE_DRAFT && (n_sink < 0 || window < 1)) return 0;
-  if (a->num_seqs < 0 || a->q_len < 1 || a->num_q_heads < 1 || a->num_kv_heads < 1 ||
-      a->num_q_heads % a->num_kv_heads || a->max_kv_len < a->q_len ||
-      (a->head_dim != 64 && a->head_dim != 128))
-    return 0;
+  if (md::check_attn_sizes(a) != MD_OK) return 0;
   return md::make_plan(a, mode, n_sink, window, md::device_cu_count()).workspace_bytes;
 }
 
 size_t md_workspace_bytes_indexed(const md_attn_args* a, int32_t idx_stride) {
   if (!a || idx_stride < 1) return 0;
-  if (a->num_seqs < 0 || a->q_len < 1 || a->num_q_heads < 1 || a->num_kv_heads < 1 ||
-      a->num_q_heads % a->num_kv_heads || a->max_kv_len < a->q_len ||
-      (a->head_dim != 64 && a->head_dim != 128))
-    return 0;
+  if (md::check_attn_sizes(a) != MD_OK) return 0;
   return md::make_plan(a, MD_MODE_DRAFT_INDEXED, 0, idx_stride, md::device_cu_count())
       .workspace_bytes;
 }
@@ -288,7 +283,8 @@ int md_snapkv_votes(const md_snapkv_args* a, void* stream) {
 
 size_t md_snapkv_workspace_bytes(const md_snapkv_args* a) {
   if (!a || a->num_seqs < 0 || a->n_obs < 1 || a->num_q_heads < 1 || a->num_kv_heads < 1 ||
-      a->num_q_heads % a->num_kv_heads || a->max_prompt_len < a->n_obs)
+      a->num_q_heads % a->num_kv_heads || a->max_prompt_len < a->n_obs ||
+      static_cast<int64_t>(a->num_seqs) * a->num_kv_heads > INT32_MAX)
     return 0;
   return md::make_snapkv_plan(a, md::device_cu_count()).workspace_bytes;
 }

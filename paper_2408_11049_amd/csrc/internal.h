@@ -48,6 +48,16 @@ struct Plan {
   size_t workspace_bytes = 0;
 };
 
+// Kernel index limits: workgroup, unit and row counts are 32-bit, and a
+// full verify tile adds a 32-bit per-lane offset spanning up to 7 token rows,
+// so the token stride is bounded.
+constexpr int64_t kMaxTokStride = int64_t{1} << 28;  // elements
+
+// Shape checks shared by the attention calls and their workspace queries:
+// MD_OK, MD_ERR_INVALID_ARG (malformed) or MD_ERR_UNSUPPORTED (beyond the
+// compiled limits).  Only sizes are read.
+int check_attn_sizes(const md_attn_args* a);
+
 // Checks every argument the host can see.  Returns MD_OK or an md_status.
 // mode MD_MODE_DRAFT_INDEXED reads `window` as the list capacity idx_stride.
 int validate_attn(const md_attn_args* a, int mode, int n_sink, int window);

@@ -29,6 +29,24 @@ int64_t visible_bound(int64_t max_kv_len, int L, int mode, int64_t n_sink, int64
 
 }  // namespace
 
+int check_attn_sizes(const md_attn_args* a) {
+  if (a->num_seqs < 0) return MD_ERR_INVALID_ARG;
+  if (a->q_len < 1 || a->q_len > 16) return MD_ERR_INVALID_ARG;
+  if (a->num_q_heads < 1 || a->num_kv_heads < 1) return MD_ERR_INVALID_ARG;
+  if (a->num_q_heads % a->num_kv_heads != 0) return MD_ERR_INVALID_ARG;
+  if (a->head_dim < 1) return MD_ERR_INVALID_ARG;
+  if (a->max_kv_len < a->q_len) return MD_ERR_INVALID_ARG;
+  if (a->head_dim != 64 && a->head_dim != 128) return MD_ERR_UNSUPPORTED;
+  if (static_cast<int64_t>(a->num_q_heads / a->num_kv_heads) * a->q_len > kMaxRows)
+    return MD_ERR_UNSUPPORTED;
+  if (a->kv_stride_tok > kMaxTokStride) return MD_ERR_UNSUPPORTED;
+  // Units (workgroups) and query rows (merge workgroups of four rows) in 32 bits.
+  if (static_cast<int64_t>(a->num_seqs) * a->num_kv_heads > INT32_MAX) return MD_ERR_UNSUPPORTED;
+  const int64_t rows_per_seq = static_cast<int64_t>(a->q_len) * a->num_q_heads;
+  if (a->num_seqs > 4 * static_cast<int64_t>(INT32_MAX) / rows_per_seq) return MD_ERR_UNSUPPORTED;
+  return MD_OK;
+}
+
 int validate_attn(const md_attn_args* a, int mode, int n_sink, int window) {
   if (!a) return MD_ERR_INVALID_ARG;
   if (mode != MD_MODE_VERIFY && mode != MD_MODE_DRAFT && mode != MD_MODE_DRAFT_INDEXED)
@@ -52,9 +70,8 @@ int validate_attn(const md_attn_args* a, int mode, int n_sink, int window) {
   }
   if (a->kv_stride_blk < 0 || a->kv_stride_tok < 0 || a->kv_stride_head < 0)
     return MD_ERR_INVALID_ARG;
-  if (a->head_dim != 64 && a->head_dim != 128) return MD_ERR_UNSUPPORTED;
-  const int64_t G = a->num_q_heads / a->num_kv_heads;
-  if (G * a->q_len > kMaxRows) return MD_ERR_UNSUPPORTED;
+  const int sizes = check_attn_sizes(a);
+  if (sizes != MD_OK) return sizes;
   if (a->num_seqs == 0) return MD_OK;  // nothing will be read or written
 
   if (!a->q || !a->k || !a->v || !a->o || !a->kv_lens) return MD_ERR_INVALID_ARG;
@@ -211,6 +228,7 @@ int validate_snapkv(const md_snapkv_args* a) {
   if (a->head_dim != 64 && a->head_dim != 128) return MD_ERR_UNSUPPORTED;
   if (static_cast<int64_t>(a->num_q_heads / a->num_kv_heads) * a->n_obs > kSnapkvMaxRows)
     return MD_ERR_UNSUPPORTED;
+  if (static_cast<int64_t>(a->num_seqs) * a->num_kv_heads > INT32_MAX) return MD_ERR_UNSUPPORTED;
   if (a->num_seqs == 0) return MD_OK;
   if (!a->q_obs || !a->k || !a->prompt_lens || !a->votes) return MD_ERR_INVALID_ARG;
   if (paged != (a->page_table != nullptr)) return MD_ERR_INVALID_ARG;

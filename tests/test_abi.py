@@ -113,6 +113,10 @@ BAD = [
                                    page_table=FAKE), md.MD_ERR_INVALID_ARG),
     ("head_dim 96", dict(head_dim=96), md.MD_ERR_UNSUPPORTED),
     ("G*L > 64", dict(num_q_heads=34, num_kv_heads=2), md.MD_ERR_UNSUPPORTED),
+    # 32-bit kernel indexing: per-lane row offsets, workgroup and row counts.
+    ("token stride over 2^28", dict(kv_stride_tok=(1 << 28) + 8), md.MD_ERR_UNSUPPORTED),
+    ("units over 2^31 - 1", dict(num_seqs=1 << 30), md.MD_ERR_UNSUPPORTED),
+    ("rows over 4 (2^31 - 1)", dict(num_seqs=1 << 28), md.MD_ERR_UNSUPPORTED),
 ]
 
 
@@ -120,6 +124,10 @@ BAD = [
 def test_verify_rejects(lib, name, over, want):
     assert lib.md_verify_attn(ctypes.byref(good_args(**over)), None) == want
     assert lib.md_draft_attn(ctypes.byref(good_args(**over)), 4, 16, None) == want
+    if want == md.MD_ERR_UNSUPPORTED:  # the workspace queries refuse the same sizes
+        a = ctypes.byref(good_args(**over))
+        assert lib.md_workspace_bytes(a, md.MD_MODE_VERIFY, 0, 1) == 0
+        assert lib.md_workspace_bytes_indexed(a, 64) == 0
 
 
 def test_indexed_rejects(lib):
@@ -164,6 +172,7 @@ SNAP_BAD = [
     ("misaligned k", dict(k=FAKE + 4), md.MD_ERR_INVALID_ARG),
     ("rows over 256", dict(n_obs=65, max_prompt_len=200, votes_stride=200), md.MD_ERR_UNSUPPORTED),
     ("head_dim 80", dict(head_dim=80), md.MD_ERR_UNSUPPORTED),
+    ("units over 2^31 - 1", dict(num_seqs=1 << 30), md.MD_ERR_UNSUPPORTED),
     ("no workspace", dict(), md.MD_ERR_WORKSPACE),
 ]
 
@@ -261,6 +270,7 @@ MERGE_BAD = [
     ("null o_parts", dict(op=None), md.MD_ERR_INVALID_ARG),
     ("null o", dict(o=None), md.MD_ERR_INVALID_ARG),
     ("misaligned lse", dict(lse=FAKE + 4), md.MD_ERR_INVALID_ARG),
+    ("rows over 4 (2^31 - 1)", dict(n_rows=4 * 2**31), md.MD_ERR_UNSUPPORTED),
 ]
 
 
