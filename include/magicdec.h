@@ -129,7 +129,8 @@ typedef struct {
  * superfluous page_table, bad sizes, a non power-of-two page size, a table too
  * narrow for max_kv_len, max_kv_len < q_len, misaligned pointers or strides;
  * MD_ERR_UNSUPPORTED for head_dim not in {64,128}, G*L > 64, or sizes past
- * the kernels' 32-bit indexing: kv_stride_tok > 2^28 elements,
+ * the kernels' 32-bit indexing: max_kv_len (or a draft window or list
+ * capacity) > 2^31 - 65, kv_stride_tok > 2^28 elements,
  * num_seqs * num_kv_heads > 2^31 - 1, num_seqs * q_len * num_q_heads >
  * 4 (2^31 - 1); MD_ERR_WORKSPACE; MD_ERR_HIP.
  */

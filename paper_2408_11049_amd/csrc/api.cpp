@@ -225,13 +225,13 @@ int md_merge_lse(int32_t n_parts, int64_t n_rows, int32_t head_dim, int32_t out_
 size_t md_workspace_bytes(const md_attn_args* a, int32_t mode, int32_t n_sink, int32_t window) {
   if (!a) return 0;
   if (mode != MD_MODE_VERIFY && mode != MD_MODE_DRAFT) return 0;
-  if (mode == MD_MODE_DRAFT && (n_sink < 0 || window < 1)) return 0;
+  if (mode == MD_MODE_DRAFT && (n_sink < 0 || window < 1 || window > md::kMaxPosition)) return 0;
   if (md::check_attn_sizes(a) != MD_OK) return 0;
   return md::make_plan(a, mode, n_sink, window, md::device_cu_count()).workspace_bytes;
 }
 
 size_t md_workspace_bytes_indexed(const md_attn_args* a, int32_t idx_stride) {
-  if (!a || idx_stride < 1) return 0;
+  if (!a || idx_stride < 1 || idx_stride > md::kMaxPosition) return 0;
   if (md::check_attn_sizes(a) != MD_OK) return 0;
   return md::make_plan(a, MD_MODE_DRAFT_INDEXED, 0, idx_stride, md::device_cu_count())
       .workspace_bytes;

@@ -52,6 +52,9 @@ struct Plan {
 // full verify tile adds a 32-bit per-lane offset spanning up to 7 token rows,
 // so the token stride is bounded.
 constexpr int64_t kMaxTokStride = int64_t{1} << 28;  // elements
+// Token positions, windows and list capacities stay below this, so that a
+// position plus a tile, q_len or the window arithmetic of a unit never wraps.
+constexpr int32_t kMaxPosition = INT32_MAX - 64;
 
 // Shape checks shared by the attention calls and their workspace queries:
 // MD_OK, MD_ERR_INVALID_ARG (malformed) or MD_ERR_UNSUPPORTED (beyond the

@@ -40,6 +40,7 @@ int check_attn_sizes(const md_attn_args* a) {
   if (static_cast<int64_t>(a->num_q_heads / a->num_kv_heads) * a->q_len > kMaxRows)
     return MD_ERR_UNSUPPORTED;
   if (a->kv_stride_tok > kMaxTokStride) return MD_ERR_UNSUPPORTED;
+  if (a->max_kv_len > kMaxPosition) return MD_ERR_UNSUPPORTED;
   // Units (workgroups) and query rows (merge workgroups of four rows) in 32 bits.
   if (static_cast<int64_t>(a->num_seqs) * a->num_kv_heads > INT32_MAX) return MD_ERR_UNSUPPORTED;
   const int64_t rows_per_seq = static_cast<int64_t>(a->q_len) * a->num_q_heads;
@@ -53,6 +54,7 @@ int validate_attn(const md_attn_args* a, int mode, int n_sink, int window) {
     return MD_ERR_INVALID_ARG;
   if (mode == MD_MODE_DRAFT && (n_sink < 0 || window < 1)) return MD_ERR_INVALID_ARG;
   if (mode == MD_MODE_DRAFT_INDEXED && window < 1) return MD_ERR_INVALID_ARG;
+  if (mode != MD_MODE_VERIFY && window > kMaxPosition) return MD_ERR_UNSUPPORTED;
   if (a->num_seqs < 0) return MD_ERR_INVALID_ARG;
   if (a->q_len < 1 || a->q_len > 16) return MD_ERR_INVALID_ARG;
   if (a->num_q_heads < 1 || a->num_kv_heads < 1) return MD_ERR_INVALID_ARG;

@@ -117,6 +117,7 @@ BAD = [
     ("token stride over 2^28", dict(kv_stride_tok=(1 << 28) + 8), md.MD_ERR_UNSUPPORTED),
     ("units over 2^31 - 1", dict(num_seqs=1 << 30), md.MD_ERR_UNSUPPORTED),
     ("rows over 4 (2^31 - 1)", dict(num_seqs=1 << 28), md.MD_ERR_UNSUPPORTED),
+    ("max_kv_len within 64 of 2^31", dict(max_kv_len=2**31 - 60), md.MD_ERR_UNSUPPORTED),
 ]
 
 
@@ -128,6 +129,14 @@ def test_verify_rejects(lib, name, over, want):
         a = ctypes.byref(good_args(**over))
         assert lib.md_workspace_bytes(a, md.MD_MODE_VERIFY, 0, 1) == 0
         assert lib.md_workspace_bytes_indexed(a, 64) == 0
+
+
+def test_window_past_position_limit(lib):
+    a = ctypes.byref(good_args())
+    assert lib.md_draft_attn(a, 4, 2**31 - 60, None) == md.MD_ERR_UNSUPPORTED
+    assert lib.md_draft_attn_indexed(a, FAKE, FAKE, 2**31 - 60, None) == md.MD_ERR_UNSUPPORTED
+    assert lib.md_workspace_bytes(a, md.MD_MODE_DRAFT, 4, 2**31 - 60) == 0
+    assert lib.md_workspace_bytes_indexed(a, 2**31 - 60) == 0
 
 
 def test_indexed_rejects(lib):
