@@ -29,13 +29,20 @@ int64_t visible_bound(int64_t max_kv_len, int L, int mode, int64_t n_sink, int64
 
 }  // namespace
 
-int check_attn_sizes(const md_attn_args* a) {
+// Sizes that are malformed in themselves.
+static int check_attn_shape(const md_attn_args* a) {
   if (a->num_seqs < 0) return MD_ERR_INVALID_ARG;
   if (a->q_len < 1 || a->q_len > 16) return MD_ERR_INVALID_ARG;
   if (a->num_q_heads < 1 || a->num_kv_heads < 1) return MD_ERR_INVALID_ARG;
   if (a->num_q_heads % a->num_kv_heads != 0) return MD_ERR_INVALID_ARG;
   if (a->head_dim < 1) return MD_ERR_INVALID_ARG;
   if (a->max_kv_len < a->q_len) return MD_ERR_INVALID_ARG;
+  return MD_OK;
+}
+
+int check_attn_sizes(const md_attn_args* a) {
+  const int shape = check_attn_shape(a);
+  if (shape != MD_OK) return shape;
   if (a->head_dim != 64 && a->head_dim != 128) return MD_ERR_UNSUPPORTED;
   if (static_cast<int64_t>(a->num_q_heads / a->num_kv_heads) * a->q_len > kMaxRows)
     return MD_ERR_UNSUPPORTED;
@@ -54,14 +61,9 @@ int validate_attn(const md_attn_args* a, int mode, int n_sink, int window) {
     return MD_ERR_INVALID_ARG;
   if (mode == MD_MODE_DRAFT && (n_sink < 0 || window < 1)) return MD_ERR_INVALID_ARG;
   if (mode == MD_MODE_DRAFT_INDEXED && window < 1) return MD_ERR_INVALID_ARG;
-  if (mode != MD_MODE_VERIFY && window > kMaxPosition) return MD_ERR_UNSUPPORTED;
-  if (a->num_seqs < 0) return MD_ERR_INVALID_ARG;
-  if (a->q_len < 1 || a->q_len > 16) return MD_ERR_INVALID_ARG;
-  if (a->num_q_heads < 1 || a->num_kv_heads < 1) return MD_ERR_INVALID_ARG;
-  if (a->num_q_heads % a->num_kv_heads != 0) return MD_ERR_INVALID_ARG;
+  const int shape = check_attn_shape(a);
+  if (shape != MD_OK) return shape;
   if (a->dtype != MD_F32 && a->dtype != MD_BF16) return MD_ERR_INVALID_ARG;
-  if (a->head_dim < 1) return MD_ERR_INVALID_ARG;
-  if (a->max_kv_len < a->q_len) return MD_ERR_INVALID_ARG;
   const bool paged = a->page_size != 0;
   if (a->page_size < 0) return MD_ERR_INVALID_ARG;
   if (paged) {
@@ -72,6 +74,8 @@ int validate_attn(const md_attn_args* a, int mode, int n_sink, int window) {
   }
   if (a->kv_stride_blk < 0 || a->kv_stride_tok < 0 || a->kv_stride_head < 0)
     return MD_ERR_INVALID_ARG;
+  // Every malformed argument above is reported before a limit below.
+  if (mode != MD_MODE_VERIFY && window > kMaxPosition) return MD_ERR_UNSUPPORTED;
   const int sizes = check_attn_sizes(a);
   if (sizes != MD_OK) return sizes;
   if (a->num_seqs == 0) return MD_OK;  // nothing will be read or written
