@@ -18,8 +18,10 @@
  *     NULL is the null stream).  Buffers must stay alive and unmodified until
  *     the stream reaches the call.  Nothing synchronises with the host.
  *   - Calls are thread-safe and re-entrant.  The only global state is a
- *     per-device cache of the compute-unit count and the MD_* tuning
- *     overrides, read once from the environment.
+ *     per-device cache of the compute-unit count.  The MD_* tuning overrides
+ *     (MD_PREFETCH_DEPTH, MD_OCCUPANCY, MD_LPT, MD_HEADS_PER_WG; for
+ *     measurement) are read from the environment on every call; do not
+ *     change them while another thread is inside the library.
  *   - Errors are return codes (md_status).  Argument errors are detected on
  *     the host before any HIP call, so a failed call has launched nothing.
  *   - Device-side contract violations leave memory in bounds but results

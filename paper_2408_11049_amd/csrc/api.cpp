@@ -49,14 +49,8 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 // K/V tiles in flight per wave.  MD_PREFETCH_DEPTH (1..3) overrides the
 // default, for tuning sweeps.
-int env_int(const char* name, int lo, int hi) {
-  const char* e = getenv(name);
-  int v = e ? atoi(e) : 0;
-  return (v >= lo && v <= hi) ? v : 0;
-}
-
 int prefetch_depth(int NT, int mode) {
-  static const int forced = env_int("MD_PREFETCH_DEPTH", 1, 3);
+  const int forced = env_knob("MD_PREFETCH_DEPTH", 1, 3);
   (void)NT;
   (void)mode;
   // Measured on MI355X: with K and V both streamed as whole rows, one tile in
@@ -70,7 +64,7 @@ int prefetch_depth(int NT, int mode) {
 // best at one wave per SIMD (more registers, no spills); the short draft
 // calls and single-row-tile shapes at two.
 int occupancy(int NT, int depth, int mode) {
-  static const int forced = env_int("MD_OCCUPANCY", 1, 2);
+  const int forced = env_knob("MD_OCCUPANCY", 1, 2);
   if (forced) return forced;
   if (depth != 1 || NT > 2) return 1;
   return (mode == MD_MODE_VERIFY && NT == 2) ? 1 : 2;
@@ -81,7 +75,7 @@ int occupancy(int NT, int depth, int mode) {
 // thread, so small batches only).  MD_LPT = 1 or 2 forces it off (1) or on
 // where allowed (2), for A/B measurements.
 int longest_first(int mode, int n_chunks, int num_seqs, int max_kv_len) {
-  static const int forced = env_int("MD_LPT", 1, 2);
+  const int forced = env_knob("MD_LPT", 1, 2);
   if (mode != MD_MODE_VERIFY || n_chunks != 1 || num_seqs < 2 || num_seqs > kLptMaxSeqs)
     return 0;
   if (forced) return forced == 2;

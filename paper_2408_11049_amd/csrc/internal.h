@@ -56,6 +56,13 @@ constexpr int64_t kMaxTokStride = int64_t{1} << 28;  // elements
 // position plus a tile, q_len or the window arithmetic of a unit never wraps.
 constexpr int32_t kMaxPosition = INT32_MAX - 64;
 
+// A tuning override from the environment: its value when set within
+// [lo, hi], else 0.  Read on every call (well under a microsecond of host
+// time), so a process can change it between calls -- the tests sweep every
+// setting in one process; changing one while another thread is inside the
+// library is not supported (setenv is not thread-safe).
+int env_knob(const char* name, int lo, int hi);
+
 // Shape checks shared by the attention calls and their workspace queries:
 // MD_OK, MD_ERR_INVALID_ARG (malformed) or MD_ERR_UNSUPPORTED (beyond the
 // compiled limits).  Only sizes are read.

@@ -40,6 +40,12 @@ static int check_attn_shape(const md_attn_args* a) {
   return MD_OK;
 }
 
+int env_knob(const char* name, int lo, int hi) {
+  const char* e = getenv(name);
+  const int v = e ? atoi(e) : 0;
+  return (v >= lo && v <= hi) ? v : 0;
+}
+
 int check_attn_sizes(const md_attn_args* a) {
   const int shape = check_attn_shape(a);
   if (shape != MD_OK) return shape;
@@ -141,11 +147,7 @@ static void split_units(int64_t U, int64_t n_groups, int64_t slots, int64_t* n_c
 // per head -- no adjacent rows -- and keeps one head per workgroup.
 // MD_HEADS_PER_WG (1 or 2) overrides, for measurement.
 static int heads_per_workgroup(const md_attn_args* a, int mode, int64_t U, int64_t slots) {
-  static const int forced = [] {
-    const char* s = getenv("MD_HEADS_PER_WG");
-    const int v = s ? atoi(s) : 0;
-    return (v == 1 || v == 2) ? v : 0;
-  }();
+  const int forced = env_knob("MD_HEADS_PER_WG", 1, 2);
   if (a->num_kv_heads % 2) return 1;
   if (forced) return forced;
   if (mode == MD_MODE_DRAFT_INDEXED) return 1;

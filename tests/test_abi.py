@@ -263,6 +263,21 @@ def test_plan_pairs_heads_only_where_they_pay(lib, B, S, hp):
     assert got == _split_bytes(n_chunks, B * 5 * 32, 128), (got, n_chunks)
 
 
+def test_tuning_overrides_are_read_per_call(lib, monkeypatch):
+    """MD_HEADS_PER_WG changes the plan of the very next call (B = 16,
+    S = 16384: 64 head pairs in 4 chunks of 4096, or 128 single heads in 2
+    chunks), and unsetting it restores the default."""
+    a = good_args(num_seqs=16, num_kv_heads=8, num_q_heads=32, q_len=5, max_kv_len=16384,
+                  kv_stride_tok=8 * 128, kv_stride_blk=16384 * 8 * 128)
+    rows = 16 * 5 * 32
+    monkeypatch.delenv("MD_HEADS_PER_WG", raising=False)
+    assert lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1) == _split_bytes(4, rows, 128)
+    monkeypatch.setenv("MD_HEADS_PER_WG", "1")
+    assert lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1) == _split_bytes(2, rows, 128)
+    monkeypatch.setenv("MD_HEADS_PER_WG", "7")  # out of range: ignored
+    assert lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1) == _split_bytes(4, rows, 128)
+
+
 def test_workspace_draft_smaller_than_verify(lib):
     a = good_args(num_seqs=2, num_kv_heads=1, num_q_heads=8, q_len=4, max_kv_len=1 << 17,
                   kv_stride_tok=128, kv_stride_blk=(1 << 17) * 128)
