@@ -738,12 +738,13 @@ static hipError_t launch_p(const AttnParams& p, bool paged, int64_t n_blocks, hi
 // Instances: tiles in flight per wave (depth) x waves per SIMD (occupancy).
 // Two waves per SIMD fit the register file with one tile in flight and up to
 // two row tiles; a second tile in flight is built for the bf16 range modes
-// with up to two row tiles; everything else runs one tile, one wave per SIMD.
+// with up to three row tiles (MD_PREFETCH_DEPTH); everything else runs one
+// tile, one wave per SIMD.
 template <int D, bool BF16, int NT, bool IDX>
 static hipError_t launch_nt(const AttnParams& p, bool paged, int depth, int occ,
                             int64_t n_blocks, hipStream_t s) {
   if constexpr (BF16) {
-    if constexpr (!IDX && NT <= 2)
+    if constexpr (!IDX && NT <= 3)
       if (depth >= 2) return launch_p<D, BF16, NT, IDX, 2, 1>(p, paged, n_blocks, s);
     if constexpr (NT <= 2)
       if (occ >= 2) return launch_p<D, BF16, NT, IDX, 1, 2>(p, paged, n_blocks, s);
