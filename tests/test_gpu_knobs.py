@@ -4,7 +4,7 @@ instances), MD_OCCUPANCY (instances compiled for one or two waves per SIMD),
 MD_LPT (longest-first dispatch off, or on wherever a plan allows it) and
 MD_HEADS_PER_WG (one head or a head pair per workgroup).  The overrides are
 read on every call, so one process sweeps them all; each setting runs the
-same shapes: one, two and three 16-row tiles, the streaming and listed
+same shapes: one to four 16-row tiles, the streaming and listed
 drafts, a split range with its merge and a longest-first batch."""
 import functools
 
@@ -33,6 +33,8 @@ CASES = [
     ("listed_rows20", oracle.INDEXED, 3, 5, 8, 2, 128, [300, 77, 1030], 16, 0, 1, 200),
     ("verify_rows16", oracle.VERIFY, 2, 4, 8, 2, 128, [513, 64], 0, 0, 1, 0),
     ("draft_rows40", oracle.DRAFT, 2, 5, 16, 2, 128, [700, 450], 0, 16, 200, 0),
+    ("verify_rows40", oracle.VERIFY, 2, 5, 16, 2, 128, [700, 450], 16, 0, 1, 0),
+    ("verify_rows64", oracle.VERIFY, 1, 16, 4, 1, 64, [300], 0, 0, 1, 0),
     ("verify_split", oracle.VERIFY, 1, 4, 8, 2, 128, [5000], 16, 0, 1, 0),
     ("verify_b64_ragged", oracle.VERIFY, 64, 4, 8, 8, 64,
      [600 + (i * 977) % 5400 for i in range(64)], 16, 0, 1, 0),
