@@ -52,6 +52,9 @@ SMALL = [
     # one past the longest-first batch limit: head pairs, no ranking
     ("bf16_b257_pairs_no_lpt", 257, 4, 32, 8, 128, [100 + (i * 37) % 300 for i in range(257)],
      "bf16", 16, 16, 64),
+    # serving-sized batch of short requests: 8192 head pairs, far more workgroups than CUs
+    ("bf16_b2048_short_paged", 2048, 2, 8, 8, 64, [16 + (i * 53) % 600 for i in range(2048)],
+     "bf16", 16, 4, 64),
     # one long sequence: 8 units split into 32 chunks of 4096, merged
     ("bf16_b1_s128k_32chunks", 1, 5, 32, 8, 128, [131072], "bf16", 0, 64, 1984),
 ]
