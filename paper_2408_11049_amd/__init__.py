@@ -209,6 +209,29 @@ def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
+def _on_gpu(ref, **tensors):
+    """Every tensor a call hands to the kernels must live on ref's GPU: a host
+    or other-device address would reach them as a wild pointer, which the
+    library (it sees plain pointers) cannot tell from a good one."""
+    if not ref.is_cuda:
+        raise ValueError(f"tensors must be on a GPU, not {ref.device}")
+    for name, t in tensors.items():
+        if t is not None and t.device != ref.device:
+            raise ValueError(f"{name} is on {t.device}; the call runs on {ref.device}")
+
+
+def _ints(name, t, n):
+    """A device int32 vector the kernels read (or write) n entries of."""
+    import torch
+    if t.dtype != torch.int32 or not t.is_contiguous() or t.numel() < n:
+        raise ValueError(f"{name} must be contiguous int32 with at least {n} entries")
+
+
+def _torch():
+    import torch
+    return torch
+
+
 def _dtype_code(t):
     import torch
     if t.dtype == torch.float32:
@@ -226,8 +249,20 @@ def make_args(q, k, v, kv_lens, *, max_kv_len: Optional[int] = None, page_table=
         raise ValueError("q, k, v must be 4-D")
     B, L, Hq, d = q.shape
     paged = page_table is not None
+    _on_gpu(q, k=k, v=v, kv_lens=kv_lens, page_table=page_table, out=out, lse=lse,
+            workspace=workspace, err_word=err_word)
     if k.shape != v.shape or k.stride() != v.stride():
         raise ValueError("k and v must share shape and strides")
+    if k.shape[3] != d:
+        raise ValueError("k/v head_dim must equal q's")
+    _ints("kv_lens", kv_lens, B)
+    if out is not None and (out.shape != q.shape or out.dtype != q.dtype):
+        raise ValueError("o must have q's shape and dtype")
+    if lse is not None and (lse.dtype != _torch().float32 or not lse.is_contiguous()
+                            or lse.numel() < B * L * Hq):
+        raise ValueError("lse must be contiguous float32 [B, L, Hq]")
+    if paged and page_table.dim() == 2 and page_table.shape[0] < B:
+        raise ValueError("page_table must have a row per sequence")
     if k.stride(3) != 1:
         raise ValueError("the head_dim axis of k/v must be unit-stride")
     if not q.is_contiguous() or (out is not None and not out.is_contiguous()):
@@ -293,6 +328,9 @@ def _attention(mode, q, k, v, kv_lens, n_sink, window, *, max_kv_len=None, page_
         need = int(lib.md_workspace_bytes(ctypes.byref(a), mode, n_sink, window))
     if need and workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    _on_gpu(q, workspace=workspace, idx=idx, idx_len=idx_len)
+    if idx_len is not None:
+        _ints("idx_len", idx_len, q.shape[0])
     if workspace is not None:
         a.workspace = workspace.data_ptr()
         a.workspace_bytes = workspace.numel() * workspace.element_size()
@@ -337,10 +375,16 @@ def make_snapkv_args(q_obs, k, prompt_lens, *, max_prompt_len=None, page_table=N
     import torch
     B, n_obs, Hq, d = q_obs.shape
     paged = page_table is not None
+    _on_gpu(q_obs, k=k, prompt_lens=prompt_lens, page_table=page_table, votes=votes,
+            workspace=workspace)
     if k.stride(3) != 1 or not q_obs.is_contiguous():
         raise ValueError("q_obs must be contiguous and k unit-stride in head_dim")
-    if prompt_lens.dtype != torch.int32:
-        raise ValueError("prompt_lens must be int32")
+    if k.dim() != 4 or k.shape[3] != d:
+        raise ValueError("k must be 4-D with q_obs's head_dim")
+    _ints("prompt_lens", prompt_lens, B)
+    if votes is not None and (votes.dtype != torch.float32 or not votes.is_contiguous()
+                              or votes.dim() != 3 or votes.shape[:2] != (B, k.shape[2])):
+        raise ValueError("votes must be contiguous float32 [B, Hkv, stride]")
     if max_prompt_len is None:
         max_prompt_len = page_table.shape[1] * k.shape[1] if paged else k.shape[1]
     if B > 0 and not paged and k.shape[1] < max_prompt_len:
@@ -403,6 +447,13 @@ def md_snapkv_select(votes, prompt_lens, n_obs, budget, *, pool=5, idx=None, idx
     B, Hkv, stride = votes.shape
     if votes.dtype != torch.float32 or not votes.is_contiguous():
         raise ValueError("votes must be contiguous float32 [B, Hkv, stride]")
+    _on_gpu(votes, prompt_lens=prompt_lens, idx=idx, idx_len=idx_len)
+    _ints("prompt_lens", prompt_lens, B)
+    if idx is not None and (idx.dtype != torch.int32 or not idx.is_contiguous()
+                            or idx.shape[:2] != (B, Hkv) or idx.shape[2] < budget):
+        raise ValueError("idx must be contiguous int32 [B, Hkv, >= budget]")
+    if idx_len is not None:
+        _ints("idx_len", idx_len, B)
     if idx is None:
         idx = torch.full((B, Hkv, budget), -1, dtype=torch.int32, device=votes.device)
     if idx_len is None:
@@ -422,6 +473,13 @@ def md_merge_lse(o_parts, lse_parts, *, out_dtype=None, out=None, lse=None, stre
         raise ValueError("o_parts and lse_parts must be float32")
     if not o_parts.is_contiguous() or not lse_parts.is_contiguous():
         raise ValueError("o_parts and lse_parts must be contiguous")
+    _on_gpu(o_parts, lse_parts=lse_parts, out=out, lse=lse)
+    if tuple(lse_parts.shape) != (n_parts, n_rows):
+        raise ValueError("lse_parts must be [n_parts, n_rows]")
+    if out is not None and (tuple(out.shape) != (n_rows, d) or not out.is_contiguous()):
+        raise ValueError("out must be contiguous [n_rows, d]")
+    if lse is not None and (lse.dtype != torch.float32 or lse.numel() < n_rows):
+        raise ValueError("lse must be float32 [n_rows]")
     if out is None:
         out = torch.empty((n_rows, d), dtype=out_dtype or torch.float32, device=o_parts.device)
     if lse is None:
@@ -439,6 +497,7 @@ def make_kv_cache(k, v, *, num_seqs=None, page_table=None) -> MdKvCache:
     import torch
     if k.dim() != 4 or k.shape != v.shape or k.stride() != v.stride() or k.stride(3) != 1:
         raise ValueError("k and v must be 4-D with equal shapes and strides, head_dim unit-stride")
+    _on_gpu(k, v=v, page_table=page_table)
     c = MdKvCache()
     paged = page_table is not None
     c.num_seqs = int(num_seqs if num_seqs is not None else
@@ -452,6 +511,8 @@ def make_kv_cache(k, v, *, num_seqs=None, page_table=None) -> MdKvCache:
     if paged:
         if page_table.dtype != torch.int32 or not page_table.is_contiguous():
             raise ValueError("page_table must be contiguous int32 [B, max_pages]")
+        if page_table.dim() != 2 or page_table.shape[0] < c.num_seqs:
+            raise ValueError("page_table must have a row per sequence")
         c.page_size, c.max_pages_per_seq = k.shape[1], page_table.shape[1]
         c.num_pages = k.shape[0]
         c.page_table = page_table.data_ptr()
@@ -476,8 +537,11 @@ def md_kv_append(k, v, k_new, v_new, pos0, *, page_table=None, lens_out=None, st
     c = make_kv_cache(k, v, num_seqs=B, page_table=page_table)
     if B and (k_new.shape[2] != c.num_kv_heads or k_new.shape[3] != c.head_dim):
         raise ValueError("appended rows must have the cache's heads and head_dim")
+    _on_gpu(k, k_new=k_new, v_new=v_new, pos0=pos0, lens_out=lens_out)
+    _ints("pos0", pos0, B)
     if lens_out is None:
         lens_out = torch.empty((B,), dtype=torch.int32, device=k.device)
+    _ints("lens_out", lens_out, B)
     _check(lib.md_kv_append(ctypes.byref(c), n_new, _ptr(k_new), _ptr(v_new), _ptr(pos0),
                             _ptr(lens_out), _stream_handle(k, stream)))
     return lens_out
@@ -495,6 +559,13 @@ def md_greedy_accept(logits, draft, *, accepted=None, tokens=None, target=None,
         raise ValueError("logits must be contiguous [B, gamma + 1, vocab]")
     if draft.shape != (B, L - 1) or draft.dtype != torch.int32 or not draft.is_contiguous():
         raise ValueError("draft must be contiguous int32 [B, gamma]")
+    _on_gpu(logits, draft=draft, accepted=accepted, tokens=tokens, target=target,
+            workspace=workspace)
+    if accepted is not None:
+        _ints("accepted", accepted, B)
+    for name, t_ in (("tokens", tokens), ("target", target)):
+        if t_ is not None:
+            _ints(name, t_, B * L)
     dev = logits.device
     if accepted is None:
         accepted = torch.empty((B,), dtype=torch.int32, device=dev)
@@ -520,8 +591,11 @@ def md_kv_commit(lens, accepted, q_len, *, idx=None, ring_start=0, ring_len=None
     lib = load_library()
     B = lens.shape[0]
     Hkv, stride = (idx.shape[1], idx.shape[2]) if idx is not None else (0, 0)
-    if idx is not None and not idx.is_contiguous():
-        raise ValueError("idx must be contiguous [B, Hkv, stride]")
+    _on_gpu(lens, accepted=accepted, idx=idx)
+    _ints("lens", lens, B)
+    _ints("accepted", accepted, B)
+    if idx is not None and (not idx.is_contiguous() or idx.dtype != lens.dtype or idx.shape[0] < B):
+        raise ValueError("idx must be contiguous int32 [B, Hkv, stride]")
     if ring_len is None:
         ring_len = stride - ring_start
     _check(lib.md_kv_commit(B, q_len, _ptr(lens), _ptr(accepted), Hkv, _ptr(idx), stride,
@@ -537,10 +611,14 @@ def md_streaming_list(prompt_lens, num_kv_heads, n_sink, window, *, idx=None, id
     lib = load_library()
     B = prompt_lens.shape[0]
     dev = prompt_lens.device
+    _on_gpu(prompt_lens, idx=idx, idx_len=idx_len)
+    _ints("prompt_lens", prompt_lens, B)
     if idx is None:
         idx = torch.empty((B, num_kv_heads, n_sink + window), dtype=torch.int32, device=dev)
     if idx_len is None:
         idx_len = torch.empty((B,), dtype=torch.int32, device=dev)
+    _ints("idx", idx, B * num_kv_heads * (n_sink + window))
+    _ints("idx_len", idx_len, B)
     _check(lib.md_streaming_list(B, num_kv_heads, _ptr(prompt_lens), n_sink, window, _ptr(idx),
                                  _ptr(idx_len), _stream_handle(prompt_lens, stream)))
     return idx, idx_len
@@ -557,10 +635,16 @@ def md_kv_gather(dst_k, dst_v, src_k, src_v, idx, idx_len, src_lens, *, dst_page
     B, Hkv, stride = idx.shape
     if idx.dtype != torch.int32 or not idx.is_contiguous():
         raise ValueError("idx must be contiguous int32 [B, Hkv, stride]")
+    _on_gpu(idx, dst_k=dst_k, dst_v=dst_v, src_k=src_k, src_v=src_v, idx_len=idx_len,
+            src_lens=src_lens, dst_page_table=dst_page_table, src_page_table=src_page_table,
+            dst_lens=dst_lens)
+    _ints("idx_len", idx_len, B)
+    _ints("src_lens", src_lens, B)
     dst = make_kv_cache(dst_k, dst_v, num_seqs=B, page_table=dst_page_table)
     src = make_kv_cache(src_k, src_v, num_seqs=B, page_table=src_page_table)
     if dst_lens is None:
         dst_lens = torch.empty((B,), dtype=torch.int32, device=idx.device)
+    _ints("dst_lens", dst_lens, B)
     _check(lib.md_kv_gather(ctypes.byref(dst), ctypes.byref(src), _ptr(idx), stride,
                             _ptr(idx_len), _ptr(src_lens), _ptr(dst_lens),
                             _stream_handle(idx, stream)))
