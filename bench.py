@@ -22,7 +22,8 @@ the dominant kernel (the verify attention kernel, a single launch here), with
 the HBM traffic and MFMA utilisation read from the committed rocprofv3
 summaries under profiles/ (null when the kernel source changed since).
 `cpu_baseline` is the fp64 oracle timed on a bounded sample of the same
-workload on this host's cores (a reported baseline, not a target).  `detail`
+workload on this host's cores (a reported baseline, not a target).
+`inputs_sha256` identifies the seeded inputs that were timed.  `detail`
 adds the one-token and warm timings, the listed and gathered SnapKV-style
 drafts, the SnapKV selection, append, acceptance and commit, whole
 engine-shaped speculative steps (eager and as a HIP graph), the read ceiling
