@@ -83,9 +83,6 @@ __device__ __forceinline__ int real_token(const UnitGeom& u, int v) {
   return v < u.seg0 ? v : v - u.seg0 + u.seg1_start;
 }
 
-// IDX: the visible range is a per-(sequence, kv head) list of prompt positions
-// followed by the speculated tokens (the indexed draft); otherwise the causal
-// prefix (verify) or sinks then windows (draft).
 // Longest-processing-time-first dispatch.  Workgroups start roughly in
 // blockIdx order (round-robin over the XCDs), so with ragged lengths the
 // units that happen to start last set the finish time.  With p.lpt (one chunk
@@ -200,6 +197,12 @@ __device__ void check_contract(const P& p, const U& u, int b, int chunk, bool fi
   if (bits) atomicOr(reinterpret_cast<unsigned int*>(p.err), bits);
 }
 
+// The attention kernel.  D: head_dim; BF16: bf16 (else fp32) K/V/Q/O; NT:
+// 16-row query tiles per unit; PAGED: K/V through the page table; IDX: the
+// visible range is a per-(sequence, kv head) list of prompt positions
+// followed by the speculated tokens (the listed draft), else the causal
+// prefix (verify) or sinks then windows (draft); P: K/V tiles in flight per
+// wave; OCC: waves per SIMD the instance is compiled for.
 template <int D, bool BF16, int NT, bool PAGED, bool IDX, int P, int OCC>
 __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(OCC)))
 attn_partial_kernel(const AttnParams p) {
