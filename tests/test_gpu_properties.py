@@ -110,13 +110,15 @@ def test_batch_permutation_equivariance():
         assert np.array_equal(op, o[perm]) and np.array_equal(lp, l[perm])
 
 
+@pytest.mark.parametrize("n_parts", [7, 150], ids=["7_parts", "150_parts"])
 @pytest.mark.parametrize("d", [64, 128])
 @pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
-def test_merge_lse_against_oracle(d, out_dtype):
+def test_merge_lse_against_oracle(d, out_dtype, n_parts):
     """md_merge_lse == oracle merge, with empty (-inf) parts holding NaN O and
-    rows where every part is empty."""
-    rng = np.random.default_rng(d)
-    n_parts, n_rows = 7, 333
+    rows where every part is empty; 150 parts take each lane of the row's
+    wave through the part list more than once."""
+    rng = np.random.default_rng(d + n_parts)
+    n_rows = 333
     o_parts = rng.standard_normal((n_parts, n_rows, d)).astype(np.float32)
     lse_parts = (rng.standard_normal((n_parts, n_rows)) * 4).astype(np.float32)
     empty = rng.random((n_parts, n_rows)) < 0.3
