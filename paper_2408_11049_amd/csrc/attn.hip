@@ -220,7 +220,12 @@ attn_partial_kernel(const AttnParams p) {
   const int l16 = lane & 15;
   const int grp = lane >> 4;
 
-  const int chunk = blockIdx.x % p.n_chunks;
+  // Workgroups are numbered chunk-major: those that start together take the
+  // same chunk of different head groups, so they read neighbouring runs of
+  // the same token rows at the same time (measured on MI355X: split verify
+  // plans 1-5% faster than group-major; with one chunk the two coincide).
+  const int n_grp = static_cast<int>(gridDim.x) / p.n_chunks;
+  const int chunk = static_cast<int>(blockIdx.x) / n_grp;
   // The workgroup's head group: hp adjacent kv heads hk0 .. hk0+hp-1 of
   // sequence b.  Wave w serves kv head hk0 + w % hp and is slot w / hp of
   // that head's wph = kWaves / hp waves, which interleave its tiles.
@@ -232,7 +237,7 @@ attn_partial_kernel(const AttnParams p) {
     group_sel = lpt_group(p, static_cast<int>(blockIdx.x), reinterpret_cast<int*>(lds), hp_sel);
     if (group_sel < 0) return;
   } else {
-    group_sel = static_cast<int>(blockIdx.x / p.n_chunks);
+    group_sel = static_cast<int>(blockIdx.x) % n_grp;
   }
   const int hp = __builtin_amdgcn_readfirstlane(hp_sel);
   const int group = __builtin_amdgcn_readfirstlane(group_sel);
