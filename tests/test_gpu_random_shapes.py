@@ -14,7 +14,7 @@ from paper_2408_11049_amd import workloads as wl
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
-N_CASES = 32
+N_CASES = 96
 WORK_BOUND = 3e8  # sum of S_b * Hq * q_len * d per case: keeps the oracle to well under a second
 
 
