@@ -468,6 +468,24 @@ def test_streaming_list_args(lib):
     assert sl(0, 2, None, 4, 8, None, None, None) == md.MD_OK
 
 
+def test_readme_c_example_compiles():
+    """The C example in README.md uses the header's names and types as they
+    are (gcc, syntax and type checks only; read from stdin)."""
+    text = open(os.path.join(ROOT, "README.md")).read()
+    start = text.index("```c") + 4
+    snippet = text[start:text.index("```", start)]
+    body = snippet.replace('#include "magicdec.h"', "")
+    src = ('#include <stdio.h>\n#include <stdint.h>\n#include "magicdec.h"\n'
+           "int demo(int B, int gamma, int Hq, int Hkv, int64_t S_alloc, int S_max,\n"
+           "         const void* d_q, const void* d_k, const void* d_v, const int32_t* d_kv_lens,\n"
+           "         void* d_o, float* d_lse, void* d_ws, void* stream) {\n"
+           + body + "\n  return st;\n}\n")
+    r = subprocess.run(["gcc", "-std=c11", "-Wall", "-Werror", "-fsyntax-only", "-x", "c",
+                        "-I", os.path.join(ROOT, "include"), "-"],
+                       input=src, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+
+
 def test_struct_layouts_match_the_header(tmp_path):
     """Offsets and sizes of every C-ABI struct, as gcc lays them out from the
     header, equal the binding's ctypes mirrors."""
