@@ -18,17 +18,21 @@
  *     NULL is the null stream).  Buffers must stay alive and unmodified until
  *     the stream reaches the call.  Nothing synchronises with the host.
  *   - Calls are thread-safe and re-entrant.  The only global state is a
- *     per-device cache of the compute-unit count.  The MD_* tuning overrides
- *     (MD_PREFETCH_DEPTH, MD_OCCUPANCY, MD_LPT, MD_HEADS_PER_WG; for
- *     measurement) are read from the environment on every call; do not
- *     change them while another thread is inside the library.
+ *     per-device cache of the compute-unit count, a per-process call counter
+ *     and, for md_attn_noalloc only, one static scratch buffer per device.
+ *     The MD_* tuning overrides (MD_PREFETCH_DEPTH, MD_OCCUPANCY, MD_LPT,
+ *     MD_HEADS_PER_WG, MD_FUSED_MERGE, MD_SLOTS_SCALE; for measurement) are
+ *     read from the environment on every call; do not change them while
+ *     another thread is inside the library.
  *   - Errors are return codes (md_status).  Argument errors are detected on
  *     the host before any HIP call, so a failed call has launched nothing.
  *   - Device-side contract violations leave memory in bounds but results
  *     meaningless: kv_lens[b] < q_len yields rows with an empty key set
  *     (O = 0, lse = -inf); kv_lens[b] is clamped to max_kv_len; page ids
- *     outside [0, num_pages) are never dereferenced (those tokens read as
- *     zero).  They are reported only to a caller that passes an error word
+ *     outside [0, num_pages) are never dereferenced (the loads of those
+ *     tokens are redirected to element 0 of k and v, and the outputs of the
+ *     rows that see them are unspecified).  They are reported only to a
+ *     caller that passes an error word
  *     (md_attn_args.err_word, for debugging): each attention call then ORs
  *     into it MD_ERRW_SHORT_LEN if some kv_lens[b] < q_len (negative
  *     included), MD_ERRW_LONG_LEN if some kv_lens[b] > max_kv_len, and
@@ -119,7 +123,8 @@ typedef struct {
   int32_t max_kv_len;         /* HOST bound on every kv_lens[b]; sizes the grid */
   void* o;
   float* lse;
-  void* workspace;            /* device scratch, >= md_workspace_bytes(), 256-byte aligned */
+  void* workspace;            /* device scratch, >= md_workspace_bytes(), 256-byte aligned;
+                                 any contents (nothing in it needs clearing) */
   size_t workspace_bytes;
   int32_t* err_word;          /* device int32 or NULL: contract checks (md_err_bits, above) */
 } md_attn_args;
@@ -189,7 +194,10 @@ int md_merge_lse(int32_t n_parts, int64_t n_rows, int32_t head_dim, int32_t out_
 
 /*
  * Workspace bytes an attention call with these arguments needs (0 when the
- * call runs as a single pass).  mode is MD_MODE_VERIFY or MD_MODE_DRAFT;
+ * call runs as a single pass).  A split-range call keeps there, per head
+ * group, an arrival counter tagged with the call, then every chunk's partial
+ * O and lse (the split-KV identity, Sec. 2); whatever the buffer held before
+ * is never mistaken for this call's state, so it needs no clearing.  mode is MD_MODE_VERIFY or MD_MODE_DRAFT;
  * n_sink and window are used for MD_MODE_DRAFT only.  Pure host arithmetic on the sizes plus the
  * current device's compute-unit count (256 if no device is visible);
  * pointers in `a` are not read.  Returns 0 for malformed arguments too:
@@ -393,8 +401,8 @@ int md_streaming_list(int32_t num_seqs, int32_t num_kv_heads, const int32_t* pro
  *   src_lens   device int32 [B]: how many positions of src are valid
  *   dst_lens   device int32 [B] out, or NULL: set to n_b; must not overlap
  *              idx_len or src_lens
- * Values move bit for bit.  Rows past dst's capacity (or its table), and
- * pages outside [0, num_pages), are not written.
+ * Values move bit for bit.  Rows on pages outside [0, num_pages) are not
+ * written.
  * Drafting over dst: md_kv_append the step's rows at position dst_lens[b] of
  * dst (as of the full cache), then md_verify_attn over dst with kv_lens =
  * dst_lens + q_len; md_kv_commit then advances dst_lens like the full
@@ -404,8 +412,9 @@ int md_streaming_list(int32_t num_seqs, int32_t num_kv_heads, const int32_t* pro
  * row, which takes part in that attention (score 0, value 0) where
  * md_draft_attn_indexed skips the entry.
  * Errors: MD_ERR_INVALID_ARG for NULL or misaligned pointers, a malformed or
- * mismatched cache, idx_stride < 1, dst_lens overlapping idx_len or
- * src_lens; MD_ERR_HIP.
+ * mismatched cache, idx_stride < 1, a destination that holds fewer than
+ * idx_stride rows per sequence (capacity, or max_pages_per_seq * page_size),
+ * dst_lens overlapping idx_len or src_lens; MD_ERR_HIP.
  */
 int md_kv_gather(const md_kv_cache* dst, const md_kv_cache* src, const int32_t* idx,
                  int32_t idx_stride, const int32_t* idx_len, const int32_t* src_lens,

@@ -14,6 +14,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "magicdec.h"
+
 #ifdef __cplusplus
 extern "C" {
 #endif
@@ -31,6 +33,21 @@ int md_bench_copy(void* dst, const void* src, size_t bytes, void* stream);
 /* Fill `bytes` of `buf` with the 32-bit `value`; writing a buffer larger than
  * the last-level caches evicts the KV cache before a cold-cache timing. */
 int md_bench_fill(void* buf, size_t bytes, uint32_t value, void* stream);
+
+/* md_verify_attn (mode 0) or md_draft_attn (mode 1) on `a`, with each
+ * workgroup of the attention launch recording four readings of the GPU's
+ * constant-rate wall clock (100 MHz on MI355X) into stamps[4 w .. 4 w + 3]:
+ * its start, the end of its first K/V tile, the end of its main loop and its
+ * end (after the split-KV merge, when it is the workgroup that merges).
+ * `*n_workgroups` receives the launch's workgroup count (also on
+ * MD_ERR_INVALID_ARG for a short `stamps`, so a caller can size it; a
+ * longest-first launch's surplus workgroups leave their entries unwritten).
+ * stamps: device uint64 [stamps_len], 8-byte aligned.  Errors as the
+ * attention call, and MD_ERR_INVALID_ARG for NULL n_workgroups, a bad mode
+ * or stamps_len < 4 * workgroups. */
+int md_bench_attn_stamps(const md_attn_args* a, int32_t mode, int32_t n_sink, int32_t window,
+                         uint64_t* stamps, int64_t stamps_len, int64_t* n_workgroups,
+                         void* stream);
 
 #ifdef __cplusplus
 }

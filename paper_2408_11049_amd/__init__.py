@@ -44,7 +44,7 @@ EXPORTED = ["md_verify_attn", "md_draft_attn", "md_draft_attn_indexed", "md_merg
             "md_streaming_list", "md_kv_gather", "md_sd_expected_tokens", "md_sd_latency_ratio",
             "md_sd_best_gamma", "md_sd_alpha_from_omega",
             "md_status_str", "md_last_hip_error", "md_attn_args_size",
-            "md_bench_stream_read", "md_bench_copy", "md_bench_fill"]
+            "md_bench_stream_read", "md_bench_copy", "md_bench_fill", "md_bench_attn_stamps"]
 
 
 class MdAttnArgs(ctypes.Structure):
@@ -166,6 +166,8 @@ def load_library(path: str = LIB_PATH):
     lib.md_bench_copy.restype = ctypes.c_int
     lib.md_bench_fill.argtypes = [vp, sz, ctypes.c_uint32, vp]
     lib.md_bench_fill.restype = ctypes.c_int
+    lib.md_bench_attn_stamps.argtypes = [args_p, i32, i32, i32, vp, i64, ctypes.POINTER(i64), vp]
+    lib.md_bench_attn_stamps.restype = ctypes.c_int
     if lib.md_attn_args_size() != ctypes.sizeof(MdAttnArgs):
         raise RuntimeError("md_attn_args layout mismatch between the binding and the library")
     _lib = lib
@@ -366,6 +368,35 @@ def md_draft_attn_indexed(q, k, v, kv_lens, idx, idx_len, **kw):
     if idx.dim() != 3 or not idx.is_contiguous() or idx.shape[:2] != (q.shape[0], k.shape[2]):
         raise ValueError("idx must be contiguous [B, Hkv, stride]")
     return _attention(MD_MODE_DRAFT_INDEXED, q, k, v, kv_lens, 0, 1, idx=idx, idx_len=idx_len, **kw)
+
+
+def md_bench_attn_stamps(mode, q, k, v, kv_lens, n_sink=0, window=1, *, max_kv_len=None,
+                         page_table=None, out=None, workspace=None, stream=None):
+    """Measurement: md_verify_attn (mode 0) or md_draft_attn (mode 1) with
+    every workgroup recording four wall-clock stamps (start, first tile done,
+    main loop done, end).  Returns (o, stamps int64 [workgroups, 4]) -- raw
+    readings of the GPU's constant-rate clock (include/magicdec_bench.h)."""
+    import torch
+    lib = load_library()
+    if out is None:
+        out = torch.empty_like(q)
+    a = make_args(q, k, v, kv_lens, max_kv_len=max_kv_len, page_table=page_table, out=out)
+    need = int(lib.md_workspace_bytes(ctypes.byref(a), mode, n_sink, window))
+    if need and workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    if workspace is not None:
+        _on_gpu(q, workspace=workspace)
+        a.workspace, a.workspace_bytes = workspace.data_ptr(), workspace.numel()
+    n = ctypes.c_int64(0)
+    s = _stream_handle(q, stream)
+    st = lib.md_bench_attn_stamps(ctypes.byref(a), mode, n_sink, window, None, 0, ctypes.byref(n), s)
+    if st != MD_ERR_INVALID_ARG or n.value < 0:
+        _check(st)
+    stamps = torch.zeros((max(n.value, 1), 4), dtype=torch.int64, device=q.device)
+    _check(lib.md_bench_attn_stamps(ctypes.byref(a), mode, n_sink, window,
+                                    ctypes.c_void_p(stamps.data_ptr()), stamps.numel(),
+                                    ctypes.byref(n), s))
+    return out, stamps[: n.value]
 
 
 def make_snapkv_args(q_obs, k, prompt_lens, *, max_prompt_len=None, page_table=None,

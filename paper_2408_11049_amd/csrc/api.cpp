@@ -82,8 +82,44 @@ int longest_first(int mode, int n_chunks, int num_seqs, int max_kv_len) {
   return max_kv_len >= kLptMinLen;
 }
 
+// A fresh tag per attention call (1 .. 2^48 - 1; a process would need
+// centuries of calls to wrap it): it marks the arrival counters of that
+// call's split plan (see attn.hip).
+unsigned long long next_call_tag() {
+  static std::atomic<unsigned long long> seq{0};
+  constexpr unsigned long long kMask = (1ull << 48) - 1;
+  unsigned long long t = (seq.fetch_add(1, std::memory_order_relaxed) + 1) & kMask;
+  while (t == 0) t = (seq.fetch_add(1, std::memory_order_relaxed) + 1) & kMask;
+  return t;
+}
+
+// Workgroups of an attention launch: a head group per chunk, or, for a
+// longest-first launch that may pair heads, one per unit.
+int64_t grid_size(const Plan& pl, int lpt) {
+  return (lpt && pl.hp == 2) ? pl.n_units : pl.n_groups * pl.n_chunks;
+}
+
+}  // namespace
+
+int64_t attn_grid_size(const md_attn_args* a, int mode, int n_sink, int window) {
+  const Plan pl = make_plan(a, mode, n_sink, window, device_cu_count());
+  return grid_size(pl, longest_first(mode, pl.n_chunks, a->num_seqs, a->max_kv_len));
+}
+
+// The attention entry points.  `workspace`/`workspace_bytes` override the
+// caller's workspace in `a` (the entry point without allocation passes the
+// library's own buffer); `stamps` is the measurement hook (NULL normally).
 int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void* stream,
-                  const int32_t* idx = nullptr, const int32_t* idx_len = nullptr) {
+                  const int32_t* idx, const int32_t* idx_len, void* workspace,
+                  size_t workspace_bytes, unsigned long long* stamps) {
+  md_attn_args local;
+  if (a && workspace) {
+    local = *a;
+    local.workspace = workspace;
+    local.workspace_bytes = workspace_bytes;
+    a = &local;
+  }
+  if (a) workspace = a->workspace;
   int st = validate_attn(a, mode, n_sink, window);
   if (st != MD_OK) return st;
   if (a->num_seqs == 0) return MD_OK;
@@ -133,36 +169,44 @@ int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void*
   p.lpt = longest_first(mode, pl.n_chunks, a->num_seqs, a->max_kv_len);
   p.hp = pl.hp;
   p.err = a->err_word;
-  int64_t n_blocks = pl.n_groups * pl.n_chunks;
+  const int64_t n_blocks = grid_size(pl, p.lpt);
   if (p.lpt && pl.hp == 2) {
     // One workgroup per unit; the kernel pairs heads (and idles the surplus
     // half) only when longest-first can still balance the pairs.
     p.hp = 1;
     p.hp_auto = 1;
     p.slots = num_cus > 0 ? num_cus : 256;
-    n_blocks = pl.n_units;
   }
   p.o = a->o;
   p.lse = a->lse;
   p.n_rows = pl.n_rows;
   if (pl.n_chunks > 1) {
-    p.part_o = static_cast<float*>(a->workspace);
-    p.part_lse = reinterpret_cast<float*>(static_cast<unsigned char*>(a->workspace) + pl.part_o_bytes);
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    p.counters = reinterpret_cast<unsigned long long*>(ws);
+    p.part_o = reinterpret_cast<float*>(ws + pl.counter_bytes);
+    p.part_lse = reinterpret_cast<float*>(ws + pl.counter_bytes + pl.part_o_bytes);
+    p.tag = next_call_tag();
+    // The chunks merge in a second launch by default.  MD_FUSED_MERGE = 1
+    // merges them inside the attention launch instead, in the last workgroup
+    // of each head group to finish: measured on MI355X, same process, that
+    // was 1-4 us slower per call (the second launch follows the first with
+    // no gap on the stream, and the device-scope fences around the arrival
+    // counters cost more than the launch saves), so it stays opt-in.
+    p.merge_launch = !env_knob("MD_FUSED_MERGE", 1, 1);
   }
+  p.stamps = stamps;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int depth = prefetch_depth(pl.NT, mode);
   hipError_t e = launch_attn_partial(p, a->head_dim, bf16, pl.NT, paged, depth,
                                      occupancy(pl.NT, depth, mode), n_blocks, s);
   if (e != hipSuccess) return hip_fail(e);
-  if (pl.n_chunks > 1) {
+  if (pl.n_chunks > 1 && p.merge_launch) {
     e = launch_merge_lse(pl.n_chunks, pl.n_rows, a->head_dim, bf16, p.part_o, p.part_lse, a->o,
                          a->lse, s);
     if (e != hipSuccess) return hip_fail(e);
   }
   return MD_OK;
 }
-
-}  // namespace
 
 int device_cu_count() {
   static std::atomic<int> cache[64];
@@ -188,16 +232,33 @@ int device_cu_count() {
 extern "C" {
 
 int md_verify_attn(const md_attn_args* a, void* stream) {
-  return md::run_attention(a, MD_MODE_VERIFY, 0, 1, stream);
+  return md::run_attention(a, MD_MODE_VERIFY, 0, 1, stream, nullptr, nullptr, nullptr, 0,
+                           nullptr);
 }
 
 int md_draft_attn(const md_attn_args* a, int32_t n_sink, int32_t window, void* stream) {
-  return md::run_attention(a, MD_MODE_DRAFT, n_sink, window, stream);
+  return md::run_attention(a, MD_MODE_DRAFT, n_sink, window, stream, nullptr, nullptr, nullptr,
+                           0, nullptr);
 }
 
 int md_draft_attn_indexed(const md_attn_args* a, const int32_t* idx, const int32_t* idx_len,
                           int32_t idx_stride, void* stream) {
-  return md::run_attention(a, MD_MODE_DRAFT_INDEXED, 0, idx_stride, stream, idx, idx_len);
+  return md::run_attention(a, MD_MODE_DRAFT_INDEXED, 0, idx_stride, stream, idx, idx_len,
+                           nullptr, 0, nullptr);
+}
+
+int md_bench_attn_stamps(const md_attn_args* a, int32_t mode, int32_t n_sink, int32_t window,
+                         uint64_t* stamps, int64_t stamps_len, int64_t* n_workgroups,
+                         void* stream) {
+  if (!a || !n_workgroups || (mode != MD_MODE_VERIFY && mode != MD_MODE_DRAFT))
+    return MD_ERR_INVALID_ARG;
+  const int st = md::validate_attn(a, mode, n_sink, window);
+  if (st != MD_OK) return st;
+  *n_workgroups = md::attn_grid_size(a, mode, n_sink, window);
+  if (!stamps || (reinterpret_cast<uintptr_t>(stamps) & 7u) || stamps_len < 4 * *n_workgroups)
+    return MD_ERR_INVALID_ARG;
+  return md::run_attention(a, mode, n_sink, window, stream, nullptr, nullptr, nullptr, 0,
+                           reinterpret_cast<unsigned long long*>(stamps));
 }
 
 int md_merge_lse(int32_t n_parts, int64_t n_rows, int32_t head_dim, int32_t out_dtype,
@@ -363,6 +424,12 @@ int md_kv_gather(const md_kv_cache* dst, const md_kv_cache* src, const int32_t* 
   if (dst->num_seqs != src->num_seqs || dst->num_kv_heads != src->num_kv_heads ||
       dst->head_dim != src->head_dim || dst->dtype != src->dtype || idx_stride < 1)
     return MD_ERR_INVALID_ARG;
+  // Every list entry has a destination row: a shorter cache would drop rows
+  // while dst_lens still counted them.
+  const int64_t dst_rows = dst->page_size
+                               ? static_cast<int64_t>(dst->max_pages_per_seq) * dst->page_size
+                               : static_cast<int64_t>(dst->capacity);
+  if (dst_rows < idx_stride) return MD_ERR_INVALID_ARG;
   if (dst->num_seqs == 0) return MD_OK;
   if (!dst->k || !dst->v || !src->k || !src->v || !idx || !idx_len || !src_lens)
     return MD_ERR_INVALID_ARG;

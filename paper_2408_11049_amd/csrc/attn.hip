@@ -35,6 +35,15 @@
 
 namespace md {
 
+// Device-scope release / acquire around a split plan's arrival counter.
+#ifndef MD_PARTIAL_RELEASE
+// s_waitcnt vmcnt(0) (expcnt and lgkmcnt left at their maxima): this wave's
+// stores are complete.
+#define MD_PARTIAL_WAVE_DONE() __builtin_amdgcn_s_waitcnt(0x0F70)
+#define MD_PARTIAL_RELEASE() __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent")
+#define MD_PARTIAL_ACQUIRE() __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent")
+#endif
+
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -219,6 +228,13 @@ attn_partial_kernel(const AttnParams p) {
   const int wave = threadIdx.x >> 6;
   const int l16 = lane & 15;
   const int grp = lane >> 4;
+  // Measurement stamps (p.stamps, normally NULL): wall clock of workgroup
+  // start, first tile done, main loop done and end, by its first lane.
+  auto stamp = [&](int k) {
+    if (p.stamps != nullptr && threadIdx.x == 0)
+      p.stamps[static_cast<int64_t>(blockIdx.x) * 4 + k] = __builtin_amdgcn_s_memrealtime();
+  };
+  stamp(0);
 
   // Workgroups are numbered chunk-major: those that start together take the
   // same chunk of different head groups, so they read neighbouring runs of
@@ -304,10 +320,13 @@ attn_partial_kernel(const AttnParams p) {
 
   // Element offset of real token t given its page id (paged).  A token that
   // must not be read (past the chunk, or a page id outside the pool) is
-  // redirected to element 0 of the tensor -- always in bounds -- and its
-  // value is discarded: scores are masked, V rows are zeroed.  Loads are
-  // therefore never under divergent control flow, which lets the compiler
-  // keep every prefetched tile in flight across loop iterations.
+  // redirected to element 0 of the tensor -- always in bounds.  Past the
+  // chunk its value is discarded (the score is masked, the V row zeroed);
+  // a page id outside the pool is a caller's contract violation, reported
+  // through the error word only, and the rows that see the token get
+  // unspecified results.  Loads are therefore never under divergent control
+  // flow, which lets the compiler keep every prefetched tile in flight
+  // across loop iterations.
   auto tok_offset = [&](int t, int pid, bool& ok) -> int64_t {
     if (PAGED) {
       ok = ok && pid >= 0 && pid < p.num_pages;
@@ -388,7 +407,7 @@ attn_partial_kernel(const AttnParams p) {
         const bool pg_ok = pid >= 0 && pid < p.num_pages;
         base = pg_ok ? static_cast<int64_t>(pid) * p.s_blk +
                            static_cast<int64_t>((v0 + n * SH::TPI) & pmask) * p.s_tok + head_off
-                     : 0;  // a page outside the pool: element 0, the row reads as zero
+                     : 0;  // a page outside the pool: element 0, in bounds
         if (!pg_ok) T.ok &= ~(1u << n);
       } else {
         base = static_cast<int64_t>(b) * p.s_blk + static_cast<int64_t>(v0 + n * SH::TPI) * p.s_tok +
@@ -639,7 +658,9 @@ attn_partial_kernel(const AttnParams p) {
   for (int base = wslot; base < n_tiles; base += P * wph) {
 #pragma unroll
     for (int s = 0; s < P; ++s) process(ring[s], base + s * wph, ref_ring[s]);
+    if (p.stamps != nullptr && base == wslot) stamp(1);
   }
+  stamp(2);
 
   // ---- row sums: add the 4 lanes that share a row
   for (int rt = 0; rt < NT; ++rt) {
@@ -682,6 +703,19 @@ attn_partial_kernel(const AttnParams p) {
 
   const bool direct = p.n_chunks == 1;
   const int tid = threadIdx.x;
+  // Final O (8 channels from c0 of row row_g, in the input dtype) and lse.
+  auto store_out = [&](int64_t row_g, int c0, const float* o8, float lse) {
+    if constexpr (BF16) {
+      *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(p.o) + row_g * D + c0) =
+          u32x4{pack_bf16x2(o8[0], o8[1]), pack_bf16x2(o8[2], o8[3]),
+                pack_bf16x2(o8[4], o8[5]), pack_bf16x2(o8[6], o8[7])};
+    } else {
+      float* op = static_cast<float*>(p.o) + row_g * D + c0;
+      *reinterpret_cast<f32x4*>(op) = f32x4{o8[0], o8[1], o8[2], o8[3]};
+      *reinterpret_cast<f32x4*>(op + 4) = f32x4{o8[4], o8[5], o8[6], o8[7]};
+    }
+    if (p.lse && c0 == 0) p.lse[row_g] = lse;
+  };
   constexpr int kGroupsPerRow = D / 8;
   constexpr int kItemsPerUnit = 16 * kGroupsPerRow;  // (row of a row tile, 8 channels)
   for (int rt = 0; rt < NT; ++rt) {
@@ -708,16 +742,7 @@ attn_partial_kernel(const AttnParams p) {
       row_stats(hs, r, M, Lt);
       const float lse = (Lt > 0.f) ? (M + fast_log2(Lt)) * 0.69314718055994530942f : -INFINITY;
       if (direct) {
-        if constexpr (BF16) {
-          *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(p.o) + row_g * D + c0) =
-              u32x4{pack_bf16x2(o8[0], o8[1]), pack_bf16x2(o8[2], o8[3]),
-                    pack_bf16x2(o8[4], o8[5]), pack_bf16x2(o8[6], o8[7])};
-        } else {
-          float* op = static_cast<float*>(p.o) + row_g * D + c0;
-          *reinterpret_cast<f32x4*>(op) = f32x4{o8[0], o8[1], o8[2], o8[3]};
-          *reinterpret_cast<f32x4*>(op + 4) = f32x4{o8[4], o8[5], o8[6], o8[7]};
-        }
-        if (p.lse && c0 == 0) p.lse[row_g] = lse;
+        store_out(row_g, c0, o8, lse);
       } else {
         float* op = p.part_o + (static_cast<int64_t>(chunk) * p.n_rows + row_g) * D + c0;
         *reinterpret_cast<f32x4*>(op) = f32x4{o8[0], o8[1], o8[2], o8[3]};
@@ -727,6 +752,82 @@ attn_partial_kernel(const AttnParams p) {
     }
     __syncthreads();
   }
+
+  // ---- split range: the last workgroup of the head group to finish merges
+  // the chunks' partials by log-sum-exp (the split-KV identity), so no
+  // second launch is needed.  Every chunk's workgroup arrives once (an empty
+  // chunk with lse = -inf), so the group's n_chunks-th arrival sees every
+  // partial.  The counter carries the call's 48-bit tag above its 16-bit
+  // arrival count: a value from any other call (or uninitialised memory)
+  // counts as zero arrivals, so the workspace needs no clearing; the last
+  // arrival resets it to 0.
+  if (!direct && !p.merge_launch) {
+    // Every wave waits until its partial stores are performed at the L2
+    // (vmcnt 0), the barrier lines the waves up, and one device-scope release
+    // fence (an L2 write-back on gfx950) then publishes them all before the
+    // arrival.  One fence per workgroup instead of one per wave: device-scope
+    // fences serialise in the L2, and four per workgroup at the end of a
+    // launch cost more than the separate merge launch they replace.
+    MD_PARTIAL_WAVE_DONE();
+    __syncthreads();
+    int* is_last = reinterpret_cast<int*>(lds);
+    if (tid == 0) {
+      MD_PARTIAL_RELEASE();
+      unsigned long long* ctr = p.counters + group;
+      unsigned long long cur = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      unsigned long long next;
+      do {
+        const unsigned long long seen = (cur >> 16) == p.tag ? (cur & 0xffffull) : 0ull;
+        next = (p.tag << 16) | (seen + 1);
+      } while (!__hip_atomic_compare_exchange_weak(ctr, &cur, next, __ATOMIC_RELAXED,
+                                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+      const int last = (next & 0xffffull) == static_cast<unsigned long long>(p.n_chunks);
+      if (last) __hip_atomic_store(ctr, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (last) MD_PARTIAL_ACQUIRE();  // the other chunks' partials, as their workgroups left them
+      *is_last = last;
+    }
+    __syncthreads();
+    if (*is_last) {
+      constexpr float kLog2e = 1.44269504088896340736f;
+      constexpr float kLn2 = 0.69314718055994530942f;
+      const int items_per_unit = p.R * kGroupsPerRow;
+      for (int item = tid; item < hp * items_per_unit; item += kWaves * 64) {
+        const int hs = item / items_per_unit;
+        const int r = (item % items_per_unit) / kGroupsPerRow;
+        const int c0 = (item % kGroupsPerRow) * 8;
+        const int i = r / p.G, h = (hk0 + hs) * p.G + r % p.G;
+        const int64_t row_g = (static_cast<int64_t>(b) * L + i) * p.Hq + h;
+        const float* lp = p.part_lse + row_g;
+        float mx = -INFINITY;
+        for (int k = 0; k < p.n_chunks; ++k) mx = fmaxf(mx, lp[static_cast<int64_t>(k) * p.n_rows]);
+        float o8[8];
+        for (int j = 0; j < 8; ++j) o8[j] = 0.f;
+        float lse = -INFINITY;
+        if (mx != -INFINITY) {
+          float tot = 0.f;
+          for (int k = 0; k < p.n_chunks; ++k) {
+            const float l = lp[static_cast<int64_t>(k) * p.n_rows];
+            if (l != -INFINITY) tot += fast_exp2((l - mx) * kLog2e);
+          }
+          lse = mx + fast_log2(tot) * kLn2;
+          for (int k = 0; k < p.n_chunks; ++k) {
+            const float l = lp[static_cast<int64_t>(k) * p.n_rows];
+            if (l == -INFINITY) continue;  // an empty chunk: its O is not read
+            const float wk = fast_exp2((l - lse) * kLog2e);
+            const float* op = p.part_o + (static_cast<int64_t>(k) * p.n_rows + row_g) * D + c0;
+            const f32x4 x0 = *reinterpret_cast<const f32x4*>(op);
+            const f32x4 x1 = *reinterpret_cast<const f32x4*>(op + 4);
+            for (int j = 0; j < 4; ++j) {
+              o8[j] += wk * x0[j];
+              o8[4 + j] += wk * x1[j];
+            }
+          }
+        }
+        store_out(row_g, c0, o8, lse);
+      }
+    }
+  }
+  stamp(3);
 }
 
 // ---------------------------------------------------------------------------

@@ -27,6 +27,7 @@ constexpr int kTile = 32;            // tokens per wave iteration
 constexpr int kMinChunkTokens = 1024;  // every wave gets >= 8 tiles of a chunk
 constexpr int kMaxRows = 64;         // G*L bound: at most four 16-row tiles
 constexpr int kPairMinChunkTokens = 4096;  // head pairs on split ranges: chunks at least this long
+constexpr int kMaxChunks = 65535;    // a split plan's arrival count fits 16 bits
 // Longest-first dispatch (single-chunk verify plans): every workgroup ranks
 // the sequences by length, so it is kept to small batches of long caches.
 constexpr int kLptMaxSeqs = 256;
@@ -43,8 +44,10 @@ struct Plan {
   int64_t n_units = 0;   // B * Hkv
   int32_t hp = 1;        // units (adjacent kv heads) per workgroup
   int64_t n_groups = 0;  // n_units / hp; the grid is n_groups * n_chunks
-  size_t part_o_bytes = 0;   // workspace: [n_chunks][n_rows][d] fp32 partial O
-  size_t part_lse_bytes = 0; // workspace: [n_chunks][n_rows] fp32 partial lse
+  // Workspace of a split plan, in this order (each part 256-byte aligned):
+  size_t counter_bytes = 0;  // [n_groups] uint64 arrival counters (tagged; never cleared)
+  size_t part_o_bytes = 0;   // [n_chunks][n_rows][d] fp32 partial O
+  size_t part_lse_bytes = 0; // [n_chunks][n_rows] fp32 partial lse
   size_t workspace_bytes = 0;
 };
 
@@ -111,6 +114,17 @@ int validate_kv_cache(const md_kv_cache* c, int32_t n_new);
 // Compute units of the current device (cached per device); 256 when no
 // device is visible, so sizes stay defined on a host without a GPU.
 int device_cu_count();
+
+// The attention calls behind md_verify_attn, md_draft_attn and
+// md_draft_attn_indexed (api.cpp).  A non-NULL `workspace` replaces the one
+// in `a`; `stamps` (measurement, normally NULL) receives four wall-clock
+// stamps per workgroup.
+int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void* stream,
+                  const int32_t* idx, const int32_t* idx_len, void* workspace,
+                  size_t workspace_bytes, unsigned long long* stamps);
+
+// Workgroups the attention launch for these (validated) arguments uses.
+int64_t attn_grid_size(const md_attn_args* a, int mode, int n_sink, int window);
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 

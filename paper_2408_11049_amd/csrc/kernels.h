@@ -31,6 +31,17 @@ struct AttnParams {
   float* lse;                 // final lse or nullptr (single chunk)
   float* part_o;              // [n_chunks][n_rows][d] (several chunks)
   float* part_lse;            // [n_chunks][n_rows]
+  // Several chunks: one arrival counter per head group; the last workgroup
+  // of a group to finish merges its chunks (see attn.hip).  A counter holds
+  // (tag << 16) | arrivals, so a value left by anything but this call reads
+  // as zero arrivals; the last arrival resets it to 0.  merge_launch = 1
+  // (the default) leaves the merge to a separate launch instead.
+  unsigned long long* counters;
+  unsigned long long tag;     // per call: nonzero, below 2^48
+  int32_t merge_launch;
+  // Measurement only (NULL in normal use): per workgroup, four wall-clock
+  // stamps (start, first K/V tile staged, main loop done, end).
+  unsigned long long* stamps;
   int64_t n_rows;
   int32_t num_seqs;           // B
   int32_t lpt;                // 1: workgroups take sequences longest first (see attn.hip)

@@ -85,6 +85,9 @@ int validate_attn(const md_attn_args* a, int mode, int n_sink, int window) {
   const int sizes = check_attn_sizes(a);
   if (sizes != MD_OK) return sizes;
   if (a->num_seqs == 0) return MD_OK;  // nothing will be read or written
+  const int num_cus = device_cu_count();
+  Plan p = make_plan(a, mode, n_sink, window, num_cus);
+  if (p.n_chunks > kMaxChunks) return MD_ERR_UNSUPPORTED;  // unreachable below ~16k compute units
 
   if (!a->q || !a->k || !a->v || !a->o || !a->kv_lens) return MD_ERR_INVALID_ARG;
   if (paged != (a->page_table != nullptr)) return MD_ERR_INVALID_ARG;
@@ -102,8 +105,6 @@ int validate_attn(const md_attn_args* a, int mode, int n_sink, int window) {
   // A token row must not overlap the next head's row.
   if (a->num_kv_heads > 1 && a->kv_stride_head < a->head_dim) return MD_ERR_INVALID_ARG;
 
-  const int num_cus = device_cu_count();
-  Plan p = make_plan(a, mode, n_sink, window, num_cus);
   if (p.workspace_bytes) {
     if (!a->workspace || a->workspace_bytes < p.workspace_bytes) return MD_ERR_WORKSPACE;
     if (reinterpret_cast<uintptr_t>(a->workspace) & 255u) return MD_ERR_WORKSPACE;
@@ -177,7 +178,9 @@ Plan make_plan(const md_attn_args* a, int mode, int n_sink, int window, int num_
   // measured on MI355X, splitting further -- two or four workgroups per
   // compute unit -- was 5-15% slower on long caches and slower still on
   // short draft ranges.)
-  const int64_t slots = num_cus > 0 ? num_cus : 256;
+  // MD_SLOTS_SCALE = 2..4 plans for that many workgroups per compute unit
+  // (measurement only).
+  const int64_t slots = (num_cus > 0 ? num_cus : 256) * std::max(1, env_knob("MD_SLOTS_SCALE", 2, 4));
   p.hp = heads_per_workgroup(a, mode, U, slots);
   p.n_groups = p.n_units / p.hp;
   int64_t n_chunks, chunk_len;
@@ -185,9 +188,10 @@ Plan make_plan(const md_attn_args* a, int mode, int n_sink, int window, int num_
   p.n_chunks = static_cast<int32_t>(n_chunks);
   p.chunk_len = static_cast<int32_t>(chunk_len);
   if (p.n_chunks > 1) {
+    p.counter_bytes = align_up(static_cast<size_t>(p.n_groups) * 8, 256);
     p.part_o_bytes = align_up(static_cast<size_t>(n_chunks) * p.n_rows * a->head_dim * 4, 256);
     p.part_lse_bytes = align_up(static_cast<size_t>(n_chunks) * p.n_rows * 4, 256);
-    p.workspace_bytes = p.part_o_bytes + p.part_lse_bytes;
+    p.workspace_bytes = p.counter_bytes + p.part_o_bytes + p.part_lse_bytes;
   }
   return p;
 }

@@ -238,9 +238,11 @@ def test_workspace_zero_when_units_fill_the_device(lib):
     assert lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1) == 0
 
 
-def _split_bytes(n_chunks, n_rows, d):
+def _split_bytes(n_chunks, n_rows, d, groups):
+    """A split plan's workspace: one 8-byte arrival counter per head group,
+    then the partial O and lse, each part 256-byte aligned."""
     up = lambda x: (x + 255) // 256 * 256
-    return up(n_chunks * n_rows * d * 4) + up(n_chunks * n_rows * 4)
+    return up(groups * 8) + up(n_chunks * n_rows * d * 4) + up(n_chunks * n_rows * 4)
 
 
 @pytest.mark.parametrize("B,S,hp", [
@@ -260,7 +262,7 @@ def test_plan_pairs_heads_only_where_they_pay(lib, B, S, hp):
     chunk = -(-(-(-S // n_chunks)) // 32) * 32
     n_chunks = -(-S // chunk)
     got = lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1)
-    assert got == _split_bytes(n_chunks, B * 5 * 32, 128), (got, n_chunks)
+    assert got == _split_bytes(n_chunks, B * 5 * 32, 128, groups), (got, n_chunks)
 
 
 def test_tuning_overrides_are_read_per_call(lib, monkeypatch):
@@ -271,11 +273,11 @@ def test_tuning_overrides_are_read_per_call(lib, monkeypatch):
                   kv_stride_tok=8 * 128, kv_stride_blk=16384 * 8 * 128)
     rows = 16 * 5 * 32
     monkeypatch.delenv("MD_HEADS_PER_WG", raising=False)
-    assert lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1) == _split_bytes(4, rows, 128)
+    assert lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1) == _split_bytes(4, rows, 128, 64)
     monkeypatch.setenv("MD_HEADS_PER_WG", "1")
-    assert lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1) == _split_bytes(2, rows, 128)
+    assert lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1) == _split_bytes(2, rows, 128, 128)
     monkeypatch.setenv("MD_HEADS_PER_WG", "7")  # out of range: ignored
-    assert lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1) == _split_bytes(4, rows, 128)
+    assert lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1) == _split_bytes(4, rows, 128, 64)
 
 
 def test_workspace_draft_smaller_than_verify(lib):
@@ -373,6 +375,10 @@ GATHER_BAD = [
     ("dtype differs", {}, {"dtype": md.MD_F32}),
     ("sequences differ", {}, {"num_seqs": 3}),
     ("bad destination", {"capacity": 0}, {}),
+    ("destination shorter than the lists", {"capacity": 15}, {}),
+    ("paged destination shorter than the lists",
+     {"capacity": 0, "page_size": 4, "page_table": FAKE + 0x2000, "max_pages_per_seq": 3,
+      "num_pages": 8}, {}),
     ("bad source", {}, {"kv_stride_tok": 100}),
     ("misaligned destination", {"k": FAKE + 4}, {}),
     ("null source", {}, {"v": None}),

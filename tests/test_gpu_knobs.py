@@ -2,7 +2,10 @@
 fp64 oracle: MD_PREFETCH_DEPTH (a second tile in flight: its own kernel
 instances), MD_OCCUPANCY (instances compiled for one or two waves per SIMD),
 MD_LPT (longest-first dispatch off, or on wherever a plan allows it) and
-MD_HEADS_PER_WG (one head or a head pair per workgroup).  The overrides are
+MD_HEADS_PER_WG (one head or a head pair per workgroup), MD_FUSED_MERGE
+(split ranges merged by each head group's last workgroup instead of a second
+launch) and MD_SLOTS_SCALE (plans for two or four workgroups per compute
+unit: more and shorter chunks).  The overrides are
 read on every call, so one process sweeps them all; each setting runs the
 same shapes: one to four 16-row tiles, the streaming and listed
 drafts, a split range with its merge and a longest-first batch."""
@@ -22,9 +25,11 @@ DEV = "cuda:0"
 SETTINGS = [
     {}, {"MD_PREFETCH_DEPTH": "2"}, {"MD_PREFETCH_DEPTH": "3"}, {"MD_OCCUPANCY": "1"},
     {"MD_OCCUPANCY": "2"}, {"MD_LPT": "1"}, {"MD_LPT": "2"}, {"MD_HEADS_PER_WG": "1"},
-    {"MD_HEADS_PER_WG": "2"},
+    {"MD_HEADS_PER_WG": "2"}, {"MD_FUSED_MERGE": "1"}, {"MD_SLOTS_SCALE": "2"},
+    {"MD_SLOTS_SCALE": "4"},
 ]
-KNOBS = ["MD_PREFETCH_DEPTH", "MD_OCCUPANCY", "MD_LPT", "MD_HEADS_PER_WG"]
+KNOBS = ["MD_PREFETCH_DEPTH", "MD_OCCUPANCY", "MD_LPT", "MD_HEADS_PER_WG", "MD_FUSED_MERGE",
+         "MD_SLOTS_SCALE"]
 
 # name, mode, B, L, Hq, Hkv, d, lens, page, n_sink, window, budget
 CASES = [
