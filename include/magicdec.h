@@ -210,6 +210,34 @@ size_t md_workspace_bytes(const md_attn_args* a, int32_t mode, int32_t n_sink, i
 size_t md_workspace_bytes_indexed(const md_attn_args* a, int32_t idx_stride);
 
 /*
+ * md_verify_attn (mode MD_MODE_VERIFY) or md_draft_attn (mode MD_MODE_DRAFT,
+ * with n_sink and window as there) without a caller workspace, for callers
+ * that cannot allocate device memory: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation.  The caller still passes
+ * every input and output; a->workspace and a->workspace_bytes are ignored.
+ *   - A split-range plan keeps its state (tagged arrival counters, partial O
+ *     and lse) in a static device buffer of MD_NOALLOC_SCRATCH_BYTES that the
+ *     library holds on each GPU it runs on until the process ends.  That
+ *     covers every plan on a device of up to 256 compute units (MI355X); a
+ *     plan needing more (md_workspace_bytes > MD_NOALLOC_SCRATCH_BYTES)
+ *     returns MD_ERR_WORKSPACE before any launch.
+ *   - The call allocates nothing (no hipMalloc, hipFree or allocating
+ *     library routine).  Its first call on a device looks up that device's
+ *     buffer address once (hipGetSymbolAddress).
+ *   - All calls on one GPU share its buffer, which keeps the last call's
+ *     contents; nothing in it needs clearing (the counters carry a per-call
+ *     tag).  Calls that can overlap in time on one GPU (other streams, other
+ *     threads) race on it and give wrong results: serialise them.
+ *   - `stream` (NULL: the null stream) must belong to the current device.
+ * Errors: as md_verify_attn / md_draft_attn; MD_ERR_INVALID_ARG for another
+ * mode or a stream of another device; MD_ERR_WORKSPACE for a plan larger than
+ * the buffer; MD_ERR_HIP if the address lookup fails.
+ */
+#define MD_NOALLOC_SCRATCH_BYTES ((size_t)33 << 20)
+int md_attn_noalloc(const md_attn_args* a, int32_t mode, int32_t n_sink, int32_t window,
+                    void* stream);
+
+/*
  * SnapKV-style selection of the static draft cache at prefill: the static
  * KV selection the paper finds best (Sec. 4.4; budget 2049 in Sec. 5.2),
  * with its observation window (32 queries) and average pooling (kernel 5).

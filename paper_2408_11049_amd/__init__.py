@@ -44,7 +44,9 @@ EXPORTED = ["md_verify_attn", "md_draft_attn", "md_draft_attn_indexed", "md_merg
             "md_streaming_list", "md_kv_gather", "md_sd_expected_tokens", "md_sd_latency_ratio",
             "md_sd_best_gamma", "md_sd_alpha_from_omega",
             "md_status_str", "md_last_hip_error", "md_attn_args_size",
+            "md_attn_noalloc",
             "md_bench_stream_read", "md_bench_copy", "md_bench_fill", "md_bench_attn_stamps"]
+MD_NOALLOC_SCRATCH_BYTES = 33 << 20
 
 
 class MdAttnArgs(ctypes.Structure):
@@ -119,6 +121,8 @@ def load_library(path: str = LIB_PATH):
     lib.md_draft_attn.restype = ctypes.c_int
     lib.md_draft_attn_indexed.argtypes = [args_p, vp, vp, i32, vp]
     lib.md_draft_attn_indexed.restype = ctypes.c_int
+    lib.md_attn_noalloc.argtypes = [args_p, i32, i32, i32, vp]
+    lib.md_attn_noalloc.restype = ctypes.c_int
     lib.md_workspace_bytes_indexed.argtypes = [args_p, i32]
     lib.md_workspace_bytes_indexed.restype = sz
     sk_p = ctypes.POINTER(MdSnapkvArgs)
@@ -344,6 +348,27 @@ def _attention(mode, q, k, v, kv_lens, n_sink, window, *, max_kv_len=None, page_
     else:
         st = lib.md_draft_attn_indexed(ctypes.byref(a), _ptr(idx), _ptr(idx_len), idx.shape[2], s)
     _check(st)
+    return out, lse
+
+
+@_stream_scoped
+def md_attn_noalloc(mode, q, k, v, kv_lens, n_sink=0, window=1, *, max_kv_len=None,
+                    page_table=None, sm_scale=0.0, out=None, lse=None, stream=None):
+    """md_verify_attn (mode 0) or md_draft_attn (mode 1) through the entry
+    point that allocates nothing on the device: the library's static scratch
+    stands in for the workspace (see include/magicdec.h).  `out` and `lse`
+    are the caller's; passing both makes the call allocation-free on the
+    torch side too."""
+    import torch
+    lib = load_library()
+    if kv_lens.dtype != torch.int32:
+        raise ValueError("kv_lens must be int32")
+    if out is None:
+        out = torch.empty_like(q)
+    a = make_args(q, k, v, kv_lens, max_kv_len=max_kv_len, page_table=page_table,
+                  sm_scale=sm_scale, out=out, lse=lse)
+    _check(lib.md_attn_noalloc(ctypes.byref(a), int(mode), int(n_sink), int(window),
+                               _stream_handle(q, stream)))
     return out, lse
 
 

@@ -16,7 +16,8 @@ BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libmagicdec.so")
 ARCH = "gfx950"
 
-SOURCES = ["api.cpp", "plan.cpp", "costmodel.cpp", "attn.hip", "merge.hip", "snapkv.hip", "step.hip", "bench.hip"]
+SOURCES = ["api.cpp", "plan.cpp", "costmodel.cpp", "attn.hip", "merge.hip", "snapkv.hip", "step.hip",
+           "bench.hip", "noalloc.hip"]
 
 
 def hipcc() -> str:

@@ -40,11 +40,6 @@ bool overlaps(const void* a, const void* b, size_t n) {
 
 thread_local std::string g_last_hip_error;
 
-int hip_fail(hipError_t e) {
-  g_last_hip_error = hipGetErrorString(e);
-  return MD_ERR_HIP;
-}
-
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 // K/V tiles in flight per wave.  MD_PREFETCH_DEPTH (1..3) overrides the
@@ -81,6 +76,16 @@ int longest_first(int mode, int n_chunks, int num_seqs, int max_kv_len) {
   if (forced) return forced == 2;
   return max_kv_len >= kLptMinLen;
 }
+
+}  // namespace
+
+int hip_fail(hipError_t e) {
+  g_last_hip_error = hipGetErrorString(e);
+  (void)hipGetLastError();  // the launch error is reported here, not to the next call
+  return MD_ERR_HIP;
+}
+
+namespace {
 
 // A fresh tag per attention call (1 .. 2^48 - 1; a process would need
 // centuries of calls to wrap it): it marks the arrival counters of that

@@ -166,6 +166,10 @@ hipError_t launch_kv_commit(int B, int q_len, int32_t* lens, const int32_t* acce
 hipError_t launch_streaming_list(int B, int Hkv, const int32_t* prompt_lens, int n_sink,
                                  int window, int32_t* idx, int32_t* idx_len, hipStream_t s);
 
+// Records a HIP error's text for md_last_hip_error (calling thread) and
+// returns MD_ERR_HIP.
+int hip_fail(hipError_t e);
+
 hipError_t launch_bench_read(const void* buf, size_t bytes, float* sink, int n_blocks,
                              hipStream_t s);
 hipError_t launch_bench_copy(void* dst, const void* src, size_t bytes, int n_blocks,

@@ -515,3 +515,48 @@ def test_struct_layouts_match_the_header(tmp_path):
         assert got[(name, "size")] == ctypes.sizeof(cls), name
         for f, _ in cls._fields_:
             assert got[(name, f)] == getattr(cls, f).offset, (name, f)
+
+
+def test_noalloc_header_limit_matches_binding():
+    text = open(HEADERS[0]).read()
+    m = re.search(r"#define MD_NOALLOC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", text)
+    assert m and int(m.group(1)) << int(m.group(2)) == md.MD_NOALLOC_SCRATCH_BYTES
+
+
+def test_noalloc_scratch_holds_every_plan():
+    """On a 256-compute-unit device (this host's fallback, and MI355X) every
+    split plan fits the static scratch: a sweep over batch, heads, query rows
+    (up to 64), head dims and lengths up to 2^30, verify and draft."""
+    worst = 0
+    for B in (1, 2, 3, 5, 8, 16, 31, 64, 127):
+        for Hkv, Hq in ((1, 64), (2, 32), (8, 64), (8, 32), (4, 4), (3, 12)):
+            for L in (1, 4, 16):
+                if (Hq // Hkv) * L > 64:
+                    continue
+                for d in (64, 128):
+                    for S in (4096, 65536, 1 << 20, 1 << 30):
+                        a = good_args(num_seqs=B, num_kv_heads=Hkv, num_q_heads=Hq, q_len=L,
+                                      head_dim=d, max_kv_len=S, kv_stride_tok=Hkv * d,
+                                      kv_stride_head=d, kv_stride_blk=S * Hkv * d)
+                        for mode, ns, w in ((0, 0, 1), (1, 64, S // 2)):
+                            worst = max(worst, lib_bytes(a, mode, ns, w))
+    assert 0 < worst <= md.MD_NOALLOC_SCRATCH_BYTES, worst
+
+
+def lib_bytes(a, mode, ns, w):
+    return md.load_library().md_workspace_bytes(ctypes.byref(a), mode, ns, w)
+
+
+def test_noalloc_refuses_before_any_hip_call(lib, monkeypatch):
+    """Argument errors and a plan larger than the scratch come back before
+    the library touches a device (this host has none)."""
+    a = good_args(num_seqs=3, num_kv_heads=2, num_q_heads=32, q_len=4, max_kv_len=1 << 21,
+                  kv_stride_tok=2 * 128, kv_stride_blk=(1 << 21) * 2 * 128)
+    assert lib.md_attn_noalloc(None, 0, 0, 1, None) == md.MD_ERR_INVALID_ARG
+    assert lib.md_attn_noalloc(ctypes.byref(a), 2, 0, 1, None) == md.MD_ERR_INVALID_ARG
+    # Four workgroups per compute unit (a measurement override) make this plan
+    # need more than the scratch: 3 head pairs x 342 chunks x 384 rows.
+    monkeypatch.setenv("MD_SLOTS_SCALE", "4")
+    need = lib.md_workspace_bytes(ctypes.byref(a), 0, 0, 1)
+    assert need > md.MD_NOALLOC_SCRATCH_BYTES
+    assert lib.md_attn_noalloc(ctypes.byref(a), 0, 0, 1, None) == md.MD_ERR_WORKSPACE
