@@ -10,28 +10,38 @@ gamma = 4, draft budget 16 sinks + 1008 window; inputs are seeded synthetic
 N(0, 1) values already resident in HBM.
 
 Timing: W untimed warm-up steps, then exactly K steps between two
-synchronisations.  Inside each step the last-level caches are evicted by
-writing a 1 GiB buffer before each call (cold cache), and HIP events on the
-launch stream bracket each call; ms_per_step and `value` come from those
-events (flush writes excluded), the wall time of the K-step region is
-reported beside them.
+synchronisations.  Inside each step the caches are evicted before each call
+by reading a 1 GiB buffer with cache-allocating loads (cold cache; a fill
+would leave dirty lines whose write-back the timed call pays for -- both are
+reported), and HIP events on the launch stream bracket each call;
+ms_per_step and `value` come from those events (eviction excluded), the wall
+time of the K-step region is reported beside them.
 
 `value` is K/V HBM GB/s: the algorithmic K/V bytes of verify + draft (every
 visible K and V element once) divided by the step time.  `roofline` is for
-the dominant kernel (the verify attention kernel, a single launch here), with
-the HBM traffic and MFMA utilisation read from the committed rocprofv3
-summaries under profiles/ (null when the kernel source changed since).
-`cpu_baseline` is the fp64 oracle timed on a bounded sample of the same
-workload on this host's cores (a reported baseline, not a target).
-`inputs_sha256` identifies the seeded inputs that were timed.  `detail`
-adds the one-token and warm timings, the listed and gathered SnapKV-style
-drafts, the SnapKV selection, append, acceptance and commit, whole
-engine-shaped speculative steps (eager and as a HIP graph), the read ceiling
-and the oracle beside the step kernels.
+the dominant kernel (the verify attention kernel, a single launch here):
+`achieved`/`frac` from the event times of the K timed calls, and
+`kernel_time` from the rocprofv3 kernel trace of the same K timed dispatches
+(profiles/, written by this script's --summarize mode from a traced run of
+itself); HBM traffic and MFMA utilisation come from the committed rocprofv3
+counter summaries.  Each profile is used only while the kernel sources it
+was taken on are unchanged (their SHA-256 is recorded in it).  `cpu_baseline`
+is the fp64 oracle timed on a bounded sample of the same workload on this
+host's cores (a reported baseline, not a target).  `inputs_sha256` identifies
+the seeded inputs that were timed.  `detail` adds every configuration of the
+workload list (verify, draft, one-token draft and verify, t_SD, GB/s), the
+one-token and warm timings, the listed and gathered SnapKV-style drafts, the
+SnapKV selection, append, acceptance and commit, whole engine-shaped
+speculative steps (eager and as a HIP graph), the read ceiling and the oracle
+beside the step kernels.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+                       [--no-configs]
+       python bench.py --summarize trace|counters|mfma --csv F [F2] --bench-json J
+                       --cmd "..."   (writes a profiles/ summary to stdout)
 """
 import argparse
+import csv
 import hashlib
 import json
 import math
@@ -45,13 +55,32 @@ sys.path.insert(0, ROOT)
 
 WORKLOAD = "llama8b_b64_s32k_paged"
 HBM_PEAK_GBS = 8000.0
-PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "attn_verify_llama8b_b64_s32k_paged_counters.md")
-PROFILE_MFMA = os.path.join(ROOT, "profiles", "attn_mfma_llama8b_b64_s32k_paged.md")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2408_11049_amd", "csrc", "attn.hip")
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+PROFILES = os.path.join(ROOT, "profiles")
+PROFILE_TRACE = os.path.join(PROFILES, "attn_verify_llama8b_b64_s32k_paged_trace.md")
+PROFILE_COUNTERS = os.path.join(PROFILES, "attn_verify_llama8b_b64_s32k_paged_counters.md")
+PROFILE_MFMA = os.path.join(PROFILES, "attn_mfma_llama8b_b64_s32k_paged.md")
+CSRC = os.path.join(ROOT, "paper_2408_11049_amd", "csrc")
+# What decides the attention launches' code and plans.
+KERNEL_SOURCES = [os.path.join(CSRC, f) for f in
+                  ("attn.hip", "merge.hip", "api.cpp", "plan.cpp", "internal.h", "kernels.h")]
+# Per-config table: the workload list's configurations (the bench workload is
+# the headline itself).
+CONFIGS = ["tiny_f32", "llama8b_b32_s8k", "llama8b_b64_ragged_paged", "llama8b_b256_s8k_koutlier",
+           "llama70b_b16_s128k"]
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_sha256(paths=None):
+    """SHA-256 over the attention launch's sources (name and bytes of each)."""
+    h = hashlib.sha256()
+    for path in paths or KERNEL_SOURCES:
+        h.update(os.path.basename(path).encode() + b"\0")
+        h.update(open(path, "rb").read())
+    return h.hexdigest()
 
 
 def kv_bytes(w, lens, mode, q_len):
@@ -71,39 +100,276 @@ def kv_bytes(w, lens, mode, q_len):
     return total
 
 
+def _profile_fields(path):
+    """The `key: value` lines of a committed profile summary, or None when it
+    is missing or was taken on other kernel sources."""
+    if not os.path.exists(path):
+        return None
+    fields = dict(re.findall(r"^([a-z0-9_]+):\s*(\S+)\s*$", open(path).read(), re.M))
+    if fields.get("kernel_source_sha256") != kernel_source_sha256():
+        return None
+    return fields
+
+
 def read_counters():
-    """HBM traffic per verify launch from the committed rocprofv3 counter
-    summary, or None if absent or taken on a different kernel source."""
-    if not os.path.exists(PROFILE_COUNTERS):
+    """HBM bytes (FETCH + WRITE, calibrated) per verify launch, from the
+    committed counter summary; None if absent or stale."""
+    f = _profile_fields(PROFILE_COUNTERS)
+    if not f or "verify_fetch_bytes_per_launch" not in f:
         return None
-    text = open(PROFILE_COUNTERS).read()
-    m_sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
-    m_f = re.search(r"fetch_bytes_per_launch:\s*([0-9.eE+]+)", text)
-    m_w = re.search(r"write_bytes_per_launch:\s*([0-9.eE+]+)", text)
-    if not (m_sha and m_f and m_w):
-        return None
-    sha = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
-    if sha != m_sha.group(1):
-        return None
-    return float(m_f.group(1)) + float(m_w.group(1))
+    return float(f["verify_fetch_bytes_per_launch"]) + float(f["verify_write_bytes_per_launch"])
 
 
 def read_mfma():
-    """The verify kernel's MFMA utilisation from the committed rocprofv3 counter
-    summary (MfmaUtil, bf16 MFMA TFLOP/s), or None if absent or taken on a
-    different kernel source."""
-    if not os.path.exists(PROFILE_MFMA):
+    """The verify kernel's bf16 MFMA rate from the committed counter summary
+    (FLOP per launch from SQ_INSTS_VALU_MFMA_MOPS_BF16 over the dispatch's
+    duration), or None if absent or stale."""
+    f = _profile_fields(PROFILE_MFMA)
+    if not f or "verify_mfma_tflops" not in f:
         return None
-    text = open(PROFILE_MFMA).read()
-    m_sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
-    m_u = re.search(r"verify_mfma_util_pct:\s*([0-9.eE+]+)", text)
-    m_t = re.search(r"verify_mfma_tflops:\s*([0-9.eE+]+)", text)
-    if not (m_sha and m_u and m_t):
+    t = float(f["verify_mfma_tflops"])
+    return {"bf16_tflops": t, "peak_tflops": MFMA_BF16_PEAK_TFLOPS,
+            "frac": round(t / MFMA_BF16_PEAK_TFLOPS, 4),
+            "busy_pct": float(f["verify_mfma_busy_pct"]) if "verify_mfma_busy_pct" in f else None,
+            "source": os.path.relpath(PROFILE_MFMA, ROOT)}
+
+
+def read_trace():
+    """Kernel durations of the timed verify and draft dispatches from the
+    committed kernel-trace summary, or None if absent or stale."""
+    f = _profile_fields(PROFILE_TRACE)
+    if not f or "verify_kernel_mean_us" not in f:
         return None
-    if hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest() != m_sha.group(1):
-        return None
-    return {"util_pct": float(m_u.group(1)), "bf16_tflops": float(m_t.group(1)),
-            "peak_tflops": 2500.0, "source": "profiles/attn_mfma_llama8b_b64_s32k_paged.md"}
+    return {k: float(v) for k, v in f.items()
+            if k.endswith("_us") or k.endswith("_frac") or k.endswith("_bytes")}
+
+
+# ---------------------------------------------------------------------------
+# Profile summaries (--summarize): turn a rocprofv3 run of this script into the
+# markdown under profiles/.  The attention dispatches of a run come in a fixed
+# order -- W warm-up steps, then the K timed steps, each a verify call then a
+# draft call -- so the timed calls are picked by ordinal, not by guesswork.
+
+def _rows(path):
+    with open(path, newline="") as f:
+        return list(csv.DictReader(f))
+
+
+def _short(name):
+    name = name.split("(")[0].replace("void ", "")
+    return name.strip()
+
+
+def _dispatches(rows):
+    """{dispatch id: {"name", "start", "end", counter: value ...}} in launch order."""
+    out = {}
+    for r in rows:
+        d = int(r["Dispatch_Id"])
+        e = out.setdefault(d, {"name": r["Kernel_Name"]})
+        if "Start_Timestamp" in r and r.get("Start_Timestamp"):
+            e["start"], e["end"] = int(r["Start_Timestamp"]), int(r["End_Timestamp"])
+        if "Counter_Name" in r:
+            e[r["Counter_Name"]] = e.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    return [out[k] for k in sorted(out)]
+
+
+def timed_calls(dispatches, warmup, steps):
+    """The timed verify and draft calls: lists of dispatch groups (an
+    attention dispatch plus a merge dispatch that follows it, if any)."""
+    calls, cur = [], None
+    for d in dispatches:
+        if "attn_partial_kernel" in d["name"]:
+            cur = [d]
+            calls.append(cur)
+        elif "merge_lse_kernel" in d["name"] and cur is not None:
+            cur.append(d)
+            cur = None
+        else:
+            cur = None
+    need = 2 * (warmup + steps)
+    if len(calls) < need:
+        raise SystemExit(f"only {len(calls)} attention calls; expected at least {need}")
+    timed = calls[2 * warmup: need]
+    return timed[0::2], timed[1::2]
+
+
+def _bench_line(path):
+    for line in open(path):
+        line = line.strip()
+        if line.startswith("{") and '"metric"' in line:
+            return json.loads(line)
+    raise SystemExit(f"no bench line in {path}")
+
+
+def summarize_trace(csv_path, bench_json, cmd):
+    rec = _bench_line(bench_json)
+    W, K = rec["warmup"], rec["steps"]
+    ver, dra = timed_calls(_dispatches(_rows(csv_path)), W, K)
+    det = rec["detail"]
+    ev = {"verify": det["t_verify_us"], "draft": det["t_draft_us"]}
+    alg = {"verify": det["verify_kv_bytes"], "draft": det["draft_kv_bytes"]}
+    out = ["# Kernel timing of the bench's timed verify and draft calls (rocprofv3 kernel trace)",
+           "",
+           f"Workload: {WORKLOAD} -- Llama-3.1-8B layer shape, B = 64, S = 32768, 16-token pages,",
+           "gamma = 4, draft 16 sinks + 1008 window, bf16; cold cache (a 1 GiB read evicts the",
+           "caches before every call).  One MI355X (gfx950).",
+           "",
+           "Command (from /tmp with TMPDIR=/tmp; R = the repository root); its stdout is the",
+           "bench line quoted below:",
+           "",
+           f"    {cmd}",
+           "",
+           f"Selection: bench.py runs W = {W} warm-up steps and then K = {K} timed steps, each",
+           "a verify call followed by a draft call, before any other attention call, so in",
+           "launch order the attention dispatches go verify, draft, verify, draft, ...  The",
+           f"timed verify calls are attention dispatches {2 * W}, {2 * W + 2}, ..., "
+           f"{2 * (W + K) - 2} (0-based), the",
+           f"timed draft calls {2 * W + 1}, ..., {2 * (W + K) - 1}; a merge dispatch that follows a call",
+           "(split plans only) counts with it.",
+           "",
+           "| call | kernel | timed calls | kernel mean us | min | max | event mean us (bench line) | kernel / event | K/V GB/s (kernel) | frac of 8 TB/s (kernel) | frac (event) |",
+           "|---|---|---|---|---|---|---|---|---|---|---|"]
+    fields = {"kernel_source_sha256": kernel_source_sha256(), "warmup": W, "steps": K}
+    for name, calls in (("verify", ver), ("draft", dra)):
+        durs = [sum((d["end"] - d["start"]) for d in c) / 1e3 for c in calls]
+        kn = sorted({_short(d["name"]) for c in calls for d in c})
+        mean = sum(durs) / len(durs)
+        gbs = alg[name] / (mean * 1e-6) / 1e9
+        out.append(f"| {name} | {' + '.join('`%s`' % k for k in kn)} | {len(durs)} | {mean:.2f} | "
+                   f"{min(durs):.2f} | {max(durs):.2f} | {ev[name]:.2f} | {mean / ev[name]:.4f} | "
+                   f"{gbs:.1f} | {gbs / HBM_PEAK_GBS:.4f} | "
+                   f"{alg[name] / (ev[name] * 1e-6) / 1e9 / HBM_PEAK_GBS:.4f} |")
+        fields.update({f"{name}_kernel_mean_us": round(mean, 3),
+                       f"{name}_kernel_min_us": round(min(durs), 3),
+                       f"{name}_kernel_max_us": round(max(durs), 3),
+                       f"{name}_event_mean_us": ev[name],
+                       f"{name}_kv_bytes": alg[name],
+                       f"{name}_kernel_frac": round(gbs / HBM_PEAK_GBS, 4)})
+        if mean > ev[name]:
+            out.append(f"\nWARNING: the {name} kernels' mean exceeds the events that bracket them.")
+    r = rec["roofline"]
+    out += ["",
+            "Each call's HIP events bracket its kernel (the launch, the dispatch and the",
+            "completion signal included), so the kernel mean sits at or below the event mean.",
+            "",
+            "The bench line of the same invocation (run under the profiler, so a little",
+            "slower than an unprofiled run):",
+            "",
+            "    " + json.dumps({k: rec[k] for k in ("metric", "value", "unit", "steps", "warmup",
+                                                   "ms_per_step")}),
+            "    roofline: " + json.dumps({k: r.get(k) for k in ("achieved", "frac",
+                                                                  "algorithmic_bytes_per_launch")}),
+            "",
+            "Fields read by bench.py (`roofline.kernel_time`), valid while the kernel sources",
+            "hash to kernel_source_sha256:",
+            ""]
+    out += [f"{k}: {v}" for k, v in fields.items()]
+    return "\n".join(out) + "\n"
+
+
+def summarize_counters(fetch_csv, write_csv, bench_json, cmd):
+    rec = _bench_line(bench_json)
+    W, K = rec["warmup"], rec["steps"]
+    det = rec["detail"]
+    alg = {"verify": det["verify_kv_bytes"], "draft": det["draft_kv_bytes"]}
+    res = {}
+    calib = {}
+    for ctr, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        ds = _dispatches(_rows(path))
+        copies = [d for d in ds if "bench_copy_kernel" in d["name"]]
+        if not copies:
+            raise SystemExit(f"{path}: no md_bench_copy dispatch to calibrate {ctr}")
+        calib[ctr] = copies[-1][ctr]
+        ver, dra = timed_calls(ds, W, K)
+        for name, calls in (("verify", ver), ("draft", dra)):
+            vals = [sum(d[ctr] for d in c) for c in calls]
+            res[(name, ctr)] = (sum(vals) / len(vals), sorted({_short(d["name"]) for c in calls for d in c}))
+    gib = float(1 << 30)
+    scale = {c: gib / (calib[c] * 1024.0) for c in calib}
+    out = ["# HBM traffic of the bench's verify and draft calls (rocprofv3 counters)",
+           "",
+           f"Workload: {WORKLOAD} -- Llama-3.1-8B layer shape, B = 64, S = 32768, 16-token pages,",
+           "gamma = 4, draft 16 sinks + 1008 window, bf16.  One MI355X (gfx950).",
+           "",
+           "Commands (from /tmp with TMPDIR=/tmp; R = the repository root), one pass per counter:",
+           ""]
+    out += [f"    {c}" for c in cmd.split(" ;; ")]
+    out += ["",
+            "Calibration: bench.py copies exactly 1 GiB with md_bench_copy (1,073,741,824 B read",
+            f"and written).  FETCH_SIZE read {calib['FETCH_SIZE']:.0f} KiB for it and WRITE_SIZE "
+            f"{calib['WRITE_SIZE']:.0f} KiB, so",
+            f"bytes = KiB x 1024 x scale with scale_fetch = {scale['FETCH_SIZE']:.5f}, "
+            f"scale_write = {scale['WRITE_SIZE']:.5f}.",
+            "",
+            "The timed calls are picked as in the kernel-trace summary (the warm-up steps, then",
+            f"the timed steps of a verify and a draft call each; here W = {W}, K = {K}); each row",
+            "averages over the K timed calls.",
+            "",
+            "| call | kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | HBM bytes read | HBM bytes written | algorithmic K/V bytes | read / algorithmic |",
+            "|---|---|---|---|---|---|---|---|"]
+    fields = {"kernel_source_sha256": kernel_source_sha256(), "warmup": W, "steps": K,
+              "scale_fetch": round(scale["FETCH_SIZE"], 6), "scale_write": round(scale["WRITE_SIZE"], 6)}
+    for name in ("verify", "draft"):
+        f_kib, kn = res[(name, "FETCH_SIZE")]
+        w_kib, _ = res[(name, "WRITE_SIZE")]
+        fb, wb = f_kib * 1024 * scale["FETCH_SIZE"], w_kib * 1024 * scale["WRITE_SIZE"]
+        out.append(f"| {name} | {' + '.join('`%s`' % k for k in kn)} | {f_kib:.0f} | {w_kib:.0f} | "
+                   f"{fb:.4e} | {wb:.4e} | {alg[name]:.4e} | {fb / alg[name]:.4f} |")
+        fields[f"{name}_fetch_bytes_per_launch"] = round(fb)
+        fields[f"{name}_write_bytes_per_launch"] = round(wb)
+        fields[f"{name}_kv_bytes"] = alg[name]
+    out += ["",
+            "Fields read by bench.py (`roofline.traffic` = verify fetch + write bytes per",
+            "launch), valid while the kernel sources hash to kernel_source_sha256:", ""]
+    out += [f"{k}: {v}" for k, v in fields.items()]
+    return "\n".join(out) + "\n"
+
+
+def summarize_mfma(csv_path, bench_json, cmd):
+    rec = _bench_line(bench_json)
+    W, K = rec["warmup"], rec["steps"]
+    cfg = rec["config"]
+    ver, dra = timed_calls(_dispatches(_rows(csv_path)), W, K)
+    tr = read_trace()
+    out = ["# MFMA use of the bench's verify and draft calls (rocprofv3 counters)",
+           "",
+           f"Workload: {WORKLOAD} (as the other profiles).  One MI355X (gfx950): 256 CUs,",
+           "1024 SIMDs, dense bf16 MFMA peak 2.5 PFLOP/s.",
+           "",
+           "Command (from /tmp with TMPDIR=/tmp; R = the repository root):",
+           "",
+           f"    {cmd}",
+           "",
+           "MfmaFlopsBF16 = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512; MfmaUtil = sum of",
+           "SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x SIMDs) x 100 (rocprofv3's own",
+           "definitions).  The rate divides the FLOP per launch by the timed kernel mean of",
+           "the kernel-trace summary.  By design each call issues, per (sequence, kv head)",
+           "and visible key (rounded up to 32-token tiles), 2 contractions x 2 FLOP x d x the",
+           "padded query rows (16 per 16-row tile).",
+           "",
+           "| call | kernel | FLOP per launch | by design | kernel mean us | bf16 TFLOP/s | frac of 2.5 PFLOP/s | MfmaUtil % |",
+           "|---|---|---|---|---|---|---|---|"]
+    G = cfg["Hq"] // cfg["Hkv"]
+    rows_pad = -(-(G * (cfg["gamma"] + 1)) // 16) * 16
+    per_key = 2 * 2 * cfg["head_dim"] * rows_pad
+    u_draft = min(cfg["S"], cfg["n_sink"] + cfg["gamma"] + cfg["window"])  # sinks + union of windows
+    design = {"verify": cfg["B"] * cfg["Hkv"] * (-(-cfg["S"] // 32) * 32) * per_key,
+              "draft": cfg["B"] * cfg["Hkv"] * (-(-u_draft // 32) * 32) * per_key}
+    fields = {"kernel_source_sha256": kernel_source_sha256(), "warmup": W, "steps": K}
+    for name, calls in (("verify", ver), ("draft", dra)):
+        fl = sum(sum(d.get("MfmaFlopsBF16", 0.0) for d in c) for c in calls) / len(calls)
+        ut = sum(sum(d.get("MfmaUtil", 0.0) for d in c) for c in calls) / len(calls)
+        kn = sorted({_short(d["name"]) for c in calls for d in c})
+        mean = tr[f"{name}_kernel_mean_us"] if tr else float("nan")
+        tf = fl / (mean * 1e-6) / 1e12
+        out.append(f"| {name} | {' + '.join('`%s`' % k for k in kn)} | {fl:.4e} | {design[name]:.4e} | "
+                   f"{mean:.2f} | {tf:.1f} | {tf / MFMA_BF16_PEAK_TFLOPS:.4f} | {ut:.2f} |")
+        fields.update({f"{name}_mfma_flop_per_launch": f"{fl:.6e}",
+                       f"{name}_mfma_tflops": round(tf, 2), f"{name}_mfma_busy_pct": round(ut, 3)})
+    out += ["", "Fields read by bench.py (`roofline.mfma`), valid while the kernel sources hash to",
+            "kernel_source_sha256:", ""]
+    out += [f"{k}: {v}" for k, v in fields.items()]
+    return "\n".join(out) + "\n"
 
 
 def input_sha256(c, piece=1 << 28):
@@ -171,8 +437,14 @@ def cpu_baseline(c, w, budget_s=15.0, batch=32):
             if line.startswith("model name"):
                 model = line.split(":", 1)[1].strip()
                 break
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except AttributeError:
+        affinity = None
     return {"value": total_b / total_t / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "cpu_model": model,
+            "cpu_model": model, "host_cpus": os.cpu_count(), "cpus_available": affinity,
+            "thread_rule": "one per CPU this process may use, at most 16 (one GPU's share "
+                           "of a shared GPU host)",
             "sample": f"{done} of {len(units)} (sequence, kv head) units of {WORKLOAD} in seeded "
                       f"random order, verify + draft, {total_t:.1f} s of fp64 oracle time"}
 
@@ -227,13 +499,85 @@ def cpu_oracle_extras(c, w, logits, draft_tok, q_obs, n_obs, t_accept_us, t_vote
             "snapkv_votes_gpu_speedup": round(t_votes_all / (t_votes_us * 1e-6), 1)}
 
 
+def config_table(w_names, dev, timed, verbose=True):
+    """Cold-cache medians (p10, p50, p90 of 10 calls) of every configuration in
+    the workload list: verify and draft at q_len = gamma + 1 and 1, t_step,
+    t_SD = gamma t_draft(1) + t_verify (the attention part of Eq. 2's step
+    time), the ratio t_verify(gamma + 1) / t_verify(1) (Sec. 3.2 predicts ~1
+    where the KV cache dominates), K/V GB/s and fractions of 8 TB/s."""
+    import torch
+
+    import paper_2408_11049_amd as md
+    from paper_2408_11049_amd import workloads as wl
+
+    table = {}
+    for name in w_names:
+        w = wl.WORKLOADS[name]
+        log(f"[bench] config {name}")
+        c = wl.make_workload(w, device=dev)
+        lens, L = c["kv_lens_np"], w.q_len
+        q1 = c["q"][:, :1].contiguous()
+        common = dict(max_kv_len=c["max_kv_len"], page_table=c["page_table"])
+        need = max(md.md_workspace_bytes(q, c["k"], c["v"], c["kv_lens"], mode=m, n_sink=w.n_sink,
+                                         window=w.window, **common)
+                   for q in (c["q"], q1) for m in (0, 1))
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev) if need else None
+        o, o1 = torch.empty_like(c["q"]), torch.empty_like(q1)
+        kw = dict(return_lse=False, workspace=ws, **common)
+        calls = {
+            "verify": lambda: md.md_verify_attn(c["q"], c["k"], c["v"], c["kv_lens"], out=o, **kw),
+            "verify_qlen1": lambda: md.md_verify_attn(q1, c["k"], c["v"], c["kv_lens"], out=o1, **kw),
+            "draft": lambda: md.md_draft_attn(c["q"], c["k"], c["v"], c["kv_lens"], w.n_sink,
+                                              w.window, out=o, **kw),
+            "draft_qlen1": lambda: md.md_draft_attn(q1, c["k"], c["v"], c["kv_lens"], w.n_sink,
+                                                    w.window, out=o1, **kw),
+        }
+        for fn in calls.values():
+            fn()
+        t = {k: timed(fn, n=10, stats=True) for k, fn in calls.items()}
+        by = {"verify": kv_bytes(w, lens, "verify", L), "verify_qlen1": kv_bytes(w, lens, "verify", 1),
+              "draft": kv_bytes(w, lens, "draft", L), "draft_qlen1": kv_bytes(w, lens, "draft", 1)}
+        row = {"shape": f"B={w.B} Hq={w.Hq} Hkv={w.Hkv} d={w.d} gamma={w.gamma} "
+                        f"S={w.S or f'{w.S_lo}..{w.S_hi}'} sinks+window={w.n_sink}+{w.window} "
+                        f"{w.dtype} {'paged ' + str(w.page_size) if w.page_size else 'contiguous'}"}
+        for k in calls:
+            p50 = t[k][1]
+            row[f"t_{k}_us_p10_p50_p90"] = t[k]
+            row[f"{k}_kv_bytes"] = by[k]
+            row[f"{k}_gbs"] = round(by[k] / (p50 * 1e-6) / 1e9, 1)
+            row[f"{k}_frac"] = round(by[k] / (p50 * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
+        row["t_step_us (verify + draft)"] = round(t["verify"][1] + t["draft"][1], 2)
+        row["t_sd_us (gamma x draft_qlen1 + verify)"] = round(w.gamma * t["draft_qlen1"][1] + t["verify"][1], 2)
+        row["verify_ratio_qlen_gamma1_vs_1"] = round(t["verify"][1] / t["verify_qlen1"][1], 4)
+        table[name] = row
+        if verbose:
+            log(f"[bench]   verify {t['verify'][1]:.1f} us ({row['verify_frac']:.3f})  draft "
+                f"{t['draft'][1]:.1f} us ({row['draft_frac']:.3f})  draft(1) {t['draft_qlen1'][1]:.1f} us")
+        del c, ws, o, o1, q1
+        torch.cuda.empty_cache()
+    return table
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-configuration table (profiling passes)")
+    ap.add_argument("--summarize", choices=["trace", "counters", "mfma"])
+    ap.add_argument("--csv", nargs="+")
+    ap.add_argument("--bench-json")
+    ap.add_argument("--cmd", default="")
     args = ap.parse_args()
+    if args.summarize:
+        fn = {"trace": lambda: summarize_trace(args.csv[0], args.bench_json, args.cmd),
+              "counters": lambda: summarize_counters(args.csv[0], args.csv[1], args.bench_json,
+                                                     args.cmd),
+              "mfma": lambda: summarize_mfma(args.csv[0], args.bench_json, args.cmd)}
+        sys.stdout.write(fn[args.summarize]())
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (the library has no multi-GPU path); "
               f"--gpus {args.gpus} is not supported", file=sys.stderr)
@@ -292,7 +636,15 @@ def main():
         md.md_draft_attn(q1, c["k"], c["v"], c["kv_lens"], w.n_sink, w.window, out=out1,
                          return_lse=False, workspace=ws_d1, **common)
 
+    flush_sink = torch.zeros(4, dtype=torch.float32, device=dev)
+
     def do_flush():
+        # Cold cache: reading 1 GiB with cache-allocating loads evicts the L2s and
+        # the 256 MB last-level cache, and leaves no dirty lines behind.
+        md._check(lib.md_bench_evict(md.ctypes.c_void_p(flush.data_ptr()), flush.numel(),
+                                     md.ctypes.c_void_p(flush_sink.data_ptr()), sh))
+
+    def do_fill_flush():
         md._check(lib.md_bench_fill(md.ctypes.c_void_p(flush.data_ptr()), flush.numel(), 0, sh))
 
     bytes_v = kv_bytes(w, lens, "verify", L)
@@ -323,14 +675,16 @@ def main():
 
     # Extra timings (outside the K-step region): the real one-token draft, the
     # one-token verify (KV-bound ratio the paper predicts ~1), the read ceiling.
-    def timed(fn, n=10):
+    def timed(fn, n=10, flush_fn=None, stats=False):
         ts = []
         for _ in range(n):
-            do_flush()
+            (flush_fn or do_flush)()
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream); fn(); b.record(stream)
             torch.cuda.synchronize()
             ts.append(a.elapsed_time(b) * 1e3)
+        if stats:
+            return [round(float(x), 2) for x in np.percentile(ts, [10, 50, 90])]
         return float(np.median(ts))
 
     def timed_warm(fn, n=10):
@@ -346,6 +700,9 @@ def main():
         return a.elapsed_time(b) * 1e3 / n
 
     t_verify_warm, t_draft_warm = timed_warm(verify), timed_warm(draft)
+    # The same calls after a 1 GiB fill instead of a read (the dirty lines it
+    # leaves are written back while the timed call runs).
+    t_verify_fill, t_draft_fill = timed(verify, flush_fn=do_fill_flush), timed(draft, flush_fn=do_fill_flush)
     t_draft1 = timed(draft1)
     t_verify1 = timed(verify1)
     # SnapKV-style draft over a listed static cache at the paper's best SnapKV
@@ -571,12 +928,38 @@ def main():
     verify_gbs = bytes_v / (np.mean(tv) * 1e-6) / 1e9
     value = (bytes_v + bytes_d) / (t_step_us * 1e-6) / 1e9
     traffic = read_counters()
+    trace = read_trace()
+    mfma = read_mfma()
+    kernel_time = None
+    if trace:
+        kernel_time = {
+            "mean_us": trace["verify_kernel_mean_us"],
+            "achieved": round(bytes_v / (trace["verify_kernel_mean_us"] * 1e-6) / 1e9, 1),
+            "frac": round(bytes_v / (trace["verify_kernel_mean_us"] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+            "event_mean_us_same_run": trace["verify_event_mean_us"],
+            "source": os.path.relpath(PROFILE_TRACE, ROOT) + " (the timed dispatches of a traced run)"}
     roofline = {"bound": "hbm", "achieved": round(verify_gbs, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(verify_gbs / HBM_PEAK_GBS, 4),
                 "traffic": traffic,
-                "kernel": "md::attn_partial_kernel<128, true, 2, true, false, 1, 1> (md_verify_attn)",
+                "kernel": "md::attn_partial_kernel (md_verify_attn), a single launch",
                 "algorithmic_bytes_per_launch": bytes_v,
-                "mfma": read_mfma()}
+                "kernel_time": kernel_time,
+                "mfma": mfma}
+    configs = None
+    if not args.no_configs:
+        configs = config_table(CONFIGS, dev, timed)
+        configs[WORKLOAD + " (headline: the event means above)"] = {
+            "t_verify_us_p10_p50_p90": [round(float(x), 2) for x in np.percentile(tv, [10, 50, 90])],
+            "t_verify_qlen1_us": round(t_verify1, 2),
+            "t_verify_us_after_fill (1 GiB written before each call, not read)": round(t_verify_fill, 2),
+            "t_draft_us_after_fill": round(t_draft_fill, 2),
+            "t_draft_us_p10_p50_p90": [round(float(x), 2) for x in np.percentile(td, [10, 50, 90])],
+            "t_draft_qlen1_us": round(t_draft1, 2),
+            "verify_frac": round(bytes_v / (np.median(tv) * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+            "draft_frac": round(bytes_d / (np.median(td) * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+            "draft_qlen1_frac": round(kv_bytes(w, lens, "draft", 1) / (t_draft1 * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+            "t_sd_us (gamma x draft_qlen1 + verify)": round(w.gamma * t_draft1 + float(np.median(tv)), 2),
+            "verify_ratio_qlen_gamma1_vs_1": round(float(np.median(tv)) / t_verify1, 4)}
 
     cpu = None
     oracle_extras = None
@@ -593,7 +976,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": WORKLOAD, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "head_dim": w.d,
                    "S": w.S, "gamma": w.gamma, "n_sink": w.n_sink, "window": w.window,
-                   "page_size": w.page_size, "cache": "cold (1 GiB flush before each call)"},
+                   "page_size": w.page_size,
+                   "cache": "cold (a 1 GiB read evicts the caches before each call)"},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "inputs_sha256": inputs,
@@ -607,6 +991,8 @@ def main():
             "t_verify_warm_us (back-to-back, no flush)": round(t_verify_warm, 2),
             "t_draft_warm_us (back-to-back, no flush)": round(t_draft_warm, 2),
             "t_verify_qlen1_us": round(t_verify1, 2),
+            "t_verify_us_after_fill (1 GiB written before each call, not read)": round(t_verify_fill, 2),
+            "t_draft_us_after_fill": round(t_draft_fill, 2),
             "verify_ratio_qlen_gamma1_vs_1": round(float(np.median(tv)) / t_verify1, 4),
             "t_sd_us (gamma*t_draft(1) + t_verify)": round(w.gamma * t_draft1 + float(np.mean(tv)), 2),
             "t_draft_indexed_us (SnapKV-style list, budget 2049)": round(t_draft_idx, 2),
@@ -642,6 +1028,7 @@ def main():
             "read_ceiling_gbs": round(ceiling, 1),
             "pct_of_read_ceiling": round(100 * value / ceiling, 2),
             "wall_ms_per_step_incl_flush": round(wall * 1e3 / K, 4),
+            "configs": configs,
             "cpu_oracle_extras": oracle_extras,
             "paper_context": "2.51x end-to-end speedup, Llama-3.1-8B SnapKV self-speculation, "
                              "8xH100 (Table 2): context only, not comparable",

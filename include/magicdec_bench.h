@@ -26,6 +26,12 @@ extern "C" {
  * keeps the loads from being optimised away. */
 int md_bench_stream_read(const void* buf, size_t bytes, float* sink, void* stream);
 
+/* Read `bytes` of `buf` once with ordinary (cache-allocating) 16-byte loads:
+ * reading a buffer larger than the L2s and the last-level cache evicts them
+ * before a cold-cache timing and, unlike md_bench_fill, leaves no dirty lines
+ * for the timed call to write back.  `sink` as for md_bench_stream_read. */
+int md_bench_evict(const void* buf, size_t bytes, float* sink, void* stream);
+
 /* dst[0:bytes] = src[0:bytes]: a plain copy of known size, used to calibrate
  * the HBM byte counters (FETCH_SIZE, WRITE_SIZE). */
 int md_bench_copy(void* dst, const void* src, size_t bytes, void* stream);

@@ -45,7 +45,8 @@ EXPORTED = ["md_verify_attn", "md_draft_attn", "md_draft_attn_indexed", "md_merg
             "md_sd_best_gamma", "md_sd_alpha_from_omega",
             "md_status_str", "md_last_hip_error", "md_attn_args_size",
             "md_attn_noalloc",
-            "md_bench_stream_read", "md_bench_copy", "md_bench_fill", "md_bench_attn_stamps"]
+            "md_bench_stream_read", "md_bench_evict", "md_bench_copy", "md_bench_fill",
+            "md_bench_attn_stamps"]
 MD_NOALLOC_SCRATCH_BYTES = 33 << 20
 
 
@@ -166,6 +167,8 @@ def load_library(path: str = LIB_PATH):
     lib.md_attn_args_size.restype = sz
     lib.md_bench_stream_read.argtypes = [vp, sz, vp, vp]
     lib.md_bench_stream_read.restype = ctypes.c_int
+    lib.md_bench_evict.argtypes = [vp, sz, vp, vp]
+    lib.md_bench_evict.restype = ctypes.c_int
     lib.md_bench_copy.argtypes = [vp, vp, sz, vp]
     lib.md_bench_copy.restype = ctypes.c_int
     lib.md_bench_fill.argtypes = [vp, sz, ctypes.c_uint32, vp]

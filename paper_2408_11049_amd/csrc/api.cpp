@@ -564,6 +564,13 @@ int md_bench_stream_read(const void* buf, size_t bytes, float* sink, void* strea
   return e == hipSuccess ? MD_OK : md::hip_fail(e);
 }
 
+int md_bench_evict(const void* buf, size_t bytes, float* sink, void* stream) {
+  if (!buf || !sink || !md::aligned16(buf) || bytes % 16) return MD_ERR_INVALID_ARG;
+  hipError_t e = md::launch_bench_evict(buf, bytes, sink, md::device_cu_count() * 2,
+                                        static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? MD_OK : md::hip_fail(e);
+}
+
 int md_bench_copy(void* dst, const void* src, size_t bytes, void* stream) {
   if (!dst || !src || !md::aligned16(dst) || !md::aligned16(src) || bytes % 16) return MD_ERR_INVALID_ARG;
   hipError_t e = md::launch_bench_copy(dst, src, bytes, md::device_cu_count() * 8,

@@ -32,6 +32,22 @@ __global__ void __launch_bounds__(256) bench_read_kernel(const u32x4* __restrict
   if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == 0x9e3779b9u) sink[0] = 1.f;
 }
 
+// The same blocked read with ordinary (temporal) loads: every line it reads
+// is allocated in the L2s and the last-level cache, so reading a buffer
+// larger than both evicts whatever they held -- without leaving dirty lines
+// whose write-back the next kernel would pay for, as a fill would.
+__global__ void __launch_bounds__(256) bench_evict_kernel(const u32x4* __restrict__ src,
+                                                           size_t n16, float* __restrict__ sink) {
+  const size_t per = (n16 + gridDim.x - 1) / gridDim.x;
+  const size_t lo = per * blockIdx.x;
+  const size_t hi = lo + per < n16 ? lo + per : n16;
+  u32x4 acc = u32x4{0, 0, 0, 0};
+  size_t i = lo + threadIdx.x;
+  for (; i + 3 * 256 < hi; i += 4 * 256) acc ^= src[i] ^ src[i + 256] ^ src[i + 512] ^ src[i + 768];
+  for (; i < hi; i += 256) acc ^= src[i];
+  if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == 0x9e3779b9u) sink[0] = 1.f;
+}
+
 __global__ void __launch_bounds__(256) bench_copy_kernel(u32x4* __restrict__ dst,
                                                           const u32x4* __restrict__ src,
                                                           size_t n16) {
@@ -52,6 +68,13 @@ __global__ void __launch_bounds__(256) bench_fill_kernel(u32x4* __restrict__ dst
 hipError_t launch_bench_read(const void* buf, size_t bytes, float* sink, int n_blocks,
                              hipStream_t s) {
   hipLaunchKernelGGL(bench_read_kernel, dim3(n_blocks), dim3(256), 0, s,
+                     static_cast<const u32x4*>(buf), bytes / 16, sink);
+  return hipGetLastError();
+}
+
+hipError_t launch_bench_evict(const void* buf, size_t bytes, float* sink, int n_blocks,
+                              hipStream_t s) {
+  hipLaunchKernelGGL(bench_evict_kernel, dim3(n_blocks), dim3(256), 0, s,
                      static_cast<const u32x4*>(buf), bytes / 16, sink);
   return hipGetLastError();
 }

@@ -172,6 +172,8 @@ int hip_fail(hipError_t e);
 
 hipError_t launch_bench_read(const void* buf, size_t bytes, float* sink, int n_blocks,
                              hipStream_t s);
+hipError_t launch_bench_evict(const void* buf, size_t bytes, float* sink, int n_blocks,
+                              hipStream_t s);
 hipError_t launch_bench_copy(void* dst, const void* src, size_t bytes, int n_blocks,
                              hipStream_t s);
 hipError_t launch_bench_fill(void* buf, size_t bytes, uint32_t value, int n_blocks,

@@ -44,11 +44,52 @@ def test_short_sequences_read_their_whole_prefix_in_draft_mode():
 
 
 def test_profile_readers_match_the_kernel_source(monkeypatch):
-    """The committed counter summaries carry the SHA-256 of attn.hip they were
-    taken on; bench.py reports traffic and MFMA figures only while it matches."""
-    traffic, mfma = bench.read_counters(), bench.read_mfma()
+    """The committed summaries carry the SHA-256 of the kernel sources they were
+    taken on; bench.py reports their figures only while it matches."""
+    traffic, mfma, trace = bench.read_counters(), bench.read_mfma(), bench.read_trace()
     assert traffic is not None and 8.5e9 < traffic < 8.7e9, "profiles/ are stale: re-profile"
-    assert mfma is not None and 0 < mfma["util_pct"] < 100
-    other = os.path.join(ROOT, "paper_2408_11049_amd", "csrc", "merge.hip")
-    monkeypatch.setattr(bench, "KERNEL_SOURCE", other)
-    assert bench.read_counters() is None and bench.read_mfma() is None
+    assert mfma is not None and 0 < mfma["frac"] < 1
+    assert trace is not None and 0 < trace["verify_kernel_mean_us"] <= trace["verify_event_mean_us"]
+    other = [os.path.join(ROOT, "paper_2408_11049_amd", "csrc", "step.hip")]
+    monkeypatch.setattr(bench, "KERNEL_SOURCES", other)
+    assert bench.read_counters() is None and bench.read_mfma() is None and bench.read_trace() is None
+
+
+def _trace_csv(path, names_durs):
+    """A kernel-trace CSV in rocprofv3's layout: one row per dispatch."""
+    import csv
+    with open(path, "w", newline="") as f:
+        wr = csv.writer(f)
+        wr.writerow(["Kind", "Dispatch_Id", "Kernel_Name", "Start_Timestamp", "End_Timestamp"])
+        t = 1000
+        for i, (n, d) in enumerate(names_durs):
+            wr.writerow(["KERNEL_DISPATCH", i + 1, n, t, t + int(d * 1000)])
+            t += int(d * 1000) + 5000
+
+
+def test_trace_summary_picks_the_timed_calls(tmp_path):
+    """W warm-up steps then K timed steps, each verify then draft, each after an
+    eviction read: the summary takes attention calls 2W .. 2(W+K)-1 only (a
+    merge dispatch counts with its call), whatever runs after them."""
+    V, D = "void md::attn_partial_kernel<128, true, 2, true, false, 1, 1>(md::AttnParams)", \
+        "void md::attn_partial_kernel<128, true, 2, true, false, 1, 2>(md::AttnParams)"
+    M, E = "void md::merge_lse_kernel<128, true>(int, long, float const*)", "md::bench_evict_kernel"
+    seq = []
+    for step in range(2 + 3):  # W = 2, K = 3
+        seq += [(E, 100), (V, 900 if step < 2 else 1000 + step), (E, 100), (D, 50), (M, 4)]
+    seq += [(V, 5.0), (D, 7.0)]  # later calls of the same templates are not timed
+    csv_path = tmp_path / "t.csv"
+    _trace_csv(csv_path, seq)
+    line = {"metric": "m", "value": 1, "unit": "GB/s", "steps": 3, "warmup": 2, "ms_per_step": 1,
+            "roofline": {"achieved": 1, "frac": 0.5, "algorithmic_bytes_per_launch": 8e9},
+            "detail": {"t_verify_us": 1010.0, "t_draft_us": 60.0, "verify_kv_bytes": 8e9,
+                       "draft_kv_bytes": 2.7e8}}
+    bj = tmp_path / "b.json"
+    bj.write_text("noise\n" + __import__("json").dumps(line) + "\n")
+    md_text = bench.summarize_trace(str(csv_path), str(bj), "cmd")
+    fields = dict(l.split(": ", 1) for l in md_text.splitlines() if ": " in l and l[0].isalpha()
+                  and " " not in l.split(": ", 1)[0])
+    assert float(fields["verify_kernel_mean_us"]) == pytest.approx((1002 + 1003 + 1004) / 3)
+    assert float(fields["draft_kernel_mean_us"]) == pytest.approx(54.0)  # attention + merge
+    assert fields["kernel_source_sha256"] == bench.kernel_source_sha256()
+    assert "WARNING" not in md_text
