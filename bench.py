@@ -558,6 +558,151 @@ def config_table(w_names, dev, timed, verbose=True):
     return table
 
 
+LATENCY_CASES = [("llama8b_b32_s8k", "draft"), ("llama8b_b32_s8k", "draft_qlen1"),
+                 ("llama70b_b16_s128k", "draft"), ("llama70b_b16_s128k", "draft_qlen1"),
+                 ("llama8b_b64_s32k_paged", "draft")]
+
+
+def latency_breakdown(dev, warm=3, reps=10):
+    """Where a short call's time goes: per case, `warm` untimed calls, then
+    `reps` calls timed by HIP events, then `reps` calls through
+    md_bench_attn_stamps (the same launch, each workgroup stamping the GPU's
+    100 MHz wall clock at its start, after its first tile, at the end of its
+    main loop and at its end).  Every call follows a cache eviction.  Run
+    under rocprofv3 --kernel-trace, the trace adds each timed call's kernel
+    duration (bench.py --summarize latency)."""
+    import numpy as np
+    import torch
+
+    import paper_2408_11049_amd as md
+    from paper_2408_11049_amd import workloads as wl
+
+    lib = md.load_library()
+    stream = torch.cuda.current_stream(dev)
+    sh = md.ctypes.c_void_p(stream.cuda_stream)
+    buf = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    sink = torch.zeros(4, dtype=torch.float32, device=dev)
+
+    def evict():
+        md._check(lib.md_bench_evict(md.ctypes.c_void_p(buf.data_ptr()), buf.numel(),
+                                     md.ctypes.c_void_p(sink.data_ptr()), sh))
+
+    out, cache = [], {}
+    for name, call in LATENCY_CASES:
+        w = wl.WORKLOADS[name]
+        if name not in cache:
+            cache.clear()
+            torch.cuda.empty_cache()
+            cache[name] = wl.make_workload(w, device=dev)
+        c = cache[name]
+        q = c["q"][:, :1].contiguous() if call.endswith("qlen1") else c["q"]
+        common = dict(max_kv_len=c["max_kv_len"], page_table=c["page_table"])
+        need = md.md_workspace_bytes(q, c["k"], c["v"], c["kv_lens"], mode=1, n_sink=w.n_sink,
+                                     window=w.window, **common)
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+        o = torch.empty_like(q)
+
+        def run():
+            md.md_draft_attn(q, c["k"], c["v"], c["kv_lens"], w.n_sink, w.window, out=o,
+                             return_lse=False, workspace=ws, **common)
+
+        for _ in range(warm):
+            evict()
+            run()
+        ev = []
+        for _ in range(reps):
+            evict()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream); run(); b.record(stream)
+            torch.cuda.synchronize()
+            ev.append(a.elapsed_time(b) * 1e3)
+        phases = {k: [] for k in ("start_spread", "first_tile", "loop", "epilogue", "span")}
+        for _ in range(reps):
+            evict()
+            _, st = md.md_bench_attn_stamps(1, q, c["k"], c["v"], c["kv_lens"], w.n_sink, w.window,
+                                            out=o, workspace=ws, **common)
+            torch.cuda.synchronize()
+            x = st.cpu().numpy().astype(np.int64)
+            x = x[x[:, 3] > 0]
+            t0 = x[:, 0].min()
+            phases["start_spread"].append((x[:, 0].max() - t0) / 100.0)
+            phases["first_tile"].append(float(np.median(x[:, 1] - x[:, 0])) / 100.0)
+            phases["loop"].append(float(np.median(x[:, 2] - x[:, 1])) / 100.0)
+            phases["epilogue"].append(float(np.median(x[:, 3] - x[:, 2])) / 100.0)
+            phases["span"].append((x[:, 3].max() - t0) / 100.0)
+        q_len = q.shape[1]
+        out.append({"workload": name, "call": call, "q_len": q_len, "warm": warm, "reps": reps,
+                    "kv_bytes": kv_bytes(w, c["kv_lens_np"], "draft", q_len),
+                    "workgroups": int(len(x)), "split": bool(need),
+                    "event_us": [round(v, 2) for v in ev],
+                    "stamps_us_median": {k: round(float(np.median(v)), 2) for k, v in phases.items()}})
+        log(f"[bench] {name} {call}: event {np.median(ev):.1f} us, stamps "
+            f"{out[-1]['stamps_us_median']}")
+    return out
+
+
+def summarize_latency(csv_path, bench_json, cmd):
+    rec = None
+    for line in open(bench_json):
+        if line.strip().startswith("{") and '"latency"' in line:
+            rec = json.loads(line)
+    if rec is None:
+        raise SystemExit(f"no latency line in {bench_json}")
+    calls, cur = [], None
+    for d in _dispatches(_rows(csv_path)):
+        if "attn_partial_kernel" in d["name"]:
+            cur = [d]
+            calls.append(cur)
+        elif "merge_lse_kernel" in d["name"] and cur is not None:
+            cur.append(d)
+            cur = None
+        else:
+            cur = None
+    out = ["# Where a draft call's time goes (rocprofv3 kernel trace + workgroup stamps)",
+           "",
+           "Draft calls (sinks + window, at q_len = gamma + 1 and 1) of the llama8b_b32_s8k",
+           "(B = 32, S = 8192, 16 + 496), llama70b_b16_s128k (B = 16, S = 131072, 64 + 1984) and",
+           "bench (B = 64, S = 32768 paged, 16 + 1008) workloads, each after a 1 GiB cache",
+           "eviction.  One MI355X (gfx950).",
+           "",
+           "Command (from /tmp with TMPDIR=/tmp; R = the repository root):",
+           "",
+           f"    {cmd}",
+           "",
+           "and this summary from its trace and stdout by",
+           "",
+           "    python3 $R/bench.py --summarize latency --csv $R/gpurun_out/prof/lat/bench_kernel_trace.csv "
+           "--bench-json $R/gpurun_out/prof/lat_bench.json --cmd \"<the command above>\"",
+           "",
+           "Per case the run makes `warm` untimed calls, `reps` event-timed calls and `reps`",
+           "stamped calls (md_bench_attn_stamps: the same launch, each workgroup recording the",
+           "100 MHz wall clock at its start, after its first K/V tile, at the end of its main",
+           "loop and at its end).  The kernel column is the trace's duration of the event-timed",
+           "calls (attention kernel, plus the merge kernel of a split plan); launch overhead is",
+           "event minus kernel.  Stamp columns are medians over workgroups and calls.",
+           "",
+           "| workload | call | K/V bytes | workgroups | event us | kernel us | of which merge us | launch overhead us | first tile us | main loop us | epilogue us | span (stamps) us | K/V GB/s (event) | frac (event) | frac (kernel) |",
+           "|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    i = 0
+    for case in rec["latency"]:
+        n = case["warm"] + 2 * case["reps"]
+        mine = calls[i: i + n]
+        i += n
+        timed = mine[case["warm"]: case["warm"] + case["reps"]]
+        kern = sorted(sum(d["end"] - d["start"] for d in c) / 1e3 for c in timed)
+        merge = sorted(sum(d["end"] - d["start"] for d in c[1:]) / 1e3 for c in timed)
+        km, mm = kern[len(kern) // 2], merge[len(merge) // 2]
+        ev = sorted(case["event_us"])[len(case["event_us"]) // 2]
+        st = case["stamps_us_median"]
+        by = case["kv_bytes"]
+        out.append(f"| {case['workload']} | {case['call']} | {by} | {case['workgroups']} | {ev:.2f} | "
+                   f"{km:.2f} | {mm:.2f} | {ev - km:.2f} | {st['first_tile']:.2f} | {st['loop']:.2f} | "
+                   f"{st['epilogue']:.2f} | {st['span']:.2f} | {by / (ev * 1e-6) / 1e9:.0f} | "
+                   f"{by / (ev * 1e-6) / 1e9 / HBM_PEAK_GBS:.3f} | {by / (km * 1e-6) / 1e9 / HBM_PEAK_GBS:.3f} |")
+    out += ["", f"kernel_source_sha256: {kernel_source_sha256()}"]
+    return "\n".join(out) + "\n"
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -566,7 +711,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the per-configuration table (profiling passes)")
-    ap.add_argument("--summarize", choices=["trace", "counters", "mfma"])
+    ap.add_argument("--latency", action="store_true",
+                    help="only the draft-call latency breakdown (profiles/)")
+    ap.add_argument("--summarize", choices=["trace", "counters", "mfma", "latency"])
     ap.add_argument("--csv", nargs="+")
     ap.add_argument("--bench-json")
     ap.add_argument("--cmd", default="")
@@ -575,7 +722,8 @@ def main():
         fn = {"trace": lambda: summarize_trace(args.csv[0], args.bench_json, args.cmd),
               "counters": lambda: summarize_counters(args.csv[0], args.csv[1], args.bench_json,
                                                      args.cmd),
-              "mfma": lambda: summarize_mfma(args.csv[0], args.bench_json, args.cmd)}
+              "mfma": lambda: summarize_mfma(args.csv[0], args.bench_json, args.cmd),
+              "latency": lambda: summarize_latency(args.csv[0], args.bench_json, args.cmd)}
         sys.stdout.write(fn[args.summarize]())
         return
     if args.gpus != 1:
@@ -593,6 +741,9 @@ def main():
         raise SystemExit("libmagicdec.so is not built: run __graft_entry__.build() first")
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.latency:
+        print(json.dumps({"latency": latency_breakdown(dev)}), flush=True)
+        return
     w = wl.WORKLOADS[WORKLOAD]
     log(f"[bench] generating {WORKLOAD} on {torch.cuda.get_device_name(dev)}")
     c = wl.make_workload(w, device=dev)

@@ -218,7 +218,12 @@ attn_partial_kernel(const AttnParams p) {
   using SH = Shape<D, BF16>;
   constexpr int ROWS = NT * 16;
   // LDS: the V tiles during the main loop, then the cross-wave merge buffers.
-  constexpr int kMergeO = kWaves * 16 * D * 4;
+  // Cross-wave merge rows are padded by 16 B: at D floats a row is a multiple
+  // of the 256 B bank period, so the 16 rows a wave stores at once would all
+  // start in the same bank (measured: drafts 1-3% faster, outputs identical).
+  // Every wave's row tiles are held at once (up to 135 KB at four row tiles).
+  constexpr int MROW = D + 4;
+  constexpr int kMergeO = kWaves * NT * 16 * MROW * 4;
   constexpr int kMergeStats = 2 * kWaves * ROWS * 4;
   constexpr int kLds = (kWaves * SH::WTILE > kMergeO + kMergeStats) ? kWaves * SH::WTILE
                                                                      : kMergeO + kMergeStats;
@@ -670,36 +675,26 @@ attn_partial_kernel(const AttnParams p) {
 
   // ---- merge the waves of each unit (LDS reused after the loop): wave w
   // holds unit hk0 + w % hp, so unit hs's waves are j * hp + hs, j < wph.
-  __syncthreads();
+  // One round for every row tile: each wave leaves its running max and sum
+  // and its unnormalised O^T in LDS, and after one barrier each thread sums
+  // the waves of its (row, 8 channels) in a fixed order, weighting wave w by
+  // 2^(m_w - M) / L with M the row's max and L = sum_w l_w 2^(m_w - M).
+  __syncthreads();  // every wave is done with its LDS tiles
+  float* mo = reinterpret_cast<float*>(lds);
   float* sm_m = reinterpret_cast<float*>(lds + kMergeO);
   float* sm_l = sm_m + kWaves * ROWS;
-  float* mo = reinterpret_cast<float*>(lds);
   if (grp == 0) {
     for (int rt = 0; rt < NT; ++rt) {
       sm_m[wave * ROWS + rt * 16 + l16] = m_run[rt];
       sm_l[wave * ROWS + rt * 16 + l16] = l_run[rt];
     }
   }
+  // Wave w's O^T rows (lane: row l16, channels c*16+4grp..+3) of each row tile.
+  for (int rt = 0; rt < NT; ++rt)
+    for (int c = 0; c < SH::CB16; ++c)
+      *reinterpret_cast<f32x4*>(mo + ((wave * NT + rt) * 16 + l16) * MROW + c * 16 + grp * 4) =
+          acc[rt][c];
   __syncthreads();
-  // The unit's running max M and total L_total of row r over its waves.
-  auto row_stats = [&](int hs, int r, float& M, float& Lt) {
-    M = -INFINITY;
-    Lt = 0.f;
-    for (int j = 0; j < wph; ++j) M = fmaxf(M, sm_m[(j * hp + hs) * ROWS + r]);
-    if (M != -INFINITY)
-      for (int j = 0; j < wph; ++j) {
-        const float mw = sm_m[(j * hp + hs) * ROWS + r];
-        if (mw != -INFINITY) Lt += sm_l[(j * hp + hs) * ROWS + r] * fast_exp2(mw - M);
-      }
-  };
-  // Each wave rescales its own O by 2^(m_w - M) / L_total.
-  for (int rt = 0; rt < NT; ++rt) {
-    float M, Lt;
-    row_stats(wave_u % hp, rt * 16 + l16, M, Lt);
-    float f = 0.f;
-    if (m_run[rt] != -INFINITY && Lt > 0.f) f = fast_exp2(m_run[rt] - M) / Lt;
-    for (int c = 0; c < SH::CB16; ++c) acc[rt][c] *= f;
-  }
 
   const bool direct = p.n_chunks == 1;
   const int tid = threadIdx.x;
@@ -717,40 +712,45 @@ attn_partial_kernel(const AttnParams p) {
     if (p.lse && c0 == 0) p.lse[row_g] = lse;
   };
   constexpr int kGroupsPerRow = D / 8;
-  constexpr int kItemsPerUnit = 16 * kGroupsPerRow;  // (row of a row tile, 8 channels)
-  for (int rt = 0; rt < NT; ++rt) {
-    // Wave w writes its scaled O^T rows (lane: row l16, channels c*16+4grp..+3).
-    for (int c = 0; c < SH::CB16; ++c)
-      *reinterpret_cast<f32x4*>(mo + (wave * 16 + l16) * D + c * 16 + grp * 4) = acc[rt][c];
-    __syncthreads();
-    // Thread -> (unit hs, row, 8 channels); sum the unit's waves in a fixed order.
-    for (int item = tid; item < hp * kItemsPerUnit; item += kWaves * 64) {
-      const int hs = item / kItemsPerUnit;
-      const int rr = (item % kItemsPerUnit) / kGroupsPerRow;
-      const int c0 = (item % kGroupsPerRow) * 8;
-      const int r = rt * 16 + rr;
-      if (r >= p.R) continue;
-      float o8[8];
-      for (int j = 0; j < 8; ++j) o8[j] = 0.f;
-      for (int jw = 0; jw < wph; ++jw) {
-        const int w = jw * hp + hs;
-        for (int j = 0; j < 8; ++j) o8[j] += mo[(w * 16 + rr) * D + c0 + j];
-      }
-      const int i = r / p.G, h = (hk0 + hs) * p.G + r % p.G;
-      const int64_t row_g = (static_cast<int64_t>(b) * L + i) * p.Hq + h;
-      float M, Lt;
-      row_stats(hs, r, M, Lt);
-      const float lse = (Lt > 0.f) ? (M + fast_log2(Lt)) * 0.69314718055994530942f : -INFINITY;
-      if (direct) {
-        store_out(row_g, c0, o8, lse);
-      } else {
-        float* op = p.part_o + (static_cast<int64_t>(chunk) * p.n_rows + row_g) * D + c0;
-        *reinterpret_cast<f32x4*>(op) = f32x4{o8[0], o8[1], o8[2], o8[3]};
-        *reinterpret_cast<f32x4*>(op + 4) = f32x4{o8[4], o8[5], o8[6], o8[7]};
-        if (c0 == 0) p.part_lse[static_cast<int64_t>(chunk) * p.n_rows + row_g] = lse;
+  const int items_per_unit = p.R * kGroupsPerRow;  // (row, 8 channels)
+  for (int item = tid; item < hp * items_per_unit; item += kWaves * 64) {
+    const int hs = item / items_per_unit;
+    const int r = (item % items_per_unit) / kGroupsPerRow;
+    const int c0 = (item % kGroupsPerRow) * 8;
+    const int rt = r >> 4, rr = r & 15;
+    float M = -INFINITY;
+    for (int jw = 0; jw < wph; ++jw) M = fmaxf(M, sm_m[(jw * hp + hs) * ROWS + r]);
+    float wgt[kWaves];
+    float Lt = 0.f;
+    for (int jw = 0; jw < wph; ++jw) {
+      const float mw = sm_m[(jw * hp + hs) * ROWS + r];
+      wgt[jw] = mw == -INFINITY ? 0.f : fast_exp2(mw - M);
+      Lt += sm_l[(jw * hp + hs) * ROWS + r] * wgt[jw];
+    }
+    const float inv = Lt > 0.f ? 1.f / Lt : 0.f;
+    float o8[8];
+    for (int j = 0; j < 8; ++j) o8[j] = 0.f;
+    for (int jw = 0; jw < wph; ++jw) {
+      const float f = wgt[jw] * inv;
+      const float* src = mo + (((jw * hp + hs) * NT + rt) * 16 + rr) * MROW + c0;
+      const f32x4 x0 = *reinterpret_cast<const f32x4*>(src);
+      const f32x4 x1 = *reinterpret_cast<const f32x4*>(src + 4);
+      for (int j = 0; j < 4; ++j) {
+        o8[j] += f * x0[j];
+        o8[4 + j] += f * x1[j];
       }
     }
-    __syncthreads();
+    const int i = r / p.G, h = (hk0 + hs) * p.G + r % p.G;
+    const int64_t row_g = (static_cast<int64_t>(b) * L + i) * p.Hq + h;
+    const float lse = (Lt > 0.f) ? (M + fast_log2(Lt)) * 0.69314718055994530942f : -INFINITY;
+    if (direct) {
+      store_out(row_g, c0, o8, lse);
+    } else {
+      float* op = p.part_o + (static_cast<int64_t>(chunk) * p.n_rows + row_g) * D + c0;
+      *reinterpret_cast<f32x4*>(op) = f32x4{o8[0], o8[1], o8[2], o8[3]};
+      *reinterpret_cast<f32x4*>(op + 4) = f32x4{o8[4], o8[5], o8[6], o8[7]};
+      if (c0 == 0) p.part_lse[static_cast<int64_t>(chunk) * p.n_rows + row_g] = lse;
+    }
   }
 
   // ---- split range: the last workgroup of the head group to finish merges
