@@ -703,6 +703,101 @@ def summarize_latency(csv_path, bench_json, cmd):
     return "\n".join(out) + "\n"
 
 
+PAGED_AB_CASES = ["paged (seeded random page order)", "paged (pages in sequence order)",
+                  "contiguous"]
+
+
+def paged_ab(dev, warm=2, reps=10):
+    """The bench-shape verify over the same K/V three ways, interleaved in one
+    process: through the workload's page table (pages in seeded random order),
+    through a table whose pages lie in sequence order, and from a contiguous
+    [B, S, Hkv, d] copy.  Each call follows a cache eviction; `warm` rounds
+    are untimed.  Run under rocprofv3 --pmc, the counter summary attributes
+    translation misses and read latency to each case."""
+    import numpy as np
+    import torch
+
+    import paper_2408_11049_amd as md
+    from paper_2408_11049_amd import workloads as wl
+
+    lib = md.load_library()
+    stream = torch.cuda.current_stream(dev)
+    sh = md.ctypes.c_void_p(stream.cuda_stream)
+    buf = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    sink = torch.zeros(4, dtype=torch.float32, device=dev)
+    w = wl.WORKLOADS[WORKLOAD]
+    c = wl.make_workload(w, device=dev)
+    B, S, ps = w.B, w.S, w.page_size
+    pt = c["page_table"].long().view(-1)
+    kc = c["k"][pt].view(B, S, w.Hkv, w.d)
+    vc = c["v"][pt].view(B, S, w.Hkv, w.d)
+    seq_table = torch.arange(B * (S // ps), device=dev, dtype=torch.int32).view(B, -1)
+    kp, vp = kc.view(-1, ps, w.Hkv, w.d), vc.view(-1, ps, w.Hkv, w.d)
+    outs = [torch.empty_like(c["q"]) for _ in PAGED_AB_CASES]
+    kw = dict(max_kv_len=S, return_lse=False)
+    calls = [
+        lambda: md.md_verify_attn(c["q"], c["k"], c["v"], c["kv_lens"], out=outs[0],
+                                  page_table=c["page_table"], **kw),
+        lambda: md.md_verify_attn(c["q"], kp, vp, c["kv_lens"], out=outs[1], page_table=seq_table,
+                                  **kw),
+        lambda: md.md_verify_attn(c["q"], kc, vc, c["kv_lens"], out=outs[2], **kw),
+    ]
+    ev = [[] for _ in calls]
+    for r in range(warm + reps):
+        for i, fn in enumerate(calls):
+            md._check(lib.md_bench_evict(md.ctypes.c_void_p(buf.data_ptr()), buf.numel(),
+                                         md.ctypes.c_void_p(sink.data_ptr()), sh))
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream); fn(); b.record(stream)
+            torch.cuda.synchronize()
+            if r >= warm:
+                ev[i].append(a.elapsed_time(b) * 1e3)
+    same = all(torch.equal(outs[0], o) for o in outs[1:])
+    res = {"cases": PAGED_AB_CASES, "warm": warm, "reps": reps, "bytes": kv_bytes(w, c["kv_lens_np"], "verify", w.q_len),
+           "event_us": [[round(x, 2) for x in e] for e in ev], "outputs_identical": bool(same)}
+    log("[bench] paged A/B: " + ", ".join(f"{n}: {np.median(e):.1f} us" for n, e in zip(PAGED_AB_CASES, ev)))
+    return res
+
+
+def summarize_paged(csv_path, bench_json, cmd):
+    rec = None
+    for line in open(bench_json):
+        if line.strip().startswith("{") and '"paged_ab"' in line:
+            rec = json.loads(line)["paged_ab"]
+    if rec is None:
+        raise SystemExit(f"no paged_ab line in {bench_json}")
+    n = len(rec["cases"])
+    calls = [d for d in _dispatches(_rows(csv_path)) if "attn_partial_kernel" in d["name"]]
+    per = [calls[i::n][rec["warm"]:] for i in range(n)]
+    out = ["# Paged against contiguous K/V: the bench-shape verify (rocprofv3 counters)",
+           "",
+           f"Workload: {WORKLOAD} (B = 64, S = 32768, Hkv = 8, d = 128, bf16, gamma = 4) verified",
+           "three ways over the same K/V values in one process, calls interleaved, each after a",
+           "1 GiB cache eviction: through the workload's 16-token page table (seeded random page",
+           "placement), through a table whose pages lie in sequence order, and from a",
+           "contiguous [B, S, Hkv, d] copy.  Outputs identical in all three: "
+           f"{rec['outputs_identical']}.  One MI355X (gfx950).",
+           "",
+           "Commands (from /tmp with TMPDIR=/tmp; R = the repository root): the times come from",
+           "an unprofiled run, the counters from a second run of the same command under",
+           "rocprofv3 (counter collection serialises the dispatches):",
+           ""]
+    out += [f"    {c}" for c in cmd.split(" ;; ")]
+    out += ["",
+            "| case | event median us | K/V GB/s | UTCL1 translation misses | UTCL1 translation hits | miss rate | TCP->TCC read requests | mean read latency (cycles) |",
+            "|---|---|---|---|---|---|---|---|"]
+    for i, name in enumerate(rec["cases"]):
+        e = sorted(rec["event_us"][i])[len(rec["event_us"][i]) // 2]
+        ds = per[i]
+        avg = lambda k: sum(d.get(k, 0.0) for d in ds) / max(len(ds), 1)
+        miss, hit = avg("TCP_UTCL1_TRANSLATION_MISS_sum"), avg("TCP_UTCL1_TRANSLATION_HIT_sum")
+        req, lat = avg("TCP_TCC_READ_REQ_sum"), avg("TCP_TCC_READ_REQ_LATENCY_sum")
+        out.append(f"| {name} | {e:.2f} | {rec['bytes'] / (e * 1e-6) / 1e9:.0f} | {miss:.4g} | {hit:.4g} | "
+                   f"{miss / max(miss + hit, 1):.4f} | {req:.4g} | {lat / max(req, 1):.1f} |")
+    out += ["", f"kernel_source_sha256: {kernel_source_sha256()}"]
+    return "\n".join(out) + "\n"
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -713,7 +808,9 @@ def main():
                     help="skip the per-configuration table (profiling passes)")
     ap.add_argument("--latency", action="store_true",
                     help="only the draft-call latency breakdown (profiles/)")
-    ap.add_argument("--summarize", choices=["trace", "counters", "mfma", "latency"])
+    ap.add_argument("--paged-ab", action="store_true",
+                    help="only the paged / sequential-page / contiguous verify A/B (profiles/)")
+    ap.add_argument("--summarize", choices=["trace", "counters", "mfma", "latency", "paged"])
     ap.add_argument("--csv", nargs="+")
     ap.add_argument("--bench-json")
     ap.add_argument("--cmd", default="")
@@ -723,7 +820,8 @@ def main():
               "counters": lambda: summarize_counters(args.csv[0], args.csv[1], args.bench_json,
                                                      args.cmd),
               "mfma": lambda: summarize_mfma(args.csv[0], args.bench_json, args.cmd),
-              "latency": lambda: summarize_latency(args.csv[0], args.bench_json, args.cmd)}
+              "latency": lambda: summarize_latency(args.csv[0], args.bench_json, args.cmd),
+              "paged": lambda: summarize_paged(args.csv[0], args.bench_json, args.cmd)}
         sys.stdout.write(fn[args.summarize]())
         return
     if args.gpus != 1:
@@ -743,6 +841,9 @@ def main():
     torch.cuda.set_device(dev)
     if args.latency:
         print(json.dumps({"latency": latency_breakdown(dev)}), flush=True)
+        return
+    if args.paged_ab:
+        print(json.dumps({"paged_ab": paged_ab(dev)}), flush=True)
         return
     w = wl.WORKLOADS[WORKLOAD]
     log(f"[bench] generating {WORKLOAD} on {torch.cuda.get_device_name(dev)}")
@@ -968,21 +1069,27 @@ def main():
                             workspace=ws_acc)
         md.md_kv_commit(sd_lens, acc, L, idx=sd_lists, ring_start=budget, ring_len=ring)
 
-    def sd_timed(run, n=8):
-        ts = []
+    def sd_timed_pair(eager, replay, restore, n=12):
+        """Median step time eagerly and as a graph replay, the two forms
+        alternating (each from the same restored state, after an eviction),
+        so drift over the run affects both alike."""
+        ts = ([], [])
         for _ in range(n):
-            sd_lens.copy_(pos0)
-            sd_lists.copy_(sd_lists0)
-            do_flush()
-            a_ev, b_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a_ev.record(stream); run(); b_ev.record(stream)
-            torch.cuda.synchronize()
-            ts.append(a_ev.elapsed_time(b_ev) * 1e3)
-        return float(np.median(ts))
+            for j, run in enumerate((eager, replay)):
+                restore()
+                do_flush()
+                a_ev, b_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a_ev.record(stream); run(); b_ev.record(stream)
+                torch.cuda.synchronize()
+                ts[j].append(a_ev.elapsed_time(b_ev) * 1e3)
+        return float(np.median(ts[0])), float(np.median(ts[1]))
+
+    def sd_restore():
+        sd_lens.copy_(pos0)
+        sd_lists.copy_(sd_lists0)
 
     sd_step()
     torch.cuda.synchronize()
-    t_sd_eager = sd_timed(sd_step)
     graph = torch.cuda.CUDAGraph()
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
@@ -991,7 +1098,7 @@ def main():
             sd_step()
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
-    t_sd_graph = sd_timed(graph.replay)
+    t_sd_eager, t_sd_graph = sd_timed_pair(sd_step, graph.replay, sd_restore)
 
     # The same selection gathered once into a draft cache of its own
     # (md_kv_gather): a draft step is then verify attention over the 2049
@@ -1040,21 +1147,12 @@ def main():
         md.md_kv_commit(sd_lens, acc, L)
         md.md_kv_commit(g_lens, acc, L)
 
-    def sd_timed_g(run, n=8):
-        ts = []
-        for _ in range(n):
-            sd_lens.copy_(pos0)
-            g_lens.copy_(glen)
-            do_flush()
-            a_ev, b_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a_ev.record(stream); run(); b_ev.record(stream)
-            torch.cuda.synchronize()
-            ts.append(a_ev.elapsed_time(b_ev) * 1e3)
-        return float(np.median(ts))
+    def sdg_restore():
+        sd_lens.copy_(pos0)
+        g_lens.copy_(glen)
 
     sd_step_gathered()
     torch.cuda.synchronize()
-    t_sdg_eager = sd_timed_g(sd_step_gathered)
     graph_g = torch.cuda.CUDAGraph()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
@@ -1062,7 +1160,7 @@ def main():
             sd_step_gathered()
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
-    t_sdg_graph = sd_timed_g(graph_g.replay)
+    t_sdg_eager, t_sdg_graph = sd_timed_pair(sd_step_gathered, graph_g.replay, sdg_restore)
     bytes_gather = 2 * bytes_idx - 2 * w.B * L * w.Hkv * 2 * w.d * w.esize  # rows read + written
     bytes_logits = logits.numel() * logits.element_size()
     # A plain 1 GiB copy of known size: its FETCH_SIZE / WRITE_SIZE readings
@@ -1163,7 +1261,8 @@ def main():
                 w.gamma * t_draft1 + t_append + float(np.mean(tv)) + t_accept + t_commit, 2),
             "t_sd_step_eager_us (gamma x (append 1 + listed draft 1) + append + verify + accept + commit)":
                 round(t_sd_eager, 2),
-            "t_sd_step_graph_us (the same step, one HIP graph replay)": round(t_sd_graph, 2),
+            "t_sd_step_graph_us (the same step, one HIP graph replay; the two forms alternate)":
+                round(t_sd_graph, 2),
             "t_kv_gather_us (the 2049 listed rows into a draft cache, once per prompt)":
                 round(t_gather, 2),
             "kv_gather_bytes (read + write)": bytes_gather,

@@ -360,7 +360,7 @@ int md_kv_append(const md_kv_cache* c, int32_t n_new, const void* k_new, const v
  *   workspace >= md_greedy_accept_workspace_bytes(), 256-byte aligned
  * The argmax is exact (a comparison), so results are bit-exact in any
  * reduction order.  Errors: MD_ERR_INVALID_ARG for NULL or misaligned
- * pointers, n_draft outside [0, 1023], vocab < 1, a bad dtype;
+ * pointers, n_draft outside [0, 1023], vocab outside [1, 2^30], a bad dtype;
  * MD_ERR_WORKSPACE; MD_ERR_HIP.
  */
 int md_greedy_accept(int32_t num_seqs, int32_t n_draft, int32_t vocab, int32_t dtype,

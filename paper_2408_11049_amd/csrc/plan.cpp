@@ -274,7 +274,9 @@ SnapkvPlan make_snapkv_plan(const md_snapkv_args* a, int num_cus) {
 }
 
 int validate_accept(int32_t num_seqs, int32_t n_draft, int32_t vocab, int32_t dtype) {
-  if (num_seqs < 0 || n_draft < 0 || n_draft + 1 > kAcceptMaxRowsPerSeq || vocab < 1)
+  // vocab <= 2^30: a chunk's length, rounded up to 8 elements, stays an int32.
+  if (num_seqs < 0 || n_draft < 0 || n_draft + 1 > kAcceptMaxRowsPerSeq || vocab < 1 ||
+      vocab > (1 << 30))
     return MD_ERR_INVALID_ARG;
   if (dtype != MD_F32 && dtype != MD_BF16) return MD_ERR_INVALID_ARG;
   const int64_t rows = static_cast<int64_t>(num_seqs) * (n_draft + 1);
