@@ -21,9 +21,11 @@
  *     per-device cache of the compute-unit count, a per-process call counter
  *     and, for md_attn_noalloc only, one static scratch buffer per device.
  *     The MD_* tuning overrides (MD_PREFETCH_DEPTH, MD_OCCUPANCY, MD_LPT,
- *     MD_HEADS_PER_WG, MD_FUSED_MERGE, MD_SLOTS_SCALE; for measurement) are
- *     read from the environment on every call; do not change them while
- *     another thread is inside the library.
+ *     MD_HEADS_PER_WG, MD_FUSED_MERGE, MD_SLOTS_SCALE, MD_BALANCED,
+ *     MD_BAL_WG_PER_CU; for measurement) are read from the environment on
+ *     every call, md_workspace_bytes included; do not change them while
+ *     another thread is inside the library, nor between sizing a workspace
+ *     and the call that uses it.
  *   - Errors are return codes (md_status).  Argument errors are detected on
  *     the host before any HIP call, so a failed call has launched nothing.
  *   - Device-side contract violations leave memory in bounds but results
@@ -196,9 +198,14 @@ int md_merge_lse(int32_t n_parts, int64_t n_rows, int32_t head_dim, int32_t out_
  * Workspace bytes an attention call with these arguments needs (0 when the
  * call runs as a single pass).  A split-range call keeps there, per head
  * group, an arrival counter tagged with the call, then every chunk's partial
- * O and lse (the split-KV identity, Sec. 2); whatever the buffer held before
- * is never mistaken for this call's state, so it needs no clearing.  mode is MD_MODE_VERIFY or MD_MODE_DRAFT;
- * n_sink and window are used for MD_MODE_DRAFT only.  Pure host arithmetic on the sizes plus the
+ * O and lse (the split-KV identity, Sec. 2).  A balanced verify (batches of
+ * 2..256 long sequences whose head groups number at most two per compute
+ * unit: every workgroup streams an equal share of all groups' key tiles, so
+ * ragged lengths do not leave units idle) keeps the same counters, then two
+ * partial slots per workgroup for the groups its share cuts.  Whatever the
+ * buffer held before is never mistaken for this call's state, so it needs no
+ * clearing.  mode is MD_MODE_VERIFY or MD_MODE_DRAFT; n_sink and window are
+ * used for MD_MODE_DRAFT only.  Pure host arithmetic on the sizes plus the
  * current device's compute-unit count (256 if no device is visible);
  * pointers in `a` are not read.  Returns 0 for malformed arguments too:
  * the attention call itself reports those.

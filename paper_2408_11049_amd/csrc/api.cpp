@@ -101,6 +101,7 @@ unsigned long long next_call_tag() {
 // Workgroups of an attention launch: a head group per chunk, or, for a
 // longest-first launch that may pair heads, one per unit.
 int64_t grid_size(const Plan& pl, int lpt) {
+  if (pl.bal) return pl.bal_nw;
   return (lpt && pl.hp == 2) ? pl.n_units : pl.n_groups * pl.n_chunks;
 }
 
@@ -108,7 +109,7 @@ int64_t grid_size(const Plan& pl, int lpt) {
 
 int64_t attn_grid_size(const md_attn_args* a, int mode, int n_sink, int window) {
   const Plan pl = make_plan(a, mode, n_sink, window, device_cu_count());
-  return grid_size(pl, longest_first(mode, pl.n_chunks, a->num_seqs, a->max_kv_len));
+  return grid_size(pl, !pl.bal && longest_first(mode, pl.n_chunks, a->num_seqs, a->max_kv_len));
 }
 
 // The attention entry points.  `workspace`/`workspace_bytes` override the
@@ -171,7 +172,8 @@ int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void*
   p.n_chunks = pl.n_chunks;
   p.chunk_len = pl.chunk_len;
   p.num_seqs = a->num_seqs;
-  p.lpt = longest_first(mode, pl.n_chunks, a->num_seqs, a->max_kv_len);
+  p.lpt = !pl.bal && longest_first(mode, pl.n_chunks, a->num_seqs, a->max_kv_len);
+  p.bal = pl.bal;
   p.hp = pl.hp;
   p.err = a->err_word;
   const int64_t n_blocks = grid_size(pl, p.lpt);
@@ -185,7 +187,7 @@ int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void*
   p.o = a->o;
   p.lse = a->lse;
   p.n_rows = pl.n_rows;
-  if (pl.n_chunks > 1) {
+  if (pl.n_chunks > 1 || pl.bal) {
     unsigned char* ws = static_cast<unsigned char*>(workspace);
     p.counters = reinterpret_cast<unsigned long long*>(ws);
     p.part_o = reinterpret_cast<float*>(ws + pl.counter_bytes);

@@ -162,6 +162,106 @@ __device__ __forceinline__ int lpt_group(const P& p, int r, int* sl, int& hp) {
   return b * gps + r % gps;
 }
 
+// Balanced verify (p.bal).  The tiles of every head group -- group g =
+// b * gps + j owns tiles_b = max(1, ceil(S_b / kTile)) of them, groups in
+// order -- form one stream of TT tiles, cut into gridDim.x ranges of equal
+// length, one per workgroup: every workgroup streams the same number of
+// tiles (to within one) whatever the lengths, and keeps the head pairs that
+// read a token row's neighbouring runs together.  A group that a range
+// boundary cuts is computed in pieces by consecutive workgroups, which merge
+// them (the split-KV identity); with NW = min(workgroups, TT) ranges, stream
+// tile t belongs to workgroup ((t + 1) NW - 1) / TT, whose range starts at
+// w TT / NW.  Only a range's first and last pieces can be cut, so workgroup
+// w keeps the partials of its first piece in slot 2w and of its last in
+// slot 2w + 1.
+struct BalCursor {
+  int lo;      // this workgroup's range [lo, hi)
+  int t, hi;   // its next stream tile and the end of its range
+  int b, j;    // the current group: sequence b, its group j
+  int g0, gt;  // the group's first stream tile and its number of tiles
+  int TT;      // tiles in the whole stream
+  int NW;      // workgroups sharing it: min(grid, TT), so no range is empty
+};
+
+template <typename P>
+__device__ __forceinline__ int bal_tiles(const P& p, int b) {
+  int s = min(p.kv_lens[b], p.max_kv_len);
+  s = s < 0 ? 0 : s;
+  return max(1, (s + kTile - 1) / kTile);
+}
+
+__device__ __forceinline__ int bal_owner(int t, int nw, int tt) {
+  return static_cast<int>((static_cast<int64_t>(t + 1) * nw - 1) / tt);
+}
+
+// The workgroup's range and its first group; false for an empty range.  sl:
+// LDS for kLptMaxSeqs + 1 ints (free again on return).
+template <typename P>
+__device__ bool bal_start(const P& p, int gps, int* sl, BalCursor& c) {
+  const int B = p.num_seqs;  // <= kLptMaxSeqs
+  if (threadIdx.x < 64) {    // wave 0: stream tiles per sequence, inclusive scan
+    constexpr int kPer = kLptMaxSeqs / 64;
+    int v[kPer];
+    int local = 0;
+    for (int e = 0; e < kPer; ++e) {
+      const int bb = static_cast<int>(threadIdx.x) * kPer + e;
+      v[e] = bb < B ? bal_tiles(p, bb) * gps : 0;
+      local += v[e];
+    }
+    int incl = local;
+    for (int o = 1; o < 64; o <<= 1) {
+      const int x = __shfl_up(incl, o);
+      if (static_cast<int>(threadIdx.x) >= o) incl += x;
+    }
+    int run = incl - local;
+    for (int e = 0; e < kPer; ++e) {
+      run += v[e];
+      sl[threadIdx.x * kPer + e] = run;
+    }
+  }
+  __syncthreads();
+  const int tt = sl[B - 1];
+  // At least one tile per range: a group's pieces then come from consecutive
+  // workgroups with no empty one between them (their count is its arrivals).
+  const int nw = min(static_cast<int>(gridDim.x), tt);
+  if (static_cast<int>(blockIdx.x) >= nw) return false;  // uniform over the workgroup
+  const int lo = static_cast<int>(static_cast<int64_t>(blockIdx.x) * tt / nw);
+  const int hi = static_cast<int>(static_cast<int64_t>(blockIdx.x + 1) * tt / nw);
+  for (int bb = threadIdx.x; bb < B; bb += kWaves * 64) {
+    const int ex = bb ? sl[bb - 1] : 0;
+    if (ex <= lo && lo < sl[bb]) sl[kLptMaxSeqs] = bb;
+  }
+  __syncthreads();
+  const int b = sl[kLptMaxSeqs];
+  const int ex = b ? sl[b - 1] : 0;
+  __syncthreads();  // the LDS is reused by the tiles
+  const int tb = bal_tiles(p, b);
+  c.TT = tt;
+  c.NW = nw;
+  c.lo = lo;
+  c.t = lo;
+  c.hi = hi;
+  c.b = b;
+  c.j = (lo - ex) / tb;
+  c.g0 = ex + c.j * tb;
+  c.gt = tb;
+  return true;
+}
+
+// Moves to the workgroup's next piece; false when its range is done.
+template <typename P>
+__device__ __forceinline__ bool bal_next(const P& p, int gps, BalCursor& c) {
+  c.t = min(c.hi, c.g0 + c.gt);
+  if (c.t >= c.hi) return false;
+  c.g0 += c.gt;
+  if (++c.j == gps) {
+    c.j = 0;
+    ++c.b;
+    c.gt = bal_tiles(p, c.b);
+  }
+  return true;
+}
+
 // Contract checks for a caller that passes an error word (debug use), ahead
 // of the K/V stream; they change no result.  The lengths are checked once per
 // sequence (its first head group's first chunk).  Paged: the page id of every
@@ -211,8 +311,10 @@ __device__ void check_contract(const P& p, const U& u, int b, int chunk, bool fi
 // visible range is a per-(sequence, kv head) list of prompt positions
 // followed by the speculated tokens (the listed draft), else the causal
 // prefix (verify) or sinks then windows (draft); P: K/V tiles in flight per
-// wave; OCC: waves per SIMD the instance is compiled for.
-template <int D, bool BF16, int NT, bool PAGED, bool IDX, int P, int OCC>
+// wave; OCC: waves per SIMD the instance is compiled for; BAL: the balanced
+// verify (a workgroup takes an equal share of all groups' tiles, piece by
+// piece; its own instances, so the others keep their register budget).
+template <int D, bool BF16, int NT, bool PAGED, bool IDX, int P, int OCC, bool BAL>
 __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(OCC)))
 attn_partial_kernel(const AttnParams p) {
   using SH = Shape<D, BF16>;
@@ -253,23 +355,34 @@ attn_partial_kernel(const AttnParams p) {
   // Wave-uniform by construction; readfirstlane lets the compiler keep the
   // unit's address arithmetic in scalar registers.
   int hp_sel = p.hp;
-  int group_sel;
-  if (p.lpt) {
+  int group_sel = 0;
+  BalCursor bc{};
+  if constexpr (BAL) {
+    if (!bal_start(p, p.Hkv / p.hp, reinterpret_cast<int*>(lds), bc)) return;
+  } else if (p.lpt) {
     group_sel = lpt_group(p, static_cast<int>(blockIdx.x), reinterpret_cast<int*>(lds), hp_sel);
     if (group_sel < 0) return;
   } else {
     group_sel = static_cast<int>(blockIdx.x) % n_grp;
   }
   const int hp = __builtin_amdgcn_readfirstlane(hp_sel);
-  const int group = __builtin_amdgcn_readfirstlane(group_sel);
   const int wph = kWaves / hp;
   const int gps = p.Hkv / hp;
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   const int wslot = wave_u / hp;
+  const int L = p.L;
+
+  // One pass per piece: a balanced workgroup takes the pieces of its range
+  // in turn; every other launch has exactly one.
+  for (;;) {
+  const int group = __builtin_amdgcn_readfirstlane(BAL ? bc.b * gps + bc.j : group_sel);
   const int b = group / gps;
   const int hk0 = (group % gps) * hp;
   const int hk = hk0 + wave_u % hp;
-  const int L = p.L;
+  // A balanced piece: tiles [lt0, lt1) of its group; whole when it is all of it.
+  const int lt0 = __builtin_amdgcn_readfirstlane(bc.t - bc.g0);
+  const int lt1 = __builtin_amdgcn_readfirstlane(min(bc.hi, bc.g0 + bc.gt) - bc.g0);
+  const bool bal_whole = lt0 == 0 && lt1 == bc.gt;
 
   // ---- the unit's visible range: the causal prefix, sinks then windows, or the list
   UnitGeom u;
@@ -292,8 +405,13 @@ attn_partial_kernel(const AttnParams p) {
       U = p.n_sink + (u.S - lo);
     }
   }
-  u.v_begin = chunk * p.chunk_len;
-  u.v_end = min(U, u.v_begin + p.chunk_len);
+  if constexpr (BAL) {
+    u.v_begin = lt0 * kTile;
+    u.v_end = min(U, lt1 * kTile);
+  } else {
+    u.v_begin = chunk * p.chunk_len;
+    u.v_end = min(U, u.v_begin + p.chunk_len);
+  }
   const int n_tiles = u.v_end > u.v_begin ? (u.v_end - u.v_begin + kTile - 1) / kTile : 0;
 
   // ---- per-lane query rows: row r = rt*16 + l16 is (i = r / G, head hk*G + r % G)
@@ -645,7 +763,8 @@ attn_partial_kernel(const AttnParams p) {
   };
 
   if (p.err)
-    check_contract<PAGED, IDX>(p, u, b, chunk, hk0 == 0, wslot == 0, idxrow, lane);
+    check_contract<PAGED, IDX>(p, u, b, BAL ? (lt0 == 0 ? 0 : 1) : chunk, hk0 == 0, wslot == 0,
+                               idxrow, lane);
 
   // Prologue: this wave's first P tiles in flight; the token locations of
   // the P tiles after them.
@@ -696,8 +815,25 @@ attn_partial_kernel(const AttnParams p) {
           acc[rt][c];
   __syncthreads();
 
-  const bool direct = p.n_chunks == 1;
+  const bool direct = BAL ? bal_whole : p.n_chunks == 1;
   const int tid = threadIdx.x;
+  // Partial results: chunk k of a split plan at row k * n_rows + row_g; piece
+  // k of a cut balanced group -- the piece of workgroup w0 + k, its
+  // workgroups being w0 .. w1 -- in that workgroup's slot, 2w for its range's
+  // first piece (every piece but possibly w0's) and 2w + 1 for its last,
+  // rows hs * R + r.
+  const int bal_w0 = BAL ? bal_owner(bc.g0, bc.NW, bc.TT) : 0;
+  const int bal_w1 = BAL ? bal_owner(bc.g0 + bc.gt - 1, bc.NW, bc.TT) : 0;
+  // w0's piece is the first of its range when the range starts with the group.
+  const int bal_w0_last =
+      BAL ? static_cast<int>(static_cast<int64_t>(bal_w0) * bc.TT / bc.NW != bc.g0) : 0;
+  const int n_parts = BAL ? bal_w1 - bal_w0 + 1 : p.n_chunks;
+  const int my_part = BAL ? static_cast<int>(blockIdx.x) - bal_w0 : chunk;
+  auto part_row = [&](int k, int hs, int r, int64_t row_g) -> int64_t {
+    return BAL ? (static_cast<int64_t>(2 * (bal_w0 + k) + (k == 0 ? bal_w0_last : 0)) * hp + hs) *
+                         p.R + r
+               : static_cast<int64_t>(k) * p.n_rows + row_g;
+  };
   // Final O (8 channels from c0 of row row_g, in the input dtype) and lse.
   auto store_out = [&](int64_t row_g, int c0, const float* o8, float lse) {
     if constexpr (BF16) {
@@ -746,10 +882,11 @@ attn_partial_kernel(const AttnParams p) {
     if (direct) {
       store_out(row_g, c0, o8, lse);
     } else {
-      float* op = p.part_o + (static_cast<int64_t>(chunk) * p.n_rows + row_g) * D + c0;
+      const int64_t prow = part_row(my_part, hs, r, row_g);
+      float* op = p.part_o + prow * D + c0;
       *reinterpret_cast<f32x4*>(op) = f32x4{o8[0], o8[1], o8[2], o8[3]};
       *reinterpret_cast<f32x4*>(op + 4) = f32x4{o8[4], o8[5], o8[6], o8[7]};
-      if (c0 == 0) p.part_lse[static_cast<int64_t>(chunk) * p.n_rows + row_g] = lse;
+      if (c0 == 0) p.part_lse[prow] = lse;
     }
   }
 
@@ -761,7 +898,7 @@ attn_partial_kernel(const AttnParams p) {
   // arrival count: a value from any other call (or uninitialised memory)
   // counts as zero arrivals, so the workspace needs no clearing; the last
   // arrival resets it to 0.
-  if (!direct && !p.merge_launch) {
+  if (!direct && (BAL || !p.merge_launch)) {
     // Every wave waits until its partial stores are performed at the L2
     // (vmcnt 0), the barrier lines the waves up, and one device-scope release
     // fence (an L2 write-back on gfx950) then publishes them all before the
@@ -781,7 +918,7 @@ attn_partial_kernel(const AttnParams p) {
         next = (p.tag << 16) | (seen + 1);
       } while (!__hip_atomic_compare_exchange_weak(ctr, &cur, next, __ATOMIC_RELAXED,
                                                    __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-      const int last = (next & 0xffffull) == static_cast<unsigned long long>(p.n_chunks);
+      const int last = (next & 0xffffull) == static_cast<unsigned long long>(n_parts);
       if (last) __hip_atomic_store(ctr, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if (last) MD_PARTIAL_ACQUIRE();  // the other chunks' partials, as their workgroups left them
       *is_last = last;
@@ -797,24 +934,24 @@ attn_partial_kernel(const AttnParams p) {
         const int c0 = (item % kGroupsPerRow) * 8;
         const int i = r / p.G, h = (hk0 + hs) * p.G + r % p.G;
         const int64_t row_g = (static_cast<int64_t>(b) * L + i) * p.Hq + h;
-        const float* lp = p.part_lse + row_g;
         float mx = -INFINITY;
-        for (int k = 0; k < p.n_chunks; ++k) mx = fmaxf(mx, lp[static_cast<int64_t>(k) * p.n_rows]);
+        for (int k = 0; k < n_parts; ++k) mx = fmaxf(mx, p.part_lse[part_row(k, hs, r, row_g)]);
         float o8[8];
         for (int j = 0; j < 8; ++j) o8[j] = 0.f;
         float lse = -INFINITY;
         if (mx != -INFINITY) {
           float tot = 0.f;
-          for (int k = 0; k < p.n_chunks; ++k) {
-            const float l = lp[static_cast<int64_t>(k) * p.n_rows];
+          for (int k = 0; k < n_parts; ++k) {
+            const float l = p.part_lse[part_row(k, hs, r, row_g)];
             if (l != -INFINITY) tot += fast_exp2((l - mx) * kLog2e);
           }
           lse = mx + fast_log2(tot) * kLn2;
-          for (int k = 0; k < p.n_chunks; ++k) {
-            const float l = lp[static_cast<int64_t>(k) * p.n_rows];
+          for (int k = 0; k < n_parts; ++k) {
+            const int64_t prow = part_row(k, hs, r, row_g);
+            const float l = p.part_lse[prow];
             if (l == -INFINITY) continue;  // an empty chunk: its O is not read
             const float wk = fast_exp2((l - lse) * kLog2e);
-            const float* op = p.part_o + (static_cast<int64_t>(k) * p.n_rows + row_g) * D + c0;
+            const float* op = p.part_o + prow * D + c0;
             const f32x4 x0 = *reinterpret_cast<const f32x4*>(op);
             const f32x4 x1 = *reinterpret_cast<const f32x4*>(op + 4);
             for (int j = 0; j < 4; ++j) {
@@ -827,20 +964,28 @@ attn_partial_kernel(const AttnParams p) {
       }
     }
   }
+  if constexpr (!BAL) {
+    break;
+  } else {
+    if (!bal_next(p, gps, bc)) break;
+  }
+  __syncthreads();  // the next piece reuses the LDS
+  }  // pieces
   stamp(3);
 }
 
 // ---------------------------------------------------------------------------
 // Host-side dispatch over the compiled instances.
 
-template <int D, bool BF16, int NT, bool IDX, int P, int OCC>
+template <int D, bool BF16, int NT, bool IDX, int P, int OCC, bool BAL = false>
 static hipError_t launch_p(const AttnParams& p, bool paged, int64_t n_blocks, hipStream_t s) {
   dim3 grid(static_cast<uint32_t>(n_blocks)), block(kWaves * 64);
   if (paged)
-    hipLaunchKernelGGL((attn_partial_kernel<D, BF16, NT, true, IDX, P, OCC>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((attn_partial_kernel<D, BF16, NT, true, IDX, P, OCC, BAL>), grid, block, 0,
+                       s, p);
   else
-    hipLaunchKernelGGL((attn_partial_kernel<D, BF16, NT, false, IDX, P, OCC>), grid, block, 0, s,
-                       p);
+    hipLaunchKernelGGL((attn_partial_kernel<D, BF16, NT, false, IDX, P, OCC, BAL>), grid, block, 0,
+                       s, p);
   return hipGetLastError();
 }
 
@@ -852,6 +997,15 @@ static hipError_t launch_p(const AttnParams& p, bool paged, int64_t n_blocks, hi
 template <int D, bool BF16, int NT, bool IDX>
 static hipError_t launch_nt(const AttnParams& p, bool paged, int depth, int occ,
                             int64_t n_blocks, hipStream_t s) {
+  if constexpr (!IDX) {
+    // The balanced verify: one tile in flight, the verify's default waves per
+    // SIMD (two for one row tile of bf16, else one).
+    if (p.bal) {
+      (void)depth;
+      (void)occ;
+      return launch_p<D, BF16, NT, IDX, 1, (BF16 && NT == 1) ? 2 : 1, true>(p, paged, n_blocks, s);
+    }
+  }
   if constexpr (BF16) {
     if constexpr (!IDX && NT <= 3)
       if (depth >= 2) return launch_p<D, BF16, NT, IDX, 2, 1>(p, paged, n_blocks, s);

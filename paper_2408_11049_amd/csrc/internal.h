@@ -32,6 +32,9 @@ constexpr int kMaxChunks = 65535;    // a split plan's arrival count fits 16 bit
 // the sequences by length, so it is kept to small batches of long caches.
 constexpr int kLptMaxSeqs = 256;
 constexpr int kLptMinLen = 4096;
+// The balanced verify (same launches as longest-first) keeps its partial
+// results within this much workspace, else longest-first is used.
+constexpr size_t kBalMaxWorkspace = size_t{20} << 20;
 
 struct Plan {
   int32_t G = 0;         // Hq / Hkv
@@ -44,6 +47,11 @@ struct Plan {
   int64_t n_units = 0;   // B * Hkv
   int32_t hp = 1;        // units (adjacent kv heads) per workgroup
   int64_t n_groups = 0;  // n_units / hp; the grid is n_groups * n_chunks
+  // Balanced verify: bal_nw workgroups take equal shares of every group's
+  // tiles; the workspace holds a counter per group and 2 bal_nw partial
+  // slots of hp * R rows.
+  bool bal = false;
+  int32_t bal_nw = 0;
   // Workspace of a split plan, in this order (each part 256-byte aligned):
   size_t counter_bytes = 0;  // [n_groups] uint64 arrival counters (tagged; never cleared)
   size_t part_o_bytes = 0;   // [n_chunks][n_rows][d] fp32 partial O

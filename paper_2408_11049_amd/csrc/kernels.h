@@ -45,6 +45,8 @@ struct AttnParams {
   int64_t n_rows;
   int32_t num_seqs;           // B
   int32_t lpt;                // 1: workgroups take sequences longest first (see attn.hip)
+  int32_t bal;                // 1: the balanced verify instances (see attn.hip): grid = workgroups
+                              // sharing all groups' tiles equally; partials at slot group + workgroup
   int32_t hp;                 // kv heads per workgroup (1 or 2; divides Hkv)
   int32_t hp_auto;            // longest-first launch of one workgroup per unit that
                               // pairs heads when the lengths allow (see attn.hip)

@@ -187,6 +187,45 @@ Plan make_plan(const md_attn_args* a, int mode, int n_sink, int window, int num_
   split_units(U, p.n_groups, slots, &n_chunks, &chunk_len);
   p.n_chunks = static_cast<int32_t>(n_chunks);
   p.chunk_len = static_cast<int32_t>(chunk_len);
+  // Balanced verify: where the units alone fill the device and lengths may
+  // differ (the cases longest-first dispatch serves), every workgroup takes
+  // an equal share of all head groups' tiles, in pairs of adjacent kv heads
+  // when the head count is even.  Only with at most two head groups per
+  // compute unit: there the longest sequence sets the makespan of one group
+  // per workgroup, while with more groups per unit the hardware dispatcher
+  // already evens the load out and the extra pieces only add prologues.
+  // MD_BALANCED = 1 / 2 turns it off / on wherever allowed (measurement).
+  const int bal_knob = env_knob("MD_BALANCED", 1, 2);
+  const int bal_hp =
+      (a->num_kv_heads % 2 == 0 && env_knob("MD_HEADS_PER_WG", 1, 2) != 1) ? 2 : 1;
+  const int64_t cus = num_cus > 0 ? num_cus : 256;
+  if (mode == MD_MODE_VERIFY && p.n_chunks == 1 && a->num_seqs >= 2 &&
+      a->num_seqs <= kLptMaxSeqs && bal_knob != 1 &&
+      (bal_knob == 2 ||
+       (a->max_kv_len >= kLptMinLen && p.n_units / bal_hp <= 2 * cus))) {
+    const int hp = bal_hp;
+    const int64_t groups = p.n_units / hp;
+    // One workgroup per compute unit: every range then streams at once.
+    // MD_BAL_WG_PER_CU = 2 doubles them (measurement).
+    const int64_t wpc = std::max(1, env_knob("MD_BAL_WG_PER_CU", 1, 2));
+    const int64_t nw = cus * wpc;
+    const int64_t tiles = ceil_div(a->max_kv_len, kTile) * (a->num_kv_heads / hp);
+    const size_t slots = static_cast<size_t>(2 * nw);  // a first and a last piece per workgroup
+    const size_t ctr = align_up(static_cast<size_t>(groups) * 8, 256);
+    const size_t po = align_up(slots * hp * p.R * a->head_dim * 4, 256);
+    const size_t pl = align_up(slots * hp * p.R * 4, 256);
+    if (tiles * a->num_seqs < (int64_t{1} << 30) && ctr + po + pl <= kBalMaxWorkspace) {
+      p.bal = true;
+      p.hp = hp;
+      p.n_groups = groups;
+      p.bal_nw = static_cast<int32_t>(nw);
+      p.counter_bytes = ctr;
+      p.part_o_bytes = po;
+      p.part_lse_bytes = pl;
+      p.workspace_bytes = ctr + po + pl;
+      return p;
+    }
+  }
   if (p.n_chunks > 1) {
     p.counter_bytes = align_up(static_cast<size_t>(p.n_groups) * 8, 256);
     p.part_o_bytes = align_up(static_cast<size_t>(n_chunks) * p.n_rows * a->head_dim * 4, 256);

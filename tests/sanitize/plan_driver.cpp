@@ -67,7 +67,12 @@ void plan_invariants(const md_attn_args& a, int mode, int n_sink, int window) {
   check(p.NT >= 1 && p.NT <= 4, "row tiles", p.NT);
   check(p.hp == 1 || p.hp == 2, "heads per workgroup", p.hp);
   check(p.n_groups * p.hp == p.n_units, "groups x hp = units", p.n_groups, p.n_units);
-  if (p.n_chunks > 1)
+  if (p.bal) {
+    check(mode == MD_MODE_VERIFY && p.n_chunks == 1 && p.bal_nw > 0, "balanced verify plan");
+    check(p.workspace_bytes <= md::kBalMaxWorkspace, "balanced workspace bound",
+          static_cast<long long>(p.workspace_bytes));
+  }
+  if (p.n_chunks > 1 || p.bal)
     check(p.workspace_bytes >= p.counter_bytes + p.part_o_bytes + p.part_lse_bytes,
           "workspace parts", static_cast<long long>(p.workspace_bytes));
   else

@@ -232,9 +232,39 @@ def test_workspace_required_and_checked(lib):
     assert lib.md_verify_attn(ctypes.byref(a), None) == md.MD_ERR_WORKSPACE  # not 256-aligned
 
 
-def test_workspace_zero_when_units_fill_the_device(lib):
-    # 64 sequences x 8 kv heads = 512 units >= two per compute unit: one pass.
+def test_workspace_zero_when_units_fill_the_device(lib, monkeypatch):
+    # 64 sequences x 8 kv heads = 512 units >= two per compute unit: one pass
+    # (the balanced verify off; on, it keeps partials of the groups it cuts).
+    monkeypatch.setenv("MD_BALANCED", "1")
     a = good_args(num_seqs=64, num_kv_heads=8, num_q_heads=32, q_len=5, max_kv_len=32768)
+    assert lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1) == 0
+    assert lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_DRAFT, 16, 1008) == 0
+
+
+@pytest.mark.parametrize("B,Hkv,Hq,L,hp,default_on", [
+    (64, 8, 32, 5, 2, True),     # 256 head pairs: one per compute unit
+    (128, 3, 12, 4, 1, True),    # odd head count: single heads, 384 groups
+    (256, 8, 32, 3, 2, False),   # 1024 pairs, four per unit: dispatch balances
+    (256, 8, 32, 5, 2, False),
+])
+def test_balanced_verify_workspace(lib, monkeypatch, B, Hkv, Hq, L, hp, default_on):
+    """The balanced verify (the units fill the device, lengths up to 32768,
+    at most two head groups per compute unit unless forced): one 8-byte
+    counter per head group, then two partial slots per workgroup (its range's
+    first and last pieces) of hp * G * L rows; one workgroup per compute unit
+    (256 on this host)."""
+    a = good_args(num_seqs=B, num_kv_heads=Hkv, num_q_heads=Hq, q_len=L, max_kv_len=32768,
+                  kv_stride_tok=Hkv * 128, kv_stride_blk=32768 * Hkv * 128)
+    groups, R = B * Hkv // hp, Hq // Hkv * L
+    nw = 256
+    up = lambda x: (x + 255) // 256 * 256
+    want = up(groups * 8) + up(2 * nw * hp * R * 128 * 4) + up(2 * nw * hp * R * 4)
+    monkeypatch.delenv("MD_BALANCED", raising=False)
+    got = lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1)
+    assert got == (want if default_on else 0)
+    monkeypatch.setenv("MD_BALANCED", "2")
+    assert lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1) == want
+    monkeypatch.setenv("MD_BALANCED", "1")
     assert lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1) == 0
 
 

@@ -26,10 +26,11 @@ SETTINGS = [
     {}, {"MD_PREFETCH_DEPTH": "2"}, {"MD_PREFETCH_DEPTH": "3"}, {"MD_OCCUPANCY": "1"},
     {"MD_OCCUPANCY": "2"}, {"MD_LPT": "1"}, {"MD_LPT": "2"}, {"MD_HEADS_PER_WG": "1"},
     {"MD_HEADS_PER_WG": "2"}, {"MD_FUSED_MERGE": "1"}, {"MD_SLOTS_SCALE": "2"},
-    {"MD_SLOTS_SCALE": "4"},
+    {"MD_SLOTS_SCALE": "4"}, {"MD_BALANCED": "1"}, {"MD_BALANCED": "2"},
+    {"MD_BALANCED": "2", "MD_BAL_WG_PER_CU": "2"},
 ]
 KNOBS = ["MD_PREFETCH_DEPTH", "MD_OCCUPANCY", "MD_LPT", "MD_HEADS_PER_WG", "MD_FUSED_MERGE",
-         "MD_SLOTS_SCALE"]
+         "MD_SLOTS_SCALE", "MD_BALANCED", "MD_BAL_WG_PER_CU"]
 
 # name, mode, B, L, Hq, Hkv, d, lens, page, n_sink, window, budget
 CASES = [
@@ -63,7 +64,8 @@ def _case(i):
 
 @pytest.mark.parametrize("ci", range(len(CASES)), ids=[c[0] for c in CASES])
 @pytest.mark.parametrize("setting", SETTINGS,
-                         ids=["default"] + ["%s=%s" % next(iter(s.items())) for s in SETTINGS[1:]])
+                         ids=["default"] + ["+".join("%s=%s" % kv for kv in s.items())
+                                            for s in SETTINGS[1:]])
 def test_setting_against_oracle(setting, ci, monkeypatch):
     for k in KNOBS:
         monkeypatch.delenv(k, raising=False)
