@@ -9,7 +9,8 @@ Llama-3.1-8B layer shape at B = 64, S = 32768 in a 16-token paged cache,
 gamma = 4, draft budget 16 sinks + 1008 window; inputs are seeded synthetic
 N(0, 1) values already resident in HBM.
 
-Timing: W untimed warm-up steps, then exactly K steps between two
+Timing: 80 untimed verify calls (~100 ms: the clocks settle after the
+host-side setup), W untimed warm-up steps, then exactly K steps between two
 synchronisations.  Inside each step the caches are evicted before each call
 by reading a 1 GiB buffer with cache-allocating loads (cold cache; a fill
 would leave dirty lines whose write-back the timed call pays for -- both are
@@ -55,6 +56,7 @@ sys.path.insert(0, ROOT)
 
 WORKLOAD = "llama8b_b64_s32k_paged"
 HBM_PEAK_GBS = 8000.0
+SETTLE_CALLS = 80  # untimed verify calls before the warm-up steps (see settle())
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 PROFILES = os.path.join(ROOT, "profiles")
 PROFILE_TRACE = os.path.join(PROFILES, "attn_verify_llama8b_b64_s32k_paged_trace.md")
@@ -147,8 +149,9 @@ def read_trace():
 # ---------------------------------------------------------------------------
 # Profile summaries (--summarize): turn a rocprofv3 run of this script into the
 # markdown under profiles/.  The attention dispatches of a run come in a fixed
-# order -- W warm-up steps, then the K timed steps, each a verify call then a
-# draft call -- so the timed calls are picked by ordinal, not by guesswork.
+# order -- the settling verify calls (their count is in the bench line), W
+# warm-up steps, then the K timed steps, each a verify call then a draft call
+# -- so the timed calls are picked by ordinal, not by guesswork.
 
 def _rows(path):
     with open(path, newline="") as f:
@@ -173,9 +176,18 @@ def _dispatches(rows):
     return [out[k] for k in sorted(out)]
 
 
-def timed_calls(dispatches, warmup, steps):
+def settle_count(rec):
+    """The untimed verify calls a bench line says ran before its warm-up."""
+    for k, v in rec.get("detail", {}).items():
+        if k.startswith("settle_calls"):
+            return int(v)
+    return 0
+
+
+def timed_calls(dispatches, warmup, steps, settle=0):
     """The timed verify and draft calls: lists of dispatch groups (an
-    attention dispatch plus a merge dispatch that follows it, if any)."""
+    attention dispatch plus a merge dispatch that follows it, if any), after
+    `settle` untimed verify calls and `warmup` warm-up steps."""
     calls, cur = [], None
     for d in dispatches:
         if "attn_partial_kernel" in d["name"]:
@@ -186,10 +198,10 @@ def timed_calls(dispatches, warmup, steps):
             cur = None
         else:
             cur = None
-    need = 2 * (warmup + steps)
+    need = settle + 2 * (warmup + steps)
     if len(calls) < need:
         raise SystemExit(f"only {len(calls)} attention calls; expected at least {need}")
-    timed = calls[2 * warmup: need]
+    timed = calls[settle + 2 * warmup: need]
     return timed[0::2], timed[1::2]
 
 
@@ -203,8 +215,8 @@ def _bench_line(path):
 
 def summarize_trace(csv_path, bench_json, cmd):
     rec = _bench_line(bench_json)
-    W, K = rec["warmup"], rec["steps"]
-    ver, dra = timed_calls(_dispatches(_rows(csv_path)), W, K)
+    W, K, S0 = rec["warmup"], rec["steps"], settle_count(rec)
+    ver, dra = timed_calls(_dispatches(_rows(csv_path)), W, K, S0)
     det = rec["detail"]
     ev = {"verify": det["t_verify_us"], "draft": det["t_draft_us"]}
     alg = {"verify": det["verify_kv_bytes"], "draft": det["draft_kv_bytes"]}
@@ -219,17 +231,20 @@ def summarize_trace(csv_path, bench_json, cmd):
            "",
            f"    {cmd}",
            "",
-           f"Selection: bench.py runs W = {W} warm-up steps and then K = {K} timed steps, each",
-           "a verify call followed by a draft call, before any other attention call, so in",
-           "launch order the attention dispatches go verify, draft, verify, draft, ...  The",
-           f"timed verify calls are attention dispatches {2 * W}, {2 * W + 2}, ..., "
-           f"{2 * (W + K) - 2} (0-based), the",
-           f"timed draft calls {2 * W + 1}, ..., {2 * (W + K) - 1}; a merge dispatch that follows a call",
+           f"Selection: bench.py runs {S0} untimed verify calls (settling the clocks), then",
+           f"W = {W} warm-up steps and K = {K} timed steps, each a verify call followed by a",
+           "draft call, before any other attention call, so in launch order the attention",
+           "dispatches go verify x settle, then verify, draft, verify, draft, ...  The",
+           f"timed verify calls are attention dispatches {S0 + 2 * W}, {S0 + 2 * W + 2}, ..., "
+           f"{S0 + 2 * (W + K) - 2} (0-based), the",
+           f"timed draft calls {S0 + 2 * W + 1}, ..., {S0 + 2 * (W + K) - 1}; a merge dispatch that "
+           "follows a call",
            "(split plans only) counts with it.",
            "",
            "| call | kernel | timed calls | kernel mean us | min | max | event mean us (bench line) | kernel / event | K/V GB/s (kernel) | frac of 8 TB/s (kernel) | frac (event) |",
            "|---|---|---|---|---|---|---|---|---|---|---|"]
-    fields = {"kernel_source_sha256": kernel_source_sha256(), "warmup": W, "steps": K}
+    fields = {"kernel_source_sha256": kernel_source_sha256(), "settle": S0, "warmup": W,
+              "steps": K}
     for name, calls in (("verify", ver), ("draft", dra)):
         durs = [sum((d["end"] - d["start"]) for d in c) / 1e3 for c in calls]
         kn = sorted({_short(d["name"]) for c in calls for d in c})
@@ -269,7 +284,7 @@ def summarize_trace(csv_path, bench_json, cmd):
 
 def summarize_counters(fetch_csv, write_csv, bench_json, cmd):
     rec = _bench_line(bench_json)
-    W, K = rec["warmup"], rec["steps"]
+    W, K, S0 = rec["warmup"], rec["steps"], settle_count(rec)
     det = rec["detail"]
     alg = {"verify": det["verify_kv_bytes"], "draft": det["draft_kv_bytes"]}
     res = {}
@@ -280,7 +295,7 @@ def summarize_counters(fetch_csv, write_csv, bench_json, cmd):
         if not copies:
             raise SystemExit(f"{path}: no md_bench_copy dispatch to calibrate {ctr}")
         calib[ctr] = copies[-1][ctr]
-        ver, dra = timed_calls(ds, W, K)
+        ver, dra = timed_calls(ds, W, K, S0)
         for name, calls in (("verify", ver), ("draft", dra)):
             vals = [sum(d[ctr] for d in c) for c in calls]
             res[(name, ctr)] = (sum(vals) / len(vals), sorted({_short(d["name"]) for c in calls for d in c}))
@@ -301,13 +316,13 @@ def summarize_counters(fetch_csv, write_csv, bench_json, cmd):
             f"bytes = KiB x 1024 x scale with scale_fetch = {scale['FETCH_SIZE']:.5f}, "
             f"scale_write = {scale['WRITE_SIZE']:.5f}.",
             "",
-            "The timed calls are picked as in the kernel-trace summary (the warm-up steps, then",
-            f"the timed steps of a verify and a draft call each; here W = {W}, K = {K}); each row",
-            "averages over the K timed calls.",
+            "The timed calls are picked as in the kernel-trace summary (the settling verify calls,",
+            "the warm-up steps, then the timed steps of a verify and a draft call each; here",
+            f"{S0} settling calls, W = {W}, K = {K}); each row averages over the K timed calls.",
             "",
             "| call | kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | HBM bytes read | HBM bytes written | algorithmic K/V bytes | read / algorithmic |",
             "|---|---|---|---|---|---|---|---|"]
-    fields = {"kernel_source_sha256": kernel_source_sha256(), "warmup": W, "steps": K,
+    fields = {"kernel_source_sha256": kernel_source_sha256(), "settle": S0, "warmup": W, "steps": K,
               "scale_fetch": round(scale["FETCH_SIZE"], 6), "scale_write": round(scale["WRITE_SIZE"], 6)}
     for name in ("verify", "draft"):
         f_kib, kn = res[(name, "FETCH_SIZE")]
@@ -327,9 +342,9 @@ def summarize_counters(fetch_csv, write_csv, bench_json, cmd):
 
 def summarize_mfma(csv_path, bench_json, cmd):
     rec = _bench_line(bench_json)
-    W, K = rec["warmup"], rec["steps"]
+    W, K, S0 = rec["warmup"], rec["steps"], settle_count(rec)
     cfg = rec["config"]
-    ver, dra = timed_calls(_dispatches(_rows(csv_path)), W, K)
+    ver, dra = timed_calls(_dispatches(_rows(csv_path)), W, K, S0)
     tr = read_trace()
     out = ["# MFMA use of the bench's verify and draft calls (rocprofv3 counters)",
            "",
@@ -355,7 +370,8 @@ def summarize_mfma(csv_path, bench_json, cmd):
     u_draft = min(cfg["S"], cfg["n_sink"] + cfg["gamma"] + cfg["window"])  # sinks + union of windows
     design = {"verify": cfg["B"] * cfg["Hkv"] * (-(-cfg["S"] // 32) * 32) * per_key,
               "draft": cfg["B"] * cfg["Hkv"] * (-(-u_draft // 32) * 32) * per_key}
-    fields = {"kernel_source_sha256": kernel_source_sha256(), "warmup": W, "steps": K}
+    fields = {"kernel_source_sha256": kernel_source_sha256(), "settle": S0, "warmup": W,
+              "steps": K}
     for name, calls in (("verify", ver), ("draft", dra)):
         fl = sum(sum(d.get("MfmaFlopsBF16", 0.0) for d in c) for c in calls) / len(calls)
         ut = sum(sum(d.get("MfmaUtil", 0.0) for d in c) for c in calls) / len(calls)
@@ -499,7 +515,29 @@ def cpu_oracle_extras(c, w, logits, draft_tok, q_obs, n_obs, t_accept_us, t_vote
             "snapkv_votes_gpu_speedup": round(t_votes_all / (t_votes_us * 1e-6), 1)}
 
 
-def config_table(w_names, dev, timed, verbose=True):
+def settle(fn, flush_fn, ms, sync, min_calls=5):
+    """Untimed: eviction + fn back to back for at least `ms` milliseconds of
+    wall time and at least `min_calls` calls (ms = 0: exactly min_calls, so a
+    profiled run's dispatch ordinals do not depend on its speed),
+    synchronising every few calls.  After
+    host-side setup or a phase of short calls leaves HBM lightly loaded, the
+    first ~15-20 ms of HBM-bound launches run up to ~20% slower on MI355X
+    (measured: a ragged B = 64 verify falls from 1161 us to ~950 us over its
+    first 15 calls, then stays); timed regions start from the steady state of
+    a serving loop instead.  Returns the number of calls."""
+    n = 0
+    t_end = time.perf_counter() + ms * 1e-3
+    while n < min_calls or (ms > 0 and time.perf_counter() < t_end):
+        flush_fn()
+        fn()
+        n += 1
+        if n % 4 == 0:
+            sync()
+    sync()
+    return n
+
+
+def config_table(w_names, dev, timed, verbose=True, settle_fn=None):
     """Cold-cache medians (p10, p50, p90 of 10 calls) of every configuration in
     the workload list: verify and draft at q_len = gamma + 1 and 1, t_step,
     t_SD = gamma t_draft(1) + t_verify (the attention part of Eq. 2's step
@@ -534,6 +572,7 @@ def config_table(w_names, dev, timed, verbose=True):
         }
         for fn in calls.values():
             fn()
+        n_settle = settle_fn(calls["verify"]) if settle_fn else 0
         t = {k: timed(fn, n=10, stats=True) for k, fn in calls.items()}
         by = {"verify": kv_bytes(w, lens, "verify", L), "verify_qlen1": kv_bytes(w, lens, "verify", 1),
               "draft": kv_bytes(w, lens, "draft", L), "draft_qlen1": kv_bytes(w, lens, "draft", 1)}
@@ -549,6 +588,7 @@ def config_table(w_names, dev, timed, verbose=True):
         row["t_step_us (verify + draft)"] = round(t["verify"][1] + t["draft"][1], 2)
         row["t_sd_us (gamma x draft_qlen1 + verify)"] = round(w.gamma * t["draft_qlen1"][1] + t["verify"][1], 2)
         row["verify_ratio_qlen_gamma1_vs_1"] = round(t["verify"][1] / t["verify_qlen1"][1], 4)
+        row["settle_calls (untimed verify calls first, >= 60 ms)"] = n_settle
         table[name] = row
         if verbose:
             log(f"[bench]   verify {t['verify'][1]:.1f} us ({row['verify_frac']:.3f})  draft "
@@ -902,7 +942,11 @@ def main():
     bytes_v = kv_bytes(w, lens, "verify", L)
     bytes_d = kv_bytes(w, lens, "draft", L)
 
-    log(f"[bench] warmup {args.warmup} steps")
+    # The host-side setup above (generation, hashing) leaves the GPU idle for
+    # seconds: settle its clocks with SETTLE_CALLS untimed verify calls
+    # (~100 ms) before the warm-up steps (see settle()).
+    n_settle = settle(verify, do_flush, 0, torch.cuda.synchronize, min_calls=SETTLE_CALLS)
+    log(f"[bench] settled with {n_settle} untimed verify calls; warmup {args.warmup} steps")
     for _ in range(args.warmup):
         do_flush(); verify()
         do_flush(); draft()
@@ -1196,7 +1240,8 @@ def main():
                 "mfma": mfma}
     configs = None
     if not args.no_configs:
-        configs = config_table(CONFIGS, dev, timed)
+        configs = config_table(CONFIGS, dev, timed,
+                               settle_fn=lambda fn: settle(fn, do_flush, 60, torch.cuda.synchronize))
         configs[WORKLOAD + " (headline: the event means above)"] = {
             "t_verify_us_p10_p50_p90": [round(float(x), 2) for x in np.percentile(tv, [10, 50, 90])],
             "t_verify_qlen1_us": round(t_verify1, 2),
@@ -1232,6 +1277,7 @@ def main():
         "inputs_sha256": inputs,
         "detail": {
             "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
+            "settle_calls (untimed verify calls before the warm-up)": n_settle,
             "t_verify_us": round(float(np.mean(tv)), 2),
             "t_verify_us_p10_p50_p90": [round(float(x), 2) for x in np.percentile(tv, [10, 50, 90])],
             "t_draft_us": round(float(np.mean(td)), 2),

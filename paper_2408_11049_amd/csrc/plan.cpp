@@ -206,9 +206,11 @@ Plan make_plan(const md_attn_args* a, int mode, int n_sink, int window, int num_
     const int hp = bal_hp;
     const int64_t groups = p.n_units / hp;
     // One workgroup per compute unit: every range then streams at once.
-    // MD_BAL_WG_PER_CU = 2 doubles them (measurement).
+    // MD_BAL_WG_PER_CU = 2 doubles them, MD_BAL_NW sets their number
+    // (measurement).
     const int64_t wpc = std::max(1, env_knob("MD_BAL_WG_PER_CU", 1, 2));
-    const int64_t nw = cus * wpc;
+    const int64_t nw_forced = env_knob("MD_BAL_NW", 1, 4096);
+    const int64_t nw = nw_forced ? nw_forced : cus * wpc;
     const int64_t tiles = ceil_div(a->max_kv_len, kTile) * (a->num_kv_heads / hp);
     const size_t slots = static_cast<size_t>(2 * nw);  // a first and a last piece per workgroup
     const size_t ctr = align_up(static_cast<size_t>(groups) * 8, 256);

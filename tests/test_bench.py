@@ -68,13 +68,14 @@ def _trace_csv(path, names_durs):
 
 
 def test_trace_summary_picks_the_timed_calls(tmp_path):
-    """W warm-up steps then K timed steps, each verify then draft, each after an
-    eviction read: the summary takes attention calls 2W .. 2(W+K)-1 only (a
-    merge dispatch counts with its call), whatever runs after them."""
+    """S settling verify calls, W warm-up steps, then K timed steps, each verify
+    then draft, each after an eviction read: the summary takes attention calls
+    S + 2W .. S + 2(W+K)-1 only (a merge dispatch counts with its call),
+    whatever runs after them."""
     V, D = "void md::attn_partial_kernel<128, true, 2, true, false, 1, 1>(md::AttnParams)", \
         "void md::attn_partial_kernel<128, true, 2, true, false, 1, 2>(md::AttnParams)"
     M, E = "void md::merge_lse_kernel<128, true>(int, long, float const*)", "md::bench_evict_kernel"
-    seq = []
+    seq = [(E, 100), (V, 1500)] * 4  # four settling verify calls, untimed
     for step in range(2 + 3):  # W = 2, K = 3
         seq += [(E, 100), (V, 900 if step < 2 else 1000 + step), (E, 100), (D, 50), (M, 4)]
     seq += [(V, 5.0), (D, 7.0)]  # later calls of the same templates are not timed
@@ -83,7 +84,7 @@ def test_trace_summary_picks_the_timed_calls(tmp_path):
     line = {"metric": "m", "value": 1, "unit": "GB/s", "steps": 3, "warmup": 2, "ms_per_step": 1,
             "roofline": {"achieved": 1, "frac": 0.5, "algorithmic_bytes_per_launch": 8e9},
             "detail": {"t_verify_us": 1010.0, "t_draft_us": 60.0, "verify_kv_bytes": 8e9,
-                       "draft_kv_bytes": 2.7e8}}
+                       "draft_kv_bytes": 2.7e8, "settle_calls (untimed verify calls)": 4}}
     bj = tmp_path / "b.json"
     bj.write_text("noise\n" + __import__("json").dumps(line) + "\n")
     md_text = bench.summarize_trace(str(csv_path), str(bj), "cmd")
