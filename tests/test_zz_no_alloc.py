@@ -82,3 +82,43 @@ def test_noalloc_single_pass_and_refusals():
     with pytest.raises(ValueError):
         md.md_attn_noalloc(md.MD_MODE_DRAFT_INDEXED, c["q"], c["k"], c["v"], c["kv_lens"],
                            out=o, lse=l, **_kw(c))
+
+
+def _check_units(c, o, l, units, what):
+    """Sampled (sequence, kv head) units against the fp64 oracle, one at a time."""
+    G = c["Hq"] // c["Hkv"]
+    for b, hk in units:
+        q, k, v, S = wl.gather_unit(c, b, hk)
+        ro, rl = oracle.attention(oracle.VERIFY, q, k, v, S)
+        compare(_f64(o[b: b + 1, :, hk * G: (hk + 1) * G]),
+                l[b: b + 1, :, hk * G: (hk + 1) * G].cpu().numpy().astype(np.float64), ro, rl,
+                "bf16", f"{what} unit ({b},{hk})")
+
+
+def test_noalloc_balanced_verify(monkeypatch):
+    """Two balanced verify calls in a row (64 ragged sequences x 8 kv heads =
+    256 head pairs, lengths past 4096: the plan that streams equal shares of
+    all groups and merges the groups its ranges cut), the second smaller:
+    bit for bit against md_verify_attn, and sampled units against the oracle."""
+    monkeypatch.delenv("MD_BALANCED", raising=False)
+    big = _case(64, 4, 32, 8, [4096 + (i * 613) % 3000 for i in range(64)], 16, 404)
+    small = _case(64, 1, 32, 8, [4096 + (i * 211) % 900 for i in range(64)], 0, 405)
+    for c in (big, small):
+        need = md.md_workspace_bytes(c["q"], c["k"], c["v"], c["kv_lens"], **_kw(c))
+        assert 0 < need <= md.MD_NOALLOC_SCRATCH_BYTES, need  # the balanced plan, in the scratch
+    got = [_buffers(big), _buffers(small)]
+    torch.cuda.synchronize()
+    mem0 = torch.cuda.memory_allocated(DEV)
+    say("[no-alloc] balanced verify: large call then small call")
+    for c, (o, l) in zip((big, small), got):
+        md.md_attn_noalloc(oracle.VERIFY, c["q"], c["k"], c["v"], c["kv_lens"], out=o, lse=l,
+                           **_kw(c))
+    torch.cuda.synchronize()
+    assert torch.cuda.memory_allocated(DEV) == mem0
+    for c, (o, l), name in zip((big, small), got, ("large", "small")):
+        ro, rl = _buffers(c)
+        md.md_verify_attn(c["q"], c["k"], c["v"], c["kv_lens"], out=ro, lse=rl, **_kw(c))
+        torch.cuda.synchronize()
+        assert torch.equal(o.view(torch.int16), ro.view(torch.int16)), f"{name}: O differs"
+        assert torch.equal(l, rl), f"{name}: lse differs"
+        _check_units(c, o, l, [(0, 0), (17, 5), (40, 2), (63, 7)], f"no-alloc balanced {name}")
