@@ -58,8 +58,11 @@ md_attn_args good_args(int B, int L, int Hq, int Hkv, int d, int64_t S, int page
   return a;
 }
 
+int g_bal_plans = 0;
+
 void plan_invariants(const md_attn_args& a, int mode, int n_sink, int window) {
   const md::Plan p = md::make_plan(&a, mode, n_sink, window, 256);
+  g_bal_plans += p.bal ? 1 : 0;
   check(p.n_chunks >= 1, "n_chunks >= 1", p.n_chunks);
   check(p.chunk_len >= md::kTile && p.chunk_len % md::kTile == 0, "chunk_len tiles", p.chunk_len);
   check(static_cast<int64_t>(p.n_chunks) * p.chunk_len >= p.U_max, "chunks cover the range",
@@ -124,6 +127,18 @@ int main() {
                           static_cast<int64_t>(md::kMaxPosition)};
   const int batches[] = {1, 2, 3, 16, 64, 255, 256, 4096, 1 << 16};
   const int heads[][2] = {{4, 1}, {8, 2}, {32, 8}, {64, 8}, {16, 16}, {64, 1}};
+  // The sweep runs with the default plan choice, then with the balanced
+  // verify forced wherever allowed, and with its range count at the knob's
+  // extremes (one range; 4096 ranges).
+  const char* const bal_env[][2] = {{nullptr, nullptr}, {"MD_BALANCED", "2"},
+                                    {"MD_BAL_NW", "1"}, {"MD_BAL_NW", "4096"}};
+  int bal_per_pass[4] = {0, 0, 0, 0};
+  for (int pass = 0; pass < 4; ++pass) {
+  unsetenv("MD_BALANCED");
+  unsetenv("MD_BAL_NW");
+  if (bal_env[pass][0]) setenv(bal_env[pass][0], bal_env[pass][1], 1);
+  if (pass >= 2) setenv("MD_BALANCED", "2", 1);
+  const int bal_before = g_bal_plans;
   for (int64_t S : lens)
     for (int B : batches)
       for (const auto& hh : heads)
@@ -140,6 +155,19 @@ int main() {
             }
           }
         }
+  bal_per_pass[pass] = g_bal_plans - bal_before;
+  }
+  unsetenv("MD_BALANCED");
+  unsetenv("MD_BAL_NW");
+  // Default choice: B = 64 x 8 kv heads at S >= 4096 is balanced; forced,
+  // more shapes are.
+  check(bal_per_pass[0] > 0, "default sweep reaches balanced plans", bal_per_pass[0]);
+  check(bal_per_pass[1] > bal_per_pass[0], "forced sweep reaches more balanced plans",
+        bal_per_pass[1], bal_per_pass[0]);
+  check(bal_per_pass[2] > 0 && bal_per_pass[3] > 0, "range-count extremes plan",
+        bal_per_pass[2], bal_per_pass[3]);
+  printf("balanced plans per pass: %d %d %d %d\n", bal_per_pass[0], bal_per_pass[1],
+         bal_per_pass[2], bal_per_pass[3]);
 
   // ---- SnapKV, acceptance and cache validators over edge sizes
   for (int32_t n : {0, 1, 32, 256, INT32_MAX}) {

@@ -43,6 +43,9 @@ def test_plan_code_under_sanitizers(tmp_path):
                        env={**os.environ, "ASAN_OPTIONS": "detect_leaks=1:abort_on_error=0"})
     assert r.returncode == 0, r.stdout + r.stderr
     assert "plan driver: ok" in r.stdout
+    # Every pass of the sweep reached balanced-verify plans (the driver
+    # checks the counts; the line shows them).
+    assert "balanced plans per pass:" in r.stdout
 
 
 def test_oracle_pins_under_sanitizers(tmp_path):
