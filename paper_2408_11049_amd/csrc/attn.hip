@@ -997,14 +997,18 @@ static hipError_t launch_p(const AttnParams& p, bool paged, int64_t n_blocks, hi
 template <int D, bool BF16, int NT, bool IDX>
 static hipError_t launch_nt(const AttnParams& p, bool paged, int depth, int occ,
                             int64_t n_blocks, hipStream_t s) {
-  if constexpr (!IDX) {
-    // The balanced verify: one tile in flight, the verify's default waves per
-    // SIMD (two for one row tile of bf16, else one).
+  // The balanced verify: one tile in flight, the verify's default waves per
+  // SIMD (two for one row tile of bf16, else one).  Compiled only where its
+  // piece loop fits the registers without spilling (bf16 up to three row
+  // tiles, fp32 up to two); the planner never chooses it elsewhere.
+  if constexpr (!IDX && NT <= kBalMaxNT(BF16)) {
     if (p.bal) {
       (void)depth;
       (void)occ;
       return launch_p<D, BF16, NT, IDX, 1, (BF16 && NT == 1) ? 2 : 1, true>(p, paged, n_blocks, s);
     }
+  } else {
+    if (p.bal) return hipErrorInvalidValue;
   }
   if constexpr (BF16) {
     if constexpr (!IDX && NT <= 3)

@@ -33,8 +33,14 @@ constexpr int kMaxChunks = 65535;    // a split plan's arrival count fits 16 bit
 constexpr int kLptMaxSeqs = 256;
 constexpr int kLptMinLen = 4096;
 // The balanced verify (same launches as longest-first) keeps its partial
-// results within this much workspace, else longest-first is used.
-constexpr size_t kBalMaxWorkspace = size_t{20} << 20;
+// results within this much workspace, else longest-first is used: enough
+// for one workgroup per compute unit on 256 of them at up to three row tiles
+// of head pairs (25.4 MB at 48 rows), and within the static scratch of the
+// entry point that allocates nothing.
+constexpr size_t kBalMaxWorkspace = size_t{30} << 20;
+// Row tiles up to which the balanced verify runs (its instances spill
+// registers beyond): three for bf16, two for fp32.
+constexpr int kBalMaxNT(bool bf16) { return bf16 ? 3 : 2; }
 
 struct Plan {
   int32_t G = 0;         // Hq / Hkv

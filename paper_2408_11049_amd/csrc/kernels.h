@@ -46,7 +46,8 @@ struct AttnParams {
   int32_t num_seqs;           // B
   int32_t lpt;                // 1: workgroups take sequences longest first (see attn.hip)
   int32_t bal;                // 1: the balanced verify instances (see attn.hip): grid = workgroups
-                              // sharing all groups' tiles equally; partials at slot group + workgroup
+                              // sharing all groups' tiles equally; workgroup w keeps the partials
+                              // of its range's first / last piece in slots 2w / 2w + 1
   int32_t hp;                 // kv heads per workgroup (1 or 2; divides Hkv)
   int32_t hp_auto;            // longest-first launch of one workgroup per unit that
                               // pairs heads when the lengths allow (see attn.hip)

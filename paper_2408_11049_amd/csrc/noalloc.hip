@@ -23,6 +23,8 @@ namespace md {
 namespace {
 
 __device__ __align__(256) unsigned char scratch[MD_NOALLOC_SCRATCH_BYTES];
+static_assert(kBalMaxWorkspace <= MD_NOALLOC_SCRATCH_BYTES,
+              "every balanced verify plan must fit the static scratch");
 
 constexpr int kMaxDevices = 64;
 std::atomic<void*> g_scratch[kMaxDevices];

@@ -200,7 +200,7 @@ Plan make_plan(const md_attn_args* a, int mode, int n_sink, int window, int num_
       (a->num_kv_heads % 2 == 0 && env_knob("MD_HEADS_PER_WG", 1, 2) != 1) ? 2 : 1;
   const int64_t cus = num_cus > 0 ? num_cus : 256;
   if (mode == MD_MODE_VERIFY && p.n_chunks == 1 && a->num_seqs >= 2 &&
-      a->num_seqs <= kLptMaxSeqs && bal_knob != 1 &&
+      a->num_seqs <= kLptMaxSeqs && bal_knob != 1 && p.NT <= kBalMaxNT(a->dtype == MD_BF16) &&
       (bal_knob == 2 ||
        (a->max_kv_len >= kLptMinLen && p.n_units / bal_hp <= 2 * cus))) {
     const int hp = bal_hp;

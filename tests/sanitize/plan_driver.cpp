@@ -72,6 +72,7 @@ void plan_invariants(const md_attn_args& a, int mode, int n_sink, int window) {
   check(p.n_groups * p.hp == p.n_units, "groups x hp = units", p.n_groups, p.n_units);
   if (p.bal) {
     check(mode == MD_MODE_VERIFY && p.n_chunks == 1 && p.bal_nw > 0, "balanced verify plan");
+    check(p.NT <= md::kBalMaxNT(a.dtype == MD_BF16), "balanced verify row tiles", p.NT);
     check(p.workspace_bytes <= md::kBalMaxWorkspace, "balanced workspace bound",
           static_cast<long long>(p.workspace_bytes));
   }

@@ -268,6 +268,22 @@ def test_balanced_verify_workspace(lib, monkeypatch, B, Hkv, Hq, L, hp, default_
     assert lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1) == 0
 
 
+@pytest.mark.parametrize("forced", [None, "2"])
+def test_balanced_verify_not_beyond_three_row_tiles(lib, monkeypatch, forced):
+    """64 query rows per kv head (G = 4, q_len = 16: four row tiles) stay on the
+    single-pass plan, forced or not: the balanced instances are compiled only
+    up to three row tiles of bf16, where their piece loop does not spill."""
+    if forced:
+        monkeypatch.setenv("MD_BALANCED", forced)
+    else:
+        monkeypatch.delenv("MD_BALANCED", raising=False)
+    a = good_args(num_seqs=64, num_kv_heads=8, num_q_heads=32, q_len=16, max_kv_len=32768,
+                  kv_stride_tok=8 * 128, kv_stride_blk=32768 * 8 * 128)
+    assert lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1) == 0
+    a.q_len = 12  # 48 rows, three row tiles: balanced
+    assert lib.md_workspace_bytes(ctypes.byref(a), md.MD_MODE_VERIFY, 0, 1) > 0
+
+
 def _split_bytes(n_chunks, n_rows, d, groups):
     """A split plan's workspace: one 8-byte arrival counter per head group,
     then the partial O and lse, each part 256-byte aligned."""
