@@ -838,6 +838,50 @@ def summarize_paged(csv_path, bench_json, cmd):
     return "\n".join(out) + "\n"
 
 
+LDS_COUNTERS = ["SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE", "SQ_LDS_ADDR_CONFLICT",
+                "SQ_LDS_UNALIGNED_STALL", "SQ_INSTS_LDS", "SQ_WAIT_INST_LDS", "SQ_ACTIVE_INST_LDS"]
+
+
+def summarize_lds(csv_path, bench_json, cmd):
+    """LDS counters per kernel instance (means per dispatch over every dispatch
+    of that instance in the run), the bench's timed verify and draft named."""
+    rec = _bench_line(bench_json)
+    W, K, S0 = rec["warmup"], rec["steps"], settle_count(rec)
+    ds = _dispatches(_rows(csv_path))
+    ver, dra = timed_calls(ds, W, K, S0)
+    role = {ver[0][0]["name"]: "verify (bench)", dra[0][0]["name"]: "draft (bench)"}
+    groups = {}
+    for d in ds:
+        if not d.get("SQ_LDS_IDX_ACTIVE") or "bench_" in d["name"]:
+            continue  # kernels without LDS traffic (copies, fills) and the bench helpers
+        groups.setdefault(d["name"], []).append(d)
+    out = ["# LDS counters of the bench's kernels (rocprofv3 --pmc)",
+           "",
+           f"Workload: {WORKLOAD} (Llama-3.1-8B layer shape, B = 64, S = 32768, 16-token pages,",
+           "gamma = 4) and the extra calls the bench times on it (one-token calls, the listed",
+           "draft, SnapKV at prefill, the speculative-step kernels).  One MI355X (gfx950).",
+           "Means per dispatch over every dispatch of each kernel instance, summed over the",
+           "device as rocprofv3 reports them.",
+           "",
+           "Command (from /tmp with TMPDIR=/tmp; R = the repository root):",
+           "",
+           f"    {cmd}",
+           "",
+           "| kernel | dispatches | SQ_INSTS_LDS | SQ_LDS_IDX_ACTIVE (cycles) | SQ_LDS_BANK_CONFLICT (cycles) | conflict / active | SQ_LDS_ADDR_CONFLICT | SQ_LDS_UNALIGNED_STALL |",
+           "|---|---|---|---|---|---|---|---|"]
+    for name, dl in sorted(groups.items(), key=lambda kv: -sum(d.get("SQ_LDS_IDX_ACTIVE", 0) for d in kv[1])):
+        m = {c: sum(d.get(c, 0.0) for d in dl) / len(dl) for c in LDS_COUNTERS}
+        ratio = m["SQ_LDS_BANK_CONFLICT"] / m["SQ_LDS_IDX_ACTIVE"] if m["SQ_LDS_IDX_ACTIVE"] else 0.0
+        label = (role[name] + " " if name in role else "") + f"`{_short(name)}`"
+        out.append(f"| {label} | {len(dl)} | {m['SQ_INSTS_LDS']:.4g} | {m['SQ_LDS_IDX_ACTIVE']:.4g} | "
+                   f"{m['SQ_LDS_BANK_CONFLICT']:.4g} | {ratio:.3f} | {m['SQ_LDS_ADDR_CONFLICT']:.4g} | "
+                   f"{m['SQ_LDS_UNALIGNED_STALL']:.4g} |")
+    snap = os.path.join(ROOT, "paper_2408_11049_amd", "csrc", "snapkv.hip")
+    out += ["", f"kernel_source_sha256: {kernel_source_sha256()}",
+            f"snapkv_source_sha256: {kernel_source_sha256([snap])}"]
+    return "\n".join(out) + "\n"
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -850,7 +894,7 @@ def main():
                     help="only the draft-call latency breakdown (profiles/)")
     ap.add_argument("--paged-ab", action="store_true",
                     help="only the paged / sequential-page / contiguous verify A/B (profiles/)")
-    ap.add_argument("--summarize", choices=["trace", "counters", "mfma", "latency", "paged"])
+    ap.add_argument("--summarize", choices=["trace", "counters", "mfma", "latency", "paged", "lds"])
     ap.add_argument("--csv", nargs="+")
     ap.add_argument("--bench-json")
     ap.add_argument("--cmd", default="")
@@ -861,7 +905,8 @@ def main():
                                                      args.cmd),
               "mfma": lambda: summarize_mfma(args.csv[0], args.bench_json, args.cmd),
               "latency": lambda: summarize_latency(args.csv[0], args.bench_json, args.cmd),
-              "paged": lambda: summarize_paged(args.csv[0], args.bench_json, args.cmd)}
+              "paged": lambda: summarize_paged(args.csv[0], args.bench_json, args.cmd),
+              "lds": lambda: summarize_lds(args.csv[0], args.bench_json, args.cmd)}
         sys.stdout.write(fn[args.summarize]())
         return
     if args.gpus != 1:

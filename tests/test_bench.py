@@ -94,3 +94,36 @@ def test_trace_summary_picks_the_timed_calls(tmp_path):
     assert float(fields["draft_kernel_mean_us"]) == pytest.approx(54.0)  # attention + merge
     assert fields["kernel_source_sha256"] == bench.kernel_source_sha256()
     assert "WARNING" not in md_text
+
+
+def test_lds_summary_groups_by_kernel(tmp_path):
+    """--summarize lds: per-instance means of the LDS counters, the bench's
+    timed verify and draft instances named, kernels without LDS traffic and the
+    bench helpers left out."""
+    import csv
+    V, D = "void md::attn_partial_kernel<128, true, 2, true, false, 1, 1, true>(md::AttnParams)", \
+        "void md::attn_partial_kernel<128, true, 2, true, false, 1, 2, false>(md::AttnParams)"
+    E, C = "md::bench_evict_kernel", "at::native::copy_kernel"
+    seq = [(E, 0, 0), (V, 100, 10)] * 2  # two settling verify calls
+    for step in range(1 + 2):            # W = 1, K = 2
+        seq += [(E, 0, 0), (V, 100, 10), (E, 0, 0), (D, 40, 8), (C, 0, 0)]
+    path = tmp_path / "c.csv"
+    with open(path, "w", newline="") as f:
+        wr = csv.writer(f)
+        wr.writerow(["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
+        for i, (n, active, conflict) in enumerate(seq):
+            for ctr in bench.LDS_COUNTERS:
+                val = {"SQ_LDS_IDX_ACTIVE": active, "SQ_LDS_BANK_CONFLICT": conflict}.get(ctr, 1.0)
+                wr.writerow([i + 1, n, ctr, val if n not in (E, C) else 0.0])
+    line = {"metric": "m", "value": 1, "unit": "GB/s", "steps": 2, "warmup": 1,
+            "detail": {"settle_calls (untimed verify calls)": 2}}
+    bj = tmp_path / "b.json"
+    bj.write_text(__import__("json").dumps(line) + "\n")
+    text = bench.summarize_lds(str(path), str(bj), "cmd")
+    rows = [l for l in text.splitlines() if l.startswith("| ") and "attn_partial" in l]
+    assert len(rows) == 2
+    v = next(r for r in rows if r.startswith("| verify (bench)"))
+    d = next(r for r in rows if r.startswith("| draft (bench)"))
+    assert "| 5 |" in v and "| 0.100 |" in v  # 2 settling + 3 step calls, 10 / 100
+    assert "| 3 |" in d and "| 0.200 |" in d
+    assert "bench_evict" not in text and "copy_kernel" not in text
