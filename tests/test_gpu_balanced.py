@@ -9,8 +9,10 @@ units -- each computed alone from the unit's own keys -- and, over every
 element, with the longest-first launch of the same call (a different
 decomposition: both within the dtype's tolerance of each other).  The cases
 cover every compiled balanced instance (one, two and three row tiles of
-bf16, both head dims, fp32), the smallest batch, and a forced plan over
-tiny ragged groups whose tile stream is shorter than the grid.
+bf16, both head dims, fp32), the smallest batch, a forced plan over tiny
+ragged groups whose tile stream is shorter than the grid, and 16 seeded
+random problems (batch, heads, head dim, q_len, lengths from below one tile
+to a few thousand, paged or contiguous) forced onto the balanced plan.
 """
 import zlib
 
@@ -86,3 +88,23 @@ def test_balanced_verify(case, monkeypatch):
         ro, rl = oracle.attention(oracle.VERIFY, q, k, v, S)
         compare(got_o[b: b + 1, :, hk * G: (hk + 1) * G], got_l[b: b + 1, :, hk * G: (hk + 1) * G],
                 ro, rl, dtype, f"{name} unit ({b},{hk})")
+
+
+def _random_case(seed):
+    """A seeded problem whose head groups fill the device (at least 512 units
+    of 8 or 16 kv heads), with lengths from below one tile to a few thousand."""
+    rng = np.random.default_rng(1000 + seed)
+    Hkv = int(rng.choice([8, 16]))
+    B = int(rng.integers(512 // Hkv, 256 + 1))
+    G = int(rng.choice([1, 2, 4, 8]))
+    L = int(rng.integers(1, min(16, 48 // G) + 1))  # q_len <= 16, at most three row tiles
+    d = int(rng.choice([64, 128]))
+    lo = L
+    lens = [int(x) for x in rng.integers(lo, int(rng.choice([40, 700, 2500])) + lo + 1, size=B)]
+    page = int(rng.choice([0, 16]))
+    return (f"random{seed}", B, L, G * Hkv, Hkv, d, lens, "bf16", page, True)
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_balanced_verify_random(seed, monkeypatch):
+    test_balanced_verify(_random_case(seed), monkeypatch)
