@@ -22,7 +22,7 @@
  *     and, for md_attn_noalloc only, one static scratch buffer per device.
  *     The MD_* tuning overrides (MD_PREFETCH_DEPTH, MD_OCCUPANCY, MD_LPT,
  *     MD_HEADS_PER_WG, MD_FUSED_MERGE, MD_SLOTS_SCALE, MD_BALANCED,
- *     MD_BAL_WG_PER_CU, MD_BAL_NW; for measurement) are read from the environment on
+ *     MD_BAL_WG_PER_CU, MD_BAL_NW, MD_WAVES; for measurement) are read from the environment on
  *     every call, md_workspace_bytes included; do not change them while
  *     another thread is inside the library, nor between sizing a workspace
  *     and the call that uses it.

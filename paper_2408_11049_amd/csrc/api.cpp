@@ -4,6 +4,7 @@
 #include <math.h>
 #include <stdlib.h>
 
+#include <algorithm>
 #include <atomic>
 #include <string>
 
@@ -98,8 +99,27 @@ unsigned long long next_call_tag() {
   return t;
 }
 
-// Workgroups of an attention launch: a head group per chunk, or, for a
-// longest-first launch that may pair heads, one per unit.
+// Waves per workgroup.  The wide instances (two waves per SIMD in one
+// workgroup, each taking half of the unit's tiles) exist for one row tile of
+// bf16 outside the listed draft and the balanced verify.  Measured on MI355X
+// (same process): one-token drafts whose waves would each take 16 tiles ran
+// 3.5-4.5% faster wide, those at 4-8 tiles per wave 4-5% slower (the merge of
+// eight waves and a larger first burst), long one-token verifies within 1%
+// either way; so drafts take them from 16 tiles per wave.  MD_WAVES = 4 / 8
+// forces either (measurement).
+int waves_per_workgroup(const Plan& pl, int mode, bool bf16) {
+  if (!bf16 || pl.NT != 1 || mode == MD_MODE_DRAFT_INDEXED || pl.bal) return kWaves;
+  const int forced = env_knob("MD_WAVES", kWaves, kWavesWide);
+  if (forced == kWaves || forced == kWavesWide) return forced;
+  if (mode != MD_MODE_DRAFT) return kWaves;
+  const int64_t range = std::min<int64_t>(pl.U_max, pl.chunk_len);
+  const int64_t tiles_per_wave = (range + kTile - 1) / kTile / (kWaves / pl.hp);
+  return tiles_per_wave >= 16 ? kWavesWide : kWaves;
+}
+
+// Workgroups of an attention launch: a head group per chunk; for a
+// longest-first launch that may pair heads, one per unit; for the balanced
+// verify, one per range of its tile stream.
 int64_t grid_size(const Plan& pl, int lpt) {
   if (pl.bal) return pl.bal_nw;
   return (lpt && pl.hp == 2) ? pl.n_units : pl.n_groups * pl.n_chunks;
@@ -174,6 +194,7 @@ int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void*
   p.num_seqs = a->num_seqs;
   p.lpt = !pl.bal && longest_first(mode, pl.n_chunks, a->num_seqs, a->max_kv_len);
   p.bal = pl.bal;
+  p.waves = waves_per_workgroup(pl, mode, bf16);
   p.hp = pl.hp;
   p.err = a->err_word;
   const int64_t n_blocks = grid_size(pl, p.lpt);
@@ -198,7 +219,9 @@ int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void*
     // of each head group to finish: measured on MI355X, same process, that
     // was 1-4 us slower per call (the second launch follows the first with
     // no gap on the stream, and the device-scope fences around the arrival
-    // counters cost more than the launch saves), so it stays opt-in.
+    // counters cost more than the launch saves), so it stays opt-in.  The
+    // balanced verify always merges its cut groups inside the launch: only
+    // the kernel knows which groups its ranges cut.
     p.merge_launch = !env_knob("MD_FUSED_MERGE", 1, 1);
   }
   p.stamps = stamps;

@@ -117,7 +117,7 @@ __device__ __forceinline__ int real_token(const UnitGeom& u, int v) {
 template <typename P>
 __device__ __forceinline__ int lpt_group(const P& p, int r, int* sl, int& hp) {
   const int B = p.num_seqs;
-  for (int t = threadIdx.x; t < B; t += kWaves * 64) {
+  for (int t = threadIdx.x; t < B; t += static_cast<int>(blockDim.x)) {
     const int s = min(p.kv_lens[t], p.max_kv_len);
     sl[t] = s < 0 ? 0 : s;
   }
@@ -147,7 +147,7 @@ __device__ __forceinline__ int lpt_group(const P& p, int r, int* sl, int& hp) {
   const int gps = p.Hkv / hp;
   if (r >= B * gps) return -1;  // uniform over the workgroup: it returns as a whole
   const int want = r / gps;
-  for (int t = threadIdx.x; t < B; t += kWaves * 64) {
+  for (int t = threadIdx.x; t < B; t += static_cast<int>(blockDim.x)) {
     const int lt = sl[t];
     int rank = 0;
     for (int j = 0; j < B; ++j) {
@@ -164,8 +164,8 @@ __device__ __forceinline__ int lpt_group(const P& p, int r, int* sl, int& hp) {
 
 // Balanced verify (p.bal).  The tiles of every head group -- group g =
 // b * gps + j owns tiles_b = max(1, ceil(S_b / kTile)) of them, groups in
-// order -- form one stream of TT tiles, cut into gridDim.x ranges of equal
-// length, one per workgroup: every workgroup streams the same number of
+// order -- form one stream of TT tiles, cut into NW ranges of equal length,
+// one per workgroup (NW below): every workgroup streams the same number of
 // tiles (to within one) whatever the lengths, and keeps the head pairs that
 // read a token row's neighbouring runs together.  A group that a range
 // boundary cuts is computed in pieces by consecutive workgroups, which merge
@@ -227,7 +227,7 @@ __device__ bool bal_start(const P& p, int gps, int* sl, BalCursor& c) {
   if (static_cast<int>(blockIdx.x) >= nw) return false;  // uniform over the workgroup
   const int lo = static_cast<int>(static_cast<int64_t>(blockIdx.x) * tt / nw);
   const int hi = static_cast<int>(static_cast<int64_t>(blockIdx.x + 1) * tt / nw);
-  for (int bb = threadIdx.x; bb < B; bb += kWaves * 64) {
+  for (int bb = threadIdx.x; bb < B; bb += static_cast<int>(blockDim.x)) {
     const int ex = bb ? sl[bb - 1] : 0;
     if (ex <= lo && lo < sl[bb]) sl[kLptMaxSeqs] = bb;
   }
@@ -281,7 +281,7 @@ __device__ void check_contract(const P& p, const U& u, int b, int chunk, bool fi
   if constexpr (PAGED) {
     const bool mine = IDX ? first_wave : first_group;
     const int start = IDX ? lane : static_cast<int>(threadIdx.x);
-    const int step = IDX ? 64 : kWaves * 64;
+    const int step = IDX ? 64 : static_cast<int>(blockDim.x);
     const int pmask = (1 << p.page_shift) - 1;
     if (mine) {
       for (int v = u.v_begin + start; v < u.v_end; v += step) {
@@ -313,9 +313,11 @@ __device__ void check_contract(const P& p, const U& u, int b, int chunk, bool fi
 // prefix (verify) or sinks then windows (draft); P: K/V tiles in flight per
 // wave; OCC: waves per SIMD the instance is compiled for; BAL: the balanced
 // verify (a workgroup takes an equal share of all groups' tiles, piece by
-// piece; its own instances, so the others keep their register budget).
-template <int D, bool BF16, int NT, bool PAGED, bool IDX, int P, int OCC, bool BAL>
-__global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(OCC)))
+// piece; its own instances, so the others keep their register budget); W:
+// waves per workgroup (kWaves, or kWavesWide: two per SIMD in one workgroup,
+// each taking half as many of the unit's tiles).
+template <int D, bool BF16, int NT, bool PAGED, bool IDX, int P, int OCC, bool BAL, int W>
+__global__ void __launch_bounds__(W * 64) __attribute__((amdgpu_waves_per_eu(OCC)))
 attn_partial_kernel(const AttnParams p) {
   using SH = Shape<D, BF16>;
   constexpr int ROWS = NT * 16;
@@ -325,10 +327,10 @@ attn_partial_kernel(const AttnParams p) {
   // start in the same bank (measured: drafts 1-3% faster, outputs identical).
   // Every wave's row tiles are held at once (up to 135 KB at four row tiles).
   constexpr int MROW = D + 4;
-  constexpr int kMergeO = kWaves * NT * 16 * MROW * 4;
-  constexpr int kMergeStats = 2 * kWaves * ROWS * 4;
-  constexpr int kLds = (kWaves * SH::WTILE > kMergeO + kMergeStats) ? kWaves * SH::WTILE
-                                                                     : kMergeO + kMergeStats;
+  constexpr int kMergeO = W * NT * 16 * MROW * 4;
+  constexpr int kMergeStats = 2 * W * ROWS * 4;
+  constexpr int kLds = (W * SH::WTILE > kMergeO + kMergeStats) ? W * SH::WTILE
+                                                               : kMergeO + kMergeStats;
   __shared__ __attribute__((aligned(16))) unsigned char lds[kLds];
 
   const int lane = threadIdx.x & 63;
@@ -351,7 +353,7 @@ attn_partial_kernel(const AttnParams p) {
   const int chunk = static_cast<int>(blockIdx.x) / n_grp;
   // The workgroup's head group: hp adjacent kv heads hk0 .. hk0+hp-1 of
   // sequence b.  Wave w serves kv head hk0 + w % hp and is slot w / hp of
-  // that head's wph = kWaves / hp waves, which interleave its tiles.
+  // that head's wph = W / hp waves, which interleave its tiles.
   // Wave-uniform by construction; readfirstlane lets the compiler keep the
   // unit's address arithmetic in scalar registers.
   int hp_sel = p.hp;
@@ -366,7 +368,7 @@ attn_partial_kernel(const AttnParams p) {
     group_sel = static_cast<int>(blockIdx.x) % n_grp;
   }
   const int hp = __builtin_amdgcn_readfirstlane(hp_sel);
-  const int wph = kWaves / hp;
+  const int wph = W / hp;
   const int gps = p.Hkv / hp;
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   const int wslot = wave_u / hp;
@@ -801,7 +803,7 @@ attn_partial_kernel(const AttnParams p) {
   __syncthreads();  // every wave is done with its LDS tiles
   float* mo = reinterpret_cast<float*>(lds);
   float* sm_m = reinterpret_cast<float*>(lds + kMergeO);
-  float* sm_l = sm_m + kWaves * ROWS;
+  float* sm_l = sm_m + W * ROWS;
   if (grp == 0) {
     for (int rt = 0; rt < NT; ++rt) {
       sm_m[wave * ROWS + rt * 16 + l16] = m_run[rt];
@@ -849,14 +851,14 @@ attn_partial_kernel(const AttnParams p) {
   };
   constexpr int kGroupsPerRow = D / 8;
   const int items_per_unit = p.R * kGroupsPerRow;  // (row, 8 channels)
-  for (int item = tid; item < hp * items_per_unit; item += kWaves * 64) {
+  for (int item = tid; item < hp * items_per_unit; item += W * 64) {
     const int hs = item / items_per_unit;
     const int r = (item % items_per_unit) / kGroupsPerRow;
     const int c0 = (item % kGroupsPerRow) * 8;
     const int rt = r >> 4, rr = r & 15;
     float M = -INFINITY;
     for (int jw = 0; jw < wph; ++jw) M = fmaxf(M, sm_m[(jw * hp + hs) * ROWS + r]);
-    float wgt[kWaves];
+    float wgt[W];
     float Lt = 0.f;
     for (int jw = 0; jw < wph; ++jw) {
       const float mw = sm_m[(jw * hp + hs) * ROWS + r];
@@ -928,7 +930,7 @@ attn_partial_kernel(const AttnParams p) {
       constexpr float kLog2e = 1.44269504088896340736f;
       constexpr float kLn2 = 0.69314718055994530942f;
       const int items_per_unit = p.R * kGroupsPerRow;
-      for (int item = tid; item < hp * items_per_unit; item += kWaves * 64) {
+      for (int item = tid; item < hp * items_per_unit; item += W * 64) {
         const int hs = item / items_per_unit;
         const int r = (item % items_per_unit) / kGroupsPerRow;
         const int c0 = (item % kGroupsPerRow) * 8;
@@ -977,15 +979,15 @@ attn_partial_kernel(const AttnParams p) {
 // ---------------------------------------------------------------------------
 // Host-side dispatch over the compiled instances.
 
-template <int D, bool BF16, int NT, bool IDX, int P, int OCC, bool BAL = false>
+template <int D, bool BF16, int NT, bool IDX, int P, int OCC, bool BAL = false, int W = kWaves>
 static hipError_t launch_p(const AttnParams& p, bool paged, int64_t n_blocks, hipStream_t s) {
-  dim3 grid(static_cast<uint32_t>(n_blocks)), block(kWaves * 64);
+  dim3 grid(static_cast<uint32_t>(n_blocks)), block(W * 64);
   if (paged)
-    hipLaunchKernelGGL((attn_partial_kernel<D, BF16, NT, true, IDX, P, OCC, BAL>), grid, block, 0,
-                       s, p);
+    hipLaunchKernelGGL((attn_partial_kernel<D, BF16, NT, true, IDX, P, OCC, BAL, W>), grid, block,
+                       0, s, p);
   else
-    hipLaunchKernelGGL((attn_partial_kernel<D, BF16, NT, false, IDX, P, OCC, BAL>), grid, block, 0,
-                       s, p);
+    hipLaunchKernelGGL((attn_partial_kernel<D, BF16, NT, false, IDX, P, OCC, BAL, W>), grid, block,
+                       0, s, p);
   return hipGetLastError();
 }
 
@@ -1010,6 +1012,13 @@ static hipError_t launch_nt(const AttnParams& p, bool paged, int depth, int occ,
   } else {
     if (p.bal) return hipErrorInvalidValue;
   }
+  if constexpr (BF16 && NT == 1 && !IDX) {
+    // Eight waves in one workgroup, two per SIMD (the registers of one row
+    // tile allow it): each takes half as many of the unit's tiles.
+    if (p.waves == kWavesWide)
+      return launch_p<D, BF16, NT, IDX, 1, 2, false, kWavesWide>(p, paged, n_blocks, s);
+  }
+  if (p.waves != kWaves) return hipErrorInvalidValue;
   if constexpr (BF16) {
     if constexpr (!IDX && NT <= 3)
       if (depth >= 2) return launch_p<D, BF16, NT, IDX, 2, 1>(p, paged, n_blocks, s);

@@ -23,6 +23,8 @@ namespace md {
 // combines them by log-sum-exp (the split-KV decomposition named in the
 // paper's Sec. 2).
 constexpr int kWaves = 4;
+// Waves of the wide instances (one row tile of bf16): two per SIMD.
+constexpr int kWavesWide = 8;
 constexpr int kTile = 32;            // tokens per wave iteration
 constexpr int kMinChunkTokens = 1024;  // every wave gets >= 8 tiles of a chunk
 constexpr int kMaxRows = 64;         // G*L bound: at most four 16-row tiles

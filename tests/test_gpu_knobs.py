@@ -27,10 +27,10 @@ SETTINGS = [
     {"MD_OCCUPANCY": "2"}, {"MD_LPT": "1"}, {"MD_LPT": "2"}, {"MD_HEADS_PER_WG": "1"},
     {"MD_HEADS_PER_WG": "2"}, {"MD_FUSED_MERGE": "1"}, {"MD_SLOTS_SCALE": "2"},
     {"MD_SLOTS_SCALE": "4"}, {"MD_BALANCED": "1"}, {"MD_BALANCED": "2"},
-    {"MD_BALANCED": "2", "MD_BAL_WG_PER_CU": "2"},
+    {"MD_BALANCED": "2", "MD_BAL_WG_PER_CU": "2"}, {"MD_WAVES": "8"},
 ]
 KNOBS = ["MD_PREFETCH_DEPTH", "MD_OCCUPANCY", "MD_LPT", "MD_HEADS_PER_WG", "MD_FUSED_MERGE",
-         "MD_SLOTS_SCALE", "MD_BALANCED", "MD_BAL_WG_PER_CU"]
+         "MD_SLOTS_SCALE", "MD_BALANCED", "MD_BAL_WG_PER_CU", "MD_WAVES"]
 
 # name, mode, B, L, Hq, Hkv, d, lens, page, n_sink, window, budget
 CASES = [
