@@ -232,7 +232,7 @@ int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void*
   if (e != hipSuccess) return hip_fail(e);
   if (pl.n_chunks > 1 && p.merge_launch) {
     e = launch_merge_lse(pl.n_chunks, pl.n_rows, a->head_dim, bf16, p.part_o, p.part_lse, a->o,
-                         a->lse, s);
+                         a->lse, s, true);
     if (e != hipSuccess) return hip_fail(e);
   }
   return MD_OK;
@@ -303,7 +303,7 @@ int md_merge_lse(int32_t n_parts, int64_t n_rows, int32_t head_dim, int32_t out_
   if (!md::aligned16(o_parts) || !md::aligned16(lse_parts) || !md::aligned16(o) || (lse && !md::aligned16(lse)))
     return MD_ERR_INVALID_ARG;
   hipError_t e = md::launch_merge_lse(n_parts, n_rows, head_dim, out_dtype == MD_BF16, o_parts,
-                                      lse_parts, o, lse, static_cast<hipStream_t>(stream));
+                                      lse_parts, o, lse, static_cast<hipStream_t>(stream), false);
   return e == hipSuccess ? MD_OK : md::hip_fail(e);
 }
 

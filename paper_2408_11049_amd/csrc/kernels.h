@@ -103,9 +103,11 @@ hipError_t launch_snapkv_select(const SnapkvSelectParams& p, hipStream_t s);
 hipError_t launch_attn_partial(const AttnParams& p, int head_dim, bool bf16, int NT, bool paged,
                                int depth, int occ, int64_t n_blocks, hipStream_t s);
 
+// parts_readable: every part's O may be read, empty parts included (the
+// library's own split plans); md_merge_lse never reads an empty part's O.
 hipError_t launch_merge_lse(int n_parts, int64_t n_rows, int head_dim, bool out_bf16,
                             const float* o_parts, const float* lse_parts, void* o, float* lse,
-                            hipStream_t s);
+                            hipStream_t s, bool parts_readable);
 
 // The speculative step around verification.
 struct AppendParams {
