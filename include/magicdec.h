@@ -141,7 +141,11 @@ typedef struct {
  * the kernels' 32-bit indexing: max_kv_len (or a draft window or list
  * capacity) > 2^31 - 65, kv_stride_tok > 2^28 elements,
  * num_seqs * num_kv_heads > 2^31 - 1, num_seqs * q_len * num_q_heads >
- * 4 (2^31 - 1); MD_ERR_WORKSPACE; MD_ERR_HIP.
+ * 4 (2^31 - 1); MD_ERR_WORKSPACE when md_workspace_bytes() is nonzero for
+ * these arguments and the workspace is missing, smaller or not 256-byte
+ * aligned (which calls need one -- split ranges, the balanced verify --
+ * depends on the sizes and the device, so size it for every new shape);
+ * MD_ERR_HIP.
  */
 int md_verify_attn(const md_attn_args* a, void* stream);
 
