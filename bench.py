@@ -184,10 +184,9 @@ def settle_count(rec):
     return 0
 
 
-def timed_calls(dispatches, warmup, steps, settle=0):
-    """The timed verify and draft calls: lists of dispatch groups (an
-    attention dispatch plus a merge dispatch that follows it, if any), after
-    `settle` untimed verify calls and `warmup` warm-up steps."""
+def attention_calls(dispatches):
+    """The run's attention calls in launch order: each an attention dispatch
+    plus the merge dispatch that follows it, if any (split plans)."""
     calls, cur = [], None
     for d in dispatches:
         if "attn_partial_kernel" in d["name"]:
@@ -198,6 +197,14 @@ def timed_calls(dispatches, warmup, steps, settle=0):
             cur = None
         else:
             cur = None
+    return calls
+
+
+def timed_calls(dispatches, warmup, steps, settle=0):
+    """The timed verify and draft calls: lists of dispatch groups (an
+    attention dispatch plus a merge dispatch that follows it, if any), after
+    `settle` untimed verify calls and `warmup` warm-up steps."""
+    calls = attention_calls(dispatches)
     need = settle + 2 * (warmup + steps)
     if len(calls) < need:
         raise SystemExit(f"only {len(calls)} attention calls; expected at least {need}")
@@ -688,16 +695,7 @@ def summarize_latency(csv_path, bench_json, cmd):
             rec = json.loads(line)
     if rec is None:
         raise SystemExit(f"no latency line in {bench_json}")
-    calls, cur = [], None
-    for d in _dispatches(_rows(csv_path)):
-        if "attn_partial_kernel" in d["name"]:
-            cur = [d]
-            calls.append(cur)
-        elif "merge_lse_kernel" in d["name"] and cur is not None:
-            cur.append(d)
-            cur = None
-        else:
-            cur = None
+    calls = attention_calls(_dispatches(_rows(csv_path)))
     out = ["# Where a draft call's time goes (rocprofv3 kernel trace + workgroup stamps)",
            "",
            "Draft calls (sinks + window, at q_len = gamma + 1 and 1) of the llama8b_b32_s8k",
@@ -838,6 +836,77 @@ def summarize_paged(csv_path, bench_json, cmd):
     return "\n".join(out) + "\n"
 
 
+CONFIG_KINDS = ["verify", "verify_qlen1", "draft", "draft_qlen1"]
+
+
+def config_calls(calls, rec):
+    """The timed calls of the per-configuration table, picked by ordinal: the
+    table is the run's last attention work, and per configuration (in CONFIGS
+    order) it makes one warm call of each kind, its settling verify calls,
+    then 10 timed calls of each kind in CONFIG_KINDS order.  Returns
+    {config: {kind: [call, ...]}}."""
+    cfgs = rec["detail"]["configs"]
+    names = [n for n in CONFIGS if n in cfgs]
+    out, idx = {}, len(calls)
+    for name in reversed(names):
+        settle = next((int(v) for k, v in cfgs[name].items() if k.startswith("settle_calls")), 0)
+        timed = calls[idx - 40: idx]
+        idx -= 40 + settle + len(CONFIG_KINDS)
+        if idx < 0 or len(timed) != 40:
+            raise SystemExit(f"{name}: the trace holds too few attention calls for the table")
+        out[name] = {k: timed[10 * i: 10 * i + 10] for i, k in enumerate(CONFIG_KINDS)}
+        for k, cl in out[name].items():
+            kn = {_short(c[0]["name"]) for c in cl}
+            if len(kn) != 1:
+                raise SystemExit(f"{name} {k}: the picked calls run different kernels: {sorted(kn)}")
+    return out
+
+
+def summarize_configs(csv_path, bench_json, cmd):
+    """Kernel-trace times of the per-configuration table's timed calls next to
+    the event-timed medians of the same bench line."""
+    import numpy as np
+
+    rec = _bench_line(bench_json)
+    cfgs = rec["detail"]["configs"]
+    per = config_calls(attention_calls(_dispatches(_rows(csv_path))), rec)
+    out = ["# Kernel timing of the per-configuration table (rocprofv3 kernel trace)",
+           "",
+           "Every configuration of the workload list, verify and draft at q_len = gamma + 1",
+           "and 1, each call after a 1 GiB cache eviction, 10 timed calls per kind after the",
+           "configuration's settling calls.  One MI355X (gfx950).",
+           "",
+           "Command (from /tmp with TMPDIR=/tmp; R = the repository root); its stdout is the",
+           "bench line whose detail.configs gives the event medians:",
+           "",
+           f"    {cmd}",
+           "",
+           "Selection: the table is the run's last attention work; per configuration it makes",
+           "one warm call of each kind, its settling verify calls (their count is in the bench",
+           "line), then 10 timed calls of verify, one-token verify, draft and one-token draft,",
+           "so the summary walks back from the last attention dispatch.  A merge dispatch that",
+           "follows a call (split plans) counts with it.  Under the tracer the event medians",
+           "run a little slower than unprofiled.",
+           "",
+           "| configuration | call | kernel | kernel median us | event median us | kernel / event | K/V bytes | frac of 8 TB/s (kernel) | frac (event) |",
+           "|---|---|---|---|---|---|---|---|---|"]
+    for name in CONFIGS:
+        if name not in per:
+            continue
+        row = cfgs[name]
+        for k in CONFIG_KINDS:
+            durs = [sum(d["end"] - d["start"] for d in c) / 1e3 for c in per[name][k]]
+            km = float(np.median(durs))
+            ev = float(row[f"t_{k}_us_p10_p50_p90"][1])
+            by = float(row[f"{k}_kv_bytes"])
+            kn = " + merge" if any(len(c) > 1 for c in per[name][k]) else ""
+            out.append(f"| {name} | {k} | `{_short(per[name][k][0][0]['name'])}`{kn} | {km:.2f} | {ev:.2f} | "
+                       f"{km / ev:.3f} | {by:.4g} | {by / (km * 1e-6) / 1e9 / HBM_PEAK_GBS:.4f} | "
+                       f"{by / (ev * 1e-6) / 1e9 / HBM_PEAK_GBS:.4f} |")
+    out += ["", f"kernel_source_sha256: {kernel_source_sha256()}"]
+    return "\n".join(out) + "\n"
+
+
 LDS_COUNTERS = ["SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE", "SQ_LDS_ADDR_CONFLICT",
                 "SQ_LDS_UNALIGNED_STALL", "SQ_INSTS_LDS", "SQ_WAIT_INST_LDS", "SQ_ACTIVE_INST_LDS"]
 
@@ -894,7 +963,8 @@ def main():
                     help="only the draft-call latency breakdown (profiles/)")
     ap.add_argument("--paged-ab", action="store_true",
                     help="only the paged / sequential-page / contiguous verify A/B (profiles/)")
-    ap.add_argument("--summarize", choices=["trace", "counters", "mfma", "latency", "paged", "lds"])
+    ap.add_argument("--summarize", choices=["trace", "counters", "mfma", "latency", "paged", "lds",
+                                            "configs"])
     ap.add_argument("--csv", nargs="+")
     ap.add_argument("--bench-json")
     ap.add_argument("--cmd", default="")
@@ -906,7 +976,8 @@ def main():
               "mfma": lambda: summarize_mfma(args.csv[0], args.bench_json, args.cmd),
               "latency": lambda: summarize_latency(args.csv[0], args.bench_json, args.cmd),
               "paged": lambda: summarize_paged(args.csv[0], args.bench_json, args.cmd),
-              "lds": lambda: summarize_lds(args.csv[0], args.bench_json, args.cmd)}
+              "lds": lambda: summarize_lds(args.csv[0], args.bench_json, args.cmd),
+              "configs": lambda: summarize_configs(args.csv[0], args.bench_json, args.cmd)}
         sys.stdout.write(fn[args.summarize]())
         return
     if args.gpus != 1:

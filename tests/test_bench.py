@@ -127,3 +127,41 @@ def test_lds_summary_groups_by_kernel(tmp_path):
     assert "| 5 |" in v and "| 0.100 |" in v  # 2 settling + 3 step calls, 10 / 100
     assert "| 3 |" in d and "| 0.200 |" in d
     assert "bench_evict" not in text and "copy_kernel" not in text
+
+
+def test_config_summary_walks_back_from_the_table(tmp_path):
+    """--summarize configs: the table is the run's last attention work; per
+    configuration one warm call of each kind, its settling verify calls, then
+    10 timed calls per kind -- picked by walking back from the end, whatever
+    ran before (here a bench-shape step and a stray earlier call)."""
+    import json
+    names = bench.CONFIGS
+    seq = [("void md::attn_partial_kernel<128, true, 2, true, false, 1, 1, true, 4>(x)", 999)] * 7
+    cfgs = {}
+    for ci, name in enumerate(names):
+        kern = {k: f"void md::attn_partial_kernel<{ci}, {ki}>(x)" for ki, k in enumerate(bench.CONFIG_KINDS)}
+        settle = 3 + ci
+        seq += [(kern[k], 500) for k in bench.CONFIG_KINDS]       # warm
+        seq += [(kern["verify"], 700)] * settle                     # settling
+        for ki, k in enumerate(bench.CONFIG_KINDS):
+            seq += [(kern[k], 100 * (ci + 1) + ki)] * 10
+            if k == "draft" and ci == 1:                           # a split plan: merge after each call
+                seq = seq[:-10] + sum([[(kern[k], 100 * (ci + 1) + ki),
+                                        ("void md::merge_lse_kernel<128, true, true>(x)", 4)]] * 10, [])
+        cfgs[name] = {"settle_calls (untimed verify calls first, >= 60 ms)": settle}
+        for ki, k in enumerate(bench.CONFIG_KINDS):
+            cfgs[name][f"t_{k}_us_p10_p50_p90"] = [1, 100 * (ci + 1) + ki + 5, 1]
+            cfgs[name][f"{k}_kv_bytes"] = 1e9
+    path = tmp_path / "t.csv"
+    _trace_csv(path, seq)
+    bj = tmp_path / "b.json"
+    bj.write_text(json.dumps({"metric": "m", "value": 1, "unit": "GB/s", "steps": 1, "warmup": 1,
+                              "detail": {"configs": cfgs}}) + "\n")
+    text = bench.summarize_configs(str(path), str(bj), "cmd")
+    rows = [l.split(" | ") for l in text.splitlines() if l.startswith("| ") and "attn_partial" in l]
+    assert len(rows) == 4 * len(names)
+    for r in rows:
+        ci, ki = names.index(r[0][2:]), bench.CONFIG_KINDS.index(r[1])
+        want = 100 * (ci + 1) + ki + (4 if (ci == 1 and ki == 2) else 0)
+        assert float(r[3]) == pytest.approx(want), r
+        assert ("+ merge" in r[2]) == (ci == 1 and ki == 2)
