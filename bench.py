@@ -38,7 +38,7 @@ beside the step kernels.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
                        [--no-configs]
-       python bench.py --summarize trace|counters|mfma --csv F [F2] --bench-json J
+       python bench.py --summarize trace|counters|mfma|... --csv F [F2] --bench-json J [J2]
                        --cmd "..."   (writes a profiles/ summary to stdout)
 """
 import argparse
@@ -907,6 +907,55 @@ def summarize_configs(csv_path, bench_json, cmd):
     return "\n".join(out) + "\n"
 
 
+def summarize_config_counters(fetch_csv, write_csv, fetch_json, write_json, cmd):
+    """HBM traffic of the per-configuration table's timed calls: FETCH_SIZE and
+    WRITE_SIZE per call (attention plus merge), scaled by a copy of known
+    size in the same run, against the algorithmic K/V bytes."""
+    res, calib, kernels = {}, {}, {}
+    for ctr, path, bj in (("FETCH_SIZE", fetch_csv, fetch_json), ("WRITE_SIZE", write_csv, write_json)):
+        rec = _bench_line(bj)
+        ds = _dispatches(_rows(path))
+        copies = [d for d in ds if "bench_copy_kernel" in d["name"]]
+        if not copies:
+            raise SystemExit(f"{path}: no md_bench_copy dispatch to calibrate {ctr}")
+        calib[ctr] = copies[-1][ctr]
+        for name, kinds in config_calls(attention_calls(ds), rec).items():
+            for k, cl in kinds.items():
+                res[(name, k, ctr)] = sum(sum(d[ctr] for d in c) for c in cl) / len(cl)
+                kernels[(name, k)] = _short(cl[0][0]["name"]) + (" + merge" if any(len(c) > 1 for c in cl) else "")
+        cfgs = rec["detail"]["configs"]
+    gib = float(1 << 30)
+    scale = {c: gib / (calib[c] * 1024.0) for c in calib}
+    out = ["# HBM traffic of the per-configuration table (rocprofv3 counters)",
+           "",
+           "Every configuration of the workload list, verify and draft at q_len = gamma + 1",
+           "and 1, each call after a 1 GiB cache eviction.  One MI355X (gfx950).  The timed",
+           "calls are picked as in the per-configuration kernel trace (by ordinal, walking back",
+           "from the last attention dispatch, with each run's own settling counts).",
+           "",
+           "Commands (from /tmp with TMPDIR=/tmp; R = the repository root):",
+           "",
+           f"    {cmd}",
+           "",
+           f"Calibration: a 1 GiB copy in each run read FETCH_SIZE = {calib['FETCH_SIZE']:.0f} KiB and",
+           f"WRITE_SIZE = {calib['WRITE_SIZE']:.0f} KiB, so bytes = KiB x 1024 x scale with",
+           f"scale_fetch = {scale['FETCH_SIZE']:.5f}, scale_write = {scale['WRITE_SIZE']:.5f}.",
+           "",
+           "| configuration | call | kernel | HBM bytes read | HBM bytes written | algorithmic K/V bytes | read / algorithmic |",
+           "|---|---|---|---|---|---|---|"]
+    for name in CONFIGS:
+        if (name, "verify") not in kernels:
+            continue
+        for k in CONFIG_KINDS:
+            rd = res[(name, k, "FETCH_SIZE")] * 1024 * scale["FETCH_SIZE"]
+            wr = res[(name, k, "WRITE_SIZE")] * 1024 * scale["WRITE_SIZE"]
+            alg = float(cfgs[name][f"{k}_kv_bytes"])
+            out.append(f"| {name} | {k} | `{kernels[(name, k)]}` | {rd:.4g} | {wr:.4g} | {alg:.4g} | "
+                       f"{rd / alg:.4f} |")
+    out += ["", f"kernel_source_sha256: {kernel_source_sha256()}"]
+    return "\n".join(out) + "\n"
+
+
 LDS_COUNTERS = ["SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE", "SQ_LDS_ADDR_CONFLICT",
                 "SQ_LDS_UNALIGNED_STALL", "SQ_INSTS_LDS", "SQ_WAIT_INST_LDS", "SQ_ACTIVE_INST_LDS"]
 
@@ -964,20 +1013,22 @@ def main():
     ap.add_argument("--paged-ab", action="store_true",
                     help="only the paged / sequential-page / contiguous verify A/B (profiles/)")
     ap.add_argument("--summarize", choices=["trace", "counters", "mfma", "latency", "paged", "lds",
-                                            "configs"])
+                                            "configs", "config-counters"])
     ap.add_argument("--csv", nargs="+")
-    ap.add_argument("--bench-json")
+    ap.add_argument("--bench-json", nargs="+")
     ap.add_argument("--cmd", default="")
     args = ap.parse_args()
     if args.summarize:
-        fn = {"trace": lambda: summarize_trace(args.csv[0], args.bench_json, args.cmd),
-              "counters": lambda: summarize_counters(args.csv[0], args.csv[1], args.bench_json,
+        fn = {"trace": lambda: summarize_trace(args.csv[0], args.bench_json[0], args.cmd),
+              "counters": lambda: summarize_counters(args.csv[0], args.csv[1], args.bench_json[0],
                                                      args.cmd),
-              "mfma": lambda: summarize_mfma(args.csv[0], args.bench_json, args.cmd),
-              "latency": lambda: summarize_latency(args.csv[0], args.bench_json, args.cmd),
-              "paged": lambda: summarize_paged(args.csv[0], args.bench_json, args.cmd),
-              "lds": lambda: summarize_lds(args.csv[0], args.bench_json, args.cmd),
-              "configs": lambda: summarize_configs(args.csv[0], args.bench_json, args.cmd)}
+              "mfma": lambda: summarize_mfma(args.csv[0], args.bench_json[0], args.cmd),
+              "latency": lambda: summarize_latency(args.csv[0], args.bench_json[0], args.cmd),
+              "paged": lambda: summarize_paged(args.csv[0], args.bench_json[0], args.cmd),
+              "lds": lambda: summarize_lds(args.csv[0], args.bench_json[0], args.cmd),
+              "configs": lambda: summarize_configs(args.csv[0], args.bench_json[0], args.cmd),
+              "config-counters": lambda: summarize_config_counters(
+                  args.csv[0], args.csv[1], args.bench_json[0], args.bench_json[-1], args.cmd)}
         sys.stdout.write(fn[args.summarize]())
         return
     if args.gpus != 1:

@@ -165,3 +165,56 @@ def test_config_summary_walks_back_from_the_table(tmp_path):
         want = 100 * (ci + 1) + ki + (4 if (ci == 1 and ki == 2) else 0)
         assert float(r[3]) == pytest.approx(want), r
         assert ("+ merge" in r[2]) == (ci == 1 and ki == 2)
+
+
+def test_config_counter_summary(tmp_path):
+    """--summarize config-counters: FETCH_SIZE and WRITE_SIZE of the table's
+    timed calls (attention plus merge), each run picked with its own settling
+    counts and scaled by the run's 1 GiB copy."""
+    import csv
+    import json
+    names = bench.CONFIGS
+
+    def run(ctr, settle_extra):
+        rows, cfgs, did = [], {}, 0
+
+        def add(name, val):
+            nonlocal did
+            did += 1
+            rows.append([did, name, ctr, val])
+        add("md::bench_copy_kernel", (1 << 20) / (2 if ctr == "FETCH_SIZE" else 1))
+        for ci, name in enumerate(names):
+            kern = {k: f"void md::attn_partial_kernel<{ci}, {ki}>(x)" for ki, k in enumerate(bench.CONFIG_KINDS)}
+            settle = 2 + ci + settle_extra
+            for k in bench.CONFIG_KINDS:
+                add(kern[k], 1.0)
+            for _ in range(settle):
+                add(kern["verify"], 1.0)
+            for k in bench.CONFIG_KINDS:
+                for _ in range(10):
+                    add(kern[k], 1000.0 * (ci + 1))
+                    if ci == 4:
+                        add("void md::merge_lse_kernel<128, true, true>(x)", 10.0)
+            cfgs[name] = {"settle_calls (untimed verify calls first, >= 60 ms)": settle}
+            for k in bench.CONFIG_KINDS:
+                cfgs[name][f"{k}_kv_bytes"] = 1024.0 * 1000.0 * (ci + 1)
+        path = tmp_path / f"{ctr}.csv"
+        with open(path, "w", newline="") as f:
+            wr = csv.writer(f)
+            wr.writerow(["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
+            wr.writerows(rows)
+        bj = tmp_path / f"{ctr}.json"
+        bj.write_text(json.dumps({"metric": "m", "value": 1, "unit": "GB/s", "steps": 1, "warmup": 1,
+                                  "detail": {"configs": cfgs}}) + "\n")
+        return str(path), str(bj)
+
+    fc, fj = run("FETCH_SIZE", 0)
+    wc, wj = run("WRITE_SIZE", 3)  # another run settles longer
+    text = bench.summarize_config_counters(fc, wc, fj, wj, "cmd")
+    rows = [l.split(" | ") for l in text.splitlines() if l.startswith("| ") and "attn_partial" in l]
+    assert len(rows) == 4 * len(names)
+    for r in rows:
+        ci = names.index(r[0][2:])
+        extra = 10.0 if ci == 4 else 0.0
+        assert float(r[3]) == pytest.approx((1000.0 * (ci + 1) + extra) * 1024 * 2, rel=1e-3)
+        assert float(r[4]) == pytest.approx((1000.0 * (ci + 1) + extra) * 1024, rel=1e-3)
