@@ -10,8 +10,9 @@
 //
 // One workgroup = one chunk of hp units (hp adjacent kv heads of a sequence,
 // so that the waves of a workgroup read neighbouring runs of each token row);
-// the kWaves / hp waves of a unit take interleaved 32-token tiles of the
-// chunk and run independent online softmaxes, merged through LDS at the end.
+// the W / hp waves of a unit (W = 4, or 8 in the wide one-row-tile
+// instances) take interleaved 32-token tiles of the chunk and run
+// independent online softmaxes, merged through LDS at the end.
 // Per tile and wave:
 //   load     K and V as whole token rows (256 B for bf16, d = 128: 16 lanes
 //            per row, nontemporal 16 B loads, one address per token), staged

@@ -17,8 +17,9 @@ namespace md {
 // once.  The unit's visible key range (the whole causal prefix for verify;
 // sinks followed by the window for draft, read as one virtual range) is cut
 // into n_chunks chunks of chunk_len tokens.  A workgroup of kWaves waves
-// takes one chunk of hp units of the same sequence (hp adjacent kv heads):
-// kWaves / hp waves per unit, which interleave kTile-token tiles.  With
+// (kWavesWide in the wide instances) takes one chunk of hp units of the same
+// sequence (hp adjacent kv heads): waves / hp per unit, which interleave
+// kTile-token tiles.  With
 // n_chunks > 1 the chunks write normalised partial results and a merge pass
 // combines them by log-sum-exp (the split-KV decomposition named in the
 // paper's Sec. 2).
