@@ -100,15 +100,16 @@ unsigned long long next_call_tag() {
 }
 
 // Waves per workgroup.  The wide instances (two waves per SIMD in one
-// workgroup, each taking half of the unit's tiles) exist for one row tile of
-// bf16 outside the listed draft and the balanced verify.  Measured on MI355X
-// (same process): one-token drafts whose waves would each take 16 tiles ran
-// 3.5-4.5% faster wide, those at 4-8 tiles per wave 4-5% slower (the merge of
-// eight waves and a larger first burst), long one-token verifies within 1%
-// either way; so drafts take them from 16 tiles per wave.  MD_WAVES = 4 / 8
-// forces either (measurement).
+// workgroup, each taking half of the unit's tiles) exist for up to two row
+// tiles of bf16 outside the listed draft and the balanced verify.  Measured
+// on MI355X (same process): drafts whose waves would each take 16 tiles ran
+// 3-6% faster wide (one-token drafts at one row tile, (gamma+1)-token drafts
+// at two), those at 4-8 tiles per wave 4-5% slower (the merge of eight waves
+// and a larger first burst), long verifies within 1% either way at one row
+// tile and slower at two; so drafts take them from 16 tiles per wave.
+// MD_WAVES = 4 / 8 forces either (measurement).
 int waves_per_workgroup(const Plan& pl, int mode, bool bf16) {
-  if (!bf16 || pl.NT != 1 || mode == MD_MODE_DRAFT_INDEXED || pl.bal) return kWaves;
+  if (!bf16 || pl.NT > 2 || mode == MD_MODE_DRAFT_INDEXED || pl.bal) return kWaves;
   const int forced = env_knob("MD_WAVES", kWaves, kWavesWide);
   if (forced == kWaves || forced == kWavesWide) return forced;
   if (mode != MD_MODE_DRAFT) return kWaves;

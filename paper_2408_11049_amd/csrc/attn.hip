@@ -10,8 +10,8 @@
 //
 // One workgroup = one chunk of hp units (hp adjacent kv heads of a sequence,
 // so that the waves of a workgroup read neighbouring runs of each token row);
-// the W / hp waves of a unit (W = 4, or 8 in the wide one-row-tile
-// instances) take interleaved 32-token tiles of the chunk and run
+// the W / hp waves of a unit (W = 4, or 8 in the wide instances of up to
+// two row tiles) take interleaved 32-token tiles of the chunk and run
 // independent online softmaxes, merged through LDS at the end.
 // Per tile and wave:
 //   load     K and V as whole token rows (256 B for bf16, d = 128: 16 lanes
@@ -1013,9 +1013,10 @@ static hipError_t launch_nt(const AttnParams& p, bool paged, int depth, int occ,
   } else {
     if (p.bal) return hipErrorInvalidValue;
   }
-  if constexpr (BF16 && NT == 1 && !IDX) {
-    // Eight waves in one workgroup, two per SIMD (the registers of one row
-    // tile allow it): each takes half as many of the unit's tiles.
+  if constexpr (BF16 && NT <= 2 && !IDX) {
+    // Eight waves in one workgroup, two per SIMD (the registers of up to two
+    // row tiles allow it, 248 at two): each takes half as many of the unit's
+    // tiles.  Their merge buffers fill 140 KB of LDS at two row tiles.
     if (p.waves == kWavesWide)
       return launch_p<D, BF16, NT, IDX, 1, 2, false, kWavesWide>(p, paged, n_blocks, s);
   }

@@ -24,7 +24,7 @@ namespace md {
 // combines them by log-sum-exp (the split-KV decomposition named in the
 // paper's Sec. 2).
 constexpr int kWaves = 4;
-// Waves of the wide instances (one row tile of bf16): two per SIMD.
+// Waves of the wide instances (up to two row tiles of bf16): two per SIMD.
 constexpr int kWavesWide = 8;
 constexpr int kTile = 32;            // tokens per wave iteration
 constexpr int kMinChunkTokens = 1024;  // every wave gets >= 8 tiles of a chunk

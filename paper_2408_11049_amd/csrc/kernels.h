@@ -49,8 +49,8 @@ struct AttnParams {
                               // sharing all groups' tiles equally; workgroup w keeps the partials
                               // of its range's first / last piece in slots 2w / 2w + 1
   int32_t hp;                 // kv heads per workgroup (1 or 2; divides Hkv)
-  int32_t waves;              // waves per workgroup: kWaves, or kWavesWide (one row tile of
-                              // bf16, not listed, not balanced)
+  int32_t waves;              // waves per workgroup: kWaves, or kWavesWide (up to two row
+                              // tiles of bf16, not listed, not balanced)
   int32_t hp_auto;            // longest-first launch of one workgroup per unit that
                               // pairs heads when the lengths allow (see attn.hip)
   int32_t slots;              // compute units of the device (hp_auto's balance test)
