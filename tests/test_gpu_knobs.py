@@ -7,8 +7,8 @@ MD_HEADS_PER_WG (one head or a head pair per workgroup), MD_FUSED_MERGE
 launch) and MD_SLOTS_SCALE (plans for two or four workgroups per compute
 unit: more and shorter chunks).  The overrides are
 read on every call, so one process sweeps them all; each setting runs the
-same shapes: one to four 16-row tiles, the streaming and listed
-drafts, a split range with its merge and a longest-first batch."""
+same shapes: one to four 16-row tiles, both head dims, the streaming and
+listed drafts, a split range with its merge and a longest-first batch."""
 import functools
 
 import numpy as np
@@ -39,6 +39,7 @@ CASES = [
     ("listed_rows20", oracle.INDEXED, 3, 5, 8, 2, 128, [300, 77, 1030], 16, 0, 1, 200),
     ("verify_rows16", oracle.VERIFY, 2, 4, 8, 2, 128, [513, 64], 0, 0, 1, 0),
     ("draft_rows40", oracle.DRAFT, 2, 5, 16, 2, 128, [700, 450], 0, 16, 200, 0),
+    ("draft_rows20_d64", oracle.DRAFT, 3, 5, 16, 4, 64, [1500, 333, 2100], 16, 8, 900, 0),
     ("verify_rows40", oracle.VERIFY, 2, 5, 16, 2, 128, [700, 450], 16, 0, 1, 0),
     ("verify_rows64", oracle.VERIFY, 1, 16, 4, 1, 64, [300], 0, 0, 1, 0),
     ("verify_split", oracle.VERIFY, 1, 4, 8, 2, 128, [5000], 16, 0, 1, 0),
