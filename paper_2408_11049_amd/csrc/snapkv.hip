@@ -292,27 +292,30 @@ __device__ __forceinline__ float sk_pooled(const float* v, int n, int j, int poo
 
 constexpr int kSelThreads = 512;
 constexpr int kSelWaves = kSelThreads / 64;
-constexpr int kSelPer = 4;             // consecutive positions per thread in a step
+constexpr int kSelPer = 4;             // global instance: consecutive positions per thread in a step
 constexpr int kSelStep = kSelThreads * kSelPer;
-constexpr int kSelLdsKeys = 33792;     // pooled keys of one row held in LDS (132 KB)
-constexpr int kSelHalo = 16;           // LDS instance: pool / 2 <= kSelHalo
-constexpr int kSelStage = kSelStep + 2 * kSelHalo;
-constexpr int kSelStagePer = (kSelStage + kSelThreads - 1) / kSelThreads;
+constexpr int kSelKpt = 66;            // register instance: pooled keys per thread
+constexpr int kSelRegKeys = kSelThreads * kSelKpt;  // its longest row: 33792 prefix positions
+constexpr int kSelRegHalo = 3;         // and its widest pooling: pool <= 7
 
 // Count every active lane's bin in the wave's histogram h.  Pooled votes of
-// similar size share their top key bytes, so the early radix passes pile
-// onto a few bins: the wave's two most common bins go in with one atomic
-// each (led by their lowest lane), the remaining lanes add directly.
+// similar size share their top key bits, so the early radix passes pile
+// onto a few bins: the bin of the lowest uncounted lane goes in with one
+// atomic for all lanes that share it, twice (with skewed keys, most likely
+// the wave's most common bins), and the remaining lanes add directly.
 __device__ __forceinline__ void sk_hist_add(uint32_t* h, bool active, uint32_t bin, int lane) {
-  uint64_t pending = __ballot(active);
-  for (int round = 0; round < 2 && pending; ++round) {
+  bool mine = active;  // this lane's key is not counted yet
+  for (int round = 0; round < 2; ++round) {
+    const uint64_t pending = __ballot(mine);
+    if (pending == 0) return;  // wave-uniform
     const int leader = __ffsll(static_cast<long long>(pending)) - 1;
     const uint32_t lb = __builtin_amdgcn_readlane(bin, leader);  // leader is wave-uniform
-    const uint64_t same = __ballot(((pending >> lane) & 1ull) && bin == lb);
-    if (lane == leader) atomicAdd(&h[lb], static_cast<uint32_t>(__popcll(same)));
-    pending &= ~same;
+    const bool same = mine && bin == lb;
+    const uint64_t n_same = __ballot(same);
+    if (lane == leader) atomicAdd(&h[lb], static_cast<uint32_t>(__popcll(n_same)));
+    mine = mine && !same;
   }
-  if ((pending >> lane) & 1ull) atomicAdd(&h[bin], 1u);
+  if (mine) atomicAdd(&h[bin], 1u);
 }
 
 // Exclusive prefix sum of x over the workgroup (thread order), and the total.
@@ -336,22 +339,181 @@ __device__ __forceinline__ uint32_t sk_block_scan(uint32_t x, uint32_t* wsum, ui
   return before + incl - x;
 }
 
-// One workgroup per (sequence, kv head) row.
-//
-// LDS instance (rows of at most kSelLdsKeys prefix positions, pool / 2 <=
-// kSelHalo): the raw votes are copied into keys[] with 16-byte loads, then
-// replaced in place, kSelStep positions per step, by their pooled keys.  A
-// step first copies its raw window plus halos into stage[] -- its left halo
-// from the previous step's stage, which kept the raw values that step
-// overwrote -- and pools from there, so no in-place write feeds a later read.
-// Every sweep then reads one LDS word per position.  Otherwise each sweep
-// pools from global memory.  The pooled sum is formed in sk_pooled's order
-// either way (terms outside the prefix add an exact 0), so both instances
-// see the same keys.
-template <bool LDS>
+// The keep-th largest key of a row and how many keys exceed it, by radix
+// select over 11-, 11- and 10-bit digits, most significant first:
+// `key_at(e)` is this thread's e-th key (0 <= e < PER), valid(e) whether it
+// is a position of the row.  hist is kSelWaves per-wave histograms of
+// kSelBins counters (LDS).  Every thread returns the same (tau, above).
+constexpr int kSelBins = 2048;
+template <int PER, typename KeyAt, typename Valid>
+__device__ __forceinline__ void sk_radix_select(KeyAt key_at, Valid valid, int keep,
+                                                uint32_t* hist, uint32_t* wsum,
+                                                uint32_t* s_prefix, uint32_t* s_above,
+                                                uint32_t& tau, uint32_t& above_out) {
+  constexpr int kDigitsPerThread = kSelBins / kSelThreads;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  uint32_t prefix = 0, above = 0;
+  for (int pass = 0; pass < 3; ++pass) {
+    const int shift = pass == 0 ? 21 : (pass == 1 ? 10 : 0);
+    const uint32_t dmask = pass == 2 ? 0x3ffu : 0x7ffu;
+    const uint32_t hi_mask = pass == 0 ? 0u : (pass == 1 ? 0xffe00000u : 0xfffffc00u);
+    for (int i = tid; i < kSelWaves * kSelBins; i += kSelThreads) hist[i] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+      const uint32_t k = key_at(e);
+      const bool act = valid(e) && (k & hi_mask) == (prefix & hi_mask);
+      sk_hist_add(hist + w * kSelBins, act, (k >> shift) & dmask, lane);
+    }
+    __syncthreads();
+    // Thread t owns digits kSelBins-1-4t .. kSelBins-4-4t (descending); a scan
+    // over the threads finds the digit where the running count reaches keep.
+    uint32_t c[kDigitsPerThread];
+    uint32_t cnt = 0;
+#pragma unroll
+    for (int i = 0; i < kDigitsPerThread; ++i) {
+      const int d = kSelBins - 1 - (kDigitsPerThread * tid + i);
+      c[i] = 0;
+      for (int x = 0; x < kSelWaves; ++x) c[i] += hist[x * kSelBins + d];
+      cnt += c[i];
+    }
+    uint32_t total;
+    uint32_t run = above + sk_block_scan(cnt, wsum, total, lane, w);
+#pragma unroll
+    for (int i = 0; i < kDigitsPerThread; ++i) {
+      const uint32_t d = static_cast<uint32_t>(kSelBins - 1 - (kDigitsPerThread * tid + i));
+      if (run < static_cast<uint32_t>(keep) && run + c[i] >= static_cast<uint32_t>(keep)) {
+        *s_prefix = prefix | (d << shift);
+        *s_above = run;
+      }
+      run += c[i];
+    }
+    __syncthreads();
+    prefix = *s_prefix;
+    above = *s_above;
+    __syncthreads();
+  }
+  tau = prefix;
+  above_out = above;
+}
+
+// Register instance, rows of at most kSelRegKeys prefix positions.  Thread
+// t owns the contiguous segment [66t, 66t + 66) of the row.  The raw votes
+// are copied into LDS with 16-byte global loads, position j at word
+// j + j / 66 (one pad word per segment, so the 64 lanes reading the same
+// offset of their segments hit distinct banks); each thread pools its
+// segment from its own window of LDS in sk_pooled's order and keeps the 66
+// keys in registers for the radix passes and the compaction.  The positions
+// a thread keeps are contiguous in its segment, so two block scans give
+// every thread its output offset and the row comes out ascending.
+__device__ __forceinline__ int sk_pad(int j) { return j + j / kSelKpt; }
+
+template <int POOL>
+__global__ void __launch_bounds__(kSelThreads) snapkv_select_reg_kernel(const SnapkvSelectParams p) {
+  // The raw votes, then (the keys in registers) the radix histograms.
+  constexpr int kBuf = kSelRegKeys + kSelThreads;
+  __shared__ float buf[kBuf];
+  static_assert(kSelWaves * kSelBins <= kBuf, "histograms fit the buffer");
+  __shared__ uint32_t wsum[kSelWaves];
+  __shared__ uint32_t s_prefix, s_above;
+
+  const int row = blockIdx.x;
+  const int b = row / p.rows_per_seq;
+  const int S = min(max(p.lens[b], 0), p.stride + p.n_obs);
+  const int n = max(S - p.n_obs, 0);  // <= stride <= kSelRegKeys
+  const int keep = min(p.budget - p.n_obs, n);
+  const float* v = p.votes + static_cast<int64_t>(row) * p.stride;
+  int32_t* out = p.idx + static_cast<int64_t>(row) * p.budget;
+  const int tid = threadIdx.x;
+  const int w = tid >> 6;
+  const int lane = tid & 63;
+  const int j0 = tid * kSelKpt;  // this thread's segment
+
+  uint32_t key[kSelKpt];
+  if (keep > 0) {
+    const bool vec = (reinterpret_cast<uintptr_t>(v) & 15u) == 0;
+    const int n4 = vec ? n / 4 : 0;
+#pragma unroll 4
+    for (int i = tid; i < n4; i += kSelThreads) {
+      const float4 x = reinterpret_cast<const float4*>(v)[i];
+      buf[sk_pad(4 * i)] = x.x;
+      buf[sk_pad(4 * i + 1)] = x.y;
+      buf[sk_pad(4 * i + 2)] = x.z;
+      buf[sk_pad(4 * i + 3)] = x.w;
+    }
+    for (int j = 4 * n4 + tid; j < n; j += kSelThreads) buf[sk_pad(j)] = v[j];
+    __syncthreads();
+    // Raw vote at segment offset o (-h <= o < 66 + h) of this thread's window,
+    // +0 outside the prefix; the word index stays inside the buffer.
+    const int base = j0 + tid;  // sk_pad(j0)
+    auto raw = [&](int o) -> float {
+      const int jj = j0 + o;
+      const int seg = o < 0 ? -1 : (o >= kSelKpt ? 1 : 0);
+      const float x = buf[min(max(base + o + seg, 0), kBuf - 1)];  // always inside the buffer
+      return (jj >= 0 && jj < n) ? x : 0.f;
+    };
+    // Taps -POOL/2 .. POOL/2 in order; a tap outside the prefix adds an exact
+    // +0 (the running sum starts at +0, so it is never -0), which leaves every
+    // sum as sk_pooled forms it.
+    constexpr int h = POOL / 2;
+#pragma unroll
+    for (int e = 0; e < kSelKpt; ++e) {
+      float acc = 0.f;
+#pragma unroll
+      for (int t = -h; t <= h; ++t) acc += raw(e + t);
+      key[e] = j0 + e < n ? sk_key(acc / static_cast<float>(POOL)) : 0u;
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < kSelKpt; ++e) key[e] = 0u;
+  }
+  __syncthreads();  // every raw read is done: the buffer holds the histograms now
+
+  // Positions past the row hold key 0, the smallest key: with keep <= n they
+  // leave the keep-th largest key and the count above it as they are, so the
+  // radix passes count every register without a mask (only the ties of the
+  // compaction below look at the position).
+  uint32_t tau = 0, above = 0;
+  if (keep > 0)
+    sk_radix_select<kSelKpt>([&](int e) { return key[e]; }, [](int) { return true; }, keep,
+                             reinterpret_cast<uint32_t*>(buf), wsum, &s_prefix, &s_above, tau,
+                             above);
+  const uint32_t need_eq = keep > 0 ? static_cast<uint32_t>(keep) - above : 0;
+
+  if (keep > 0) {
+    // Keep key > tau, and key == tau while fewer than need_eq of those lie
+    // before it; ties go to the smaller position.
+    uint32_t n_gt = 0, n_eq = 0;
+#pragma unroll
+    for (int e = 0; e < kSelKpt; ++e) {
+      n_gt += key[e] > tau;  // never a position past the row (key 0)
+      n_eq += j0 + e < n && key[e] == tau;
+    }
+    uint32_t eq_total;
+    const uint32_t eq_before = sk_block_scan(n_eq, wsum, eq_total, lane, w);
+    const uint32_t eq_take =
+        eq_before >= need_eq ? 0u : (need_eq - eq_before < n_eq ? need_eq - eq_before : n_eq);
+    uint32_t take_total;
+    uint32_t pos = sk_block_scan(n_gt + eq_take, wsum, take_total, lane, w);
+    uint32_t eq_left = eq_take;
+#pragma unroll
+    for (int e = 0; e < kSelKpt; ++e) {
+      const bool eq = j0 + e < n && key[e] == tau;
+      const bool take = key[e] > tau || (eq && eq_left > 0);
+      eq_left -= (eq && eq_left > 0) ? 1u : 0u;
+      if (take) out[pos++] = j0 + e;
+    }
+  }
+  // The observation window, always kept.
+  const int kept = keep > 0 ? keep : 0;
+  for (int j = n + tid; j < S; j += kSelThreads) out[kept + (j - n)] = j;
+  if (tid == 0 && (row % p.rows_per_seq) == 0) p.counts[b] = kept + (S - n);
+}
+
+// Global instance, rows longer than kSelRegKeys: every sweep pools from
+// global memory (each pooled key is formed in sk_pooled's order, so both
+// instances see the same keys), kSelPer * kSelThreads positions per step.
 __global__ void __launch_bounds__(kSelThreads) snapkv_select_kernel(const SnapkvSelectParams p) {
-  __shared__ uint32_t keys[LDS ? kSelLdsKeys : 1];
-  __shared__ float stage[LDS ? kSelStage : 1];
   __shared__ uint32_t hist[kSelWaves][256];
   __shared__ uint32_t wsum[kSelWaves];
   __shared__ uint32_t s_prefix, s_above;
@@ -367,51 +529,7 @@ __global__ void __launch_bounds__(kSelThreads) snapkv_select_kernel(const Snapkv
   const int w = tid >> 6;
   const int lane = tid & 63;
 
-  auto key_at = [&](int j) -> uint32_t {
-    if (LDS) return keys[j];
-    return sk_key(sk_pooled(v, n, j, p.pool));
-  };
-
-  if (LDS && keep > 0) {
-    float* rawf = reinterpret_cast<float*>(keys);
-    const bool vec = (reinterpret_cast<uintptr_t>(v) & 15u) == 0;
-    const int n4 = vec ? n / 4 : 0;
-#pragma unroll 4
-    for (int i = tid; i < n4; i += kSelThreads)
-      reinterpret_cast<float4*>(rawf)[i] = reinterpret_cast<const float4*>(v)[i];
-    for (int j = 4 * n4 + tid; j < n; j += kSelThreads) rawf[j] = v[j];
-    __syncthreads();
-    const int h = p.pool / 2;
-    const int span = kSelStep + 2 * h;
-    for (int base = 0; base < n; base += kSelStep) {
-      // stage[i] <- raw position base - h + i (0 outside the prefix).
-      float x[kSelStagePer];
-#pragma unroll
-      for (int r = 0; r < kSelStagePer; ++r) {
-        const int i = tid + r * kSelThreads;
-        const int j = base - h + i;
-        x[r] = 0.f;
-        if (i < span && j >= 0 && j < n) x[r] = (base > 0 && i < 2 * h) ? stage[kSelStep + i] : rawf[j];
-      }
-      __syncthreads();
-#pragma unroll
-      for (int r = 0; r < kSelStagePer; ++r) {
-        const int i = tid + r * kSelThreads;
-        if (i < span) stage[i] = x[r];
-      }
-      __syncthreads();
-#pragma unroll
-      for (int e = 0; e < kSelPer; ++e) {
-        const int j = base + tid * kSelPer + e;
-        if (j < n) {
-          float s = 0.f;
-          for (int t2 = 0; t2 < p.pool; ++t2) s += stage[j - base + t2];
-          keys[j] = sk_key(s / static_cast<float>(p.pool));
-        }
-      }
-      __syncthreads();
-    }
-  }
+  auto key_at = [&](int j) -> uint32_t { return sk_key(sk_pooled(v, n, j, p.pool)); };
 
   // Radix select, most significant byte first: after four passes tau is the
   // key of the keep-th largest pooled vote and `above` keys exceed it.
@@ -436,8 +554,6 @@ __global__ void __launch_bounds__(kSelThreads) snapkv_select_kernel(const Snapkv
         }
       }
       __syncthreads();
-      // Threads 0..255 own digits 255..0; a scan from the top digit finds the
-      // one where the running count reaches keep.
       uint32_t cnt = 0;
       const uint32_t d = 255u - static_cast<uint32_t>(tid);
       if (tid < 256)
@@ -556,10 +672,17 @@ hipError_t launch_snapkv_votes(const SnapkvParams& p, int head_dim, bool bf16, i
 
 hipError_t launch_snapkv_select(const SnapkvSelectParams& p, hipStream_t s) {
   if (p.rows <= 0) return hipSuccess;
-  if (p.stride <= kSelLdsKeys && p.pool / 2 <= kSelHalo)
-    hipLaunchKernelGGL(snapkv_select_kernel<true>, dim3(p.rows), dim3(kSelThreads), 0, s, p);
-  else
-    hipLaunchKernelGGL(snapkv_select_kernel<false>, dim3(p.rows), dim3(kSelThreads), 0, s, p);
+  const dim3 grid(p.rows), block(kSelThreads);
+  if (p.stride <= kSelRegKeys && p.pool / 2 <= kSelRegHalo) {
+    switch (p.pool) {  // odd, checked by the caller
+      case 1: hipLaunchKernelGGL(snapkv_select_reg_kernel<1>, grid, block, 0, s, p); break;
+      case 3: hipLaunchKernelGGL(snapkv_select_reg_kernel<3>, grid, block, 0, s, p); break;
+      case 5: hipLaunchKernelGGL(snapkv_select_reg_kernel<5>, grid, block, 0, s, p); break;
+      default: hipLaunchKernelGGL(snapkv_select_reg_kernel<7>, grid, block, 0, s, p); break;
+    }
+  } else {
+    hipLaunchKernelGGL(snapkv_select_kernel, grid, block, 0, s, p);
+  }
   return hipGetLastError();
 }
 
