@@ -67,18 +67,22 @@ SELECT = [
     (2, 300, 8, 40, 1, [308, 100], 1),
     (1, 70, 32, 64, 5, [32], 2),           # prompt == window: nothing to select
     (2, 1000, 32, 33, 3, [1032, 900], 2),  # one prefix position kept
-    (2, 40000, 32, 2049, 5, [40032, 20000], 2),  # rows longer than the LDS key buffer
+    (2, 40000, 32, 2049, 5, [40032, 20000], 2),  # rows longer than the register instance
+    (2, 2000, 16, 600, 7, [2016, 1500], 2),      # the widest pooling of the register instance
+    (1, 900, 8, 400, 9, [908], 2),               # wider pooling: the global instance
+    (2, 5000, 32, 3000, 5, [4999, 3001], 2, 1),  # all votes 0: every key ties
 ]
 
 
 @pytest.mark.parametrize("case", SELECT, ids=[f"sel{i}" for i in range(len(SELECT))])
 def test_select_exact(case):
-    _, stride, n_obs, budget, pool, lens, Hkv = case
+    _, stride, n_obs, budget, pool, lens, Hkv = case[:7]
+    hi = case[7] if len(case) > 7 else 40
     B = len(lens)
     rng = np.random.default_rng(stride * 7 + budget)
     # Small integers (heavy ties): 5-tap sums are exact, so pooled order is the
     # same in fp32 (GPU) and fp64 (oracle).
-    vals = rng.integers(0, 40, size=(B, Hkv, stride)).astype(np.float32)
+    vals = rng.integers(0, hi, size=(B, Hkv, stride)).astype(np.float32)
     idx, cnt = md.md_snapkv_select(torch.from_numpy(vals).to(DEV),
                                    torch.tensor(lens, dtype=torch.int32, device=DEV), n_obs,
                                    budget, pool=pool)
