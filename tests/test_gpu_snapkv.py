@@ -71,6 +71,7 @@ SELECT = [
     (2, 2000, 16, 600, 7, [2016, 1500], 2),      # the widest pooling of the register instance
     (1, 900, 8, 400, 9, [908], 2),               # wider pooling: the global instance
     (2, 5000, 32, 3000, 5, [4999, 3001], 2, 1),  # all votes 0: every key ties
+    (3, 1001, 16, 300, 5, [1017, 800, 499], 2),  # rows not 16-byte aligned: scalar copies
 ]
 
 
