@@ -218,7 +218,7 @@ int run_attention(const md_attn_args* a, int mode, int n_sink, int window, void*
     // The chunks merge in a second launch by default.  MD_FUSED_MERGE = 1
     // merges them inside the attention launch instead, in the last workgroup
     // of each head group to finish: measured on MI355X, same process, that
-    // was 1-4 us slower per call (the second launch follows the first with
+    // was 1-10 us slower per call (the second launch follows the first with
     // no gap on the stream, and the device-scope fences around the arrival
     // counters cost more than the launch saves), so it stays opt-in.  The
     // balanced verify always merges its cut groups inside the launch: only
@@ -489,6 +489,13 @@ int md_kv_gather(const md_kv_cache* dst, const md_kv_cache* src, const int32_t* 
   const double items = 2.0 * p.B * idx_stride * p.Hkv * p.row_vecs;
   if (items > 9.0e18) return MD_ERR_INVALID_ARG;
   p.n_items = 2 * static_cast<int64_t>(p.B) * idx_stride * p.Hkv * p.row_vecs;
+  auto log2_exact = [](int32_t x) {
+    int s = 0;
+    while ((int64_t{1} << s) < x) ++s;
+    return (int64_t{1} << s) == x ? s : -1;
+  };
+  p.vec_shift = log2_exact(p.row_vecs);
+  p.head_shift = log2_exact(p.Hkv);
   const hipError_t e = md::launch_kv_gather(p, src->page_size != 0, dst->page_size != 0,
                                             static_cast<hipStream_t>(stream));
   return e == hipSuccess ? MD_OK : md::hip_fail(e);

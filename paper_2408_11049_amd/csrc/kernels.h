@@ -150,6 +150,8 @@ struct GatherParams {
   int32_t row_vecs;         // 16-byte vectors per row (d * element size / 16)
   int32_t esize;
   int64_t n_items;          // 2 (K, V) * B * idx_stride * Hkv * row_vecs
+  int32_t vec_shift;        // log2(row_vecs) and log2(Hkv) when both are powers of
+  int32_t head_shift;       // two (then one grid row per sequence), else -1
 };
 
 struct AcceptParams {

@@ -137,7 +137,62 @@ __global__ void __launch_bounds__(256) kv_gather_kernel(const GatherParams p) {
   }
 }
 
+// The same copy when row_vecs and Hkv are powers of two: grid (items of one
+// sequence, sequences, K/V), each sequence's items in the order above, so an
+// item's (list slot, kv head, vector) are shifts and masks of its index
+// rather than 64-bit divisions, and only the listed rows are visited.
+template <bool SRC_PAGED, bool DST_PAGED>
+__global__ void __launch_bounds__(256) kv_gather_pow2_kernel(const GatherParams p) {
+  const bool is_v = blockIdx.z != 0;
+  const int vshift = p.vec_shift, hshift = p.head_shift;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * 256;
+  for (int b = blockIdx.y; b < p.B; b += gridDim.y) {
+    const int n = min(max(p.idx_len[b], 0), p.idx_stride);
+    if (!is_v && blockIdx.x == 0 && threadIdx.x == 0 && p.dst_lens) p.dst_lens[b] = n;
+    const int64_t live = static_cast<int64_t>(n) << (hshift + vshift);
+    const int src_len = p.src_lens[b];
+    const int32_t* idxb = p.idx + static_cast<int64_t>(b) * p.Hkv * p.idx_stride;
+    for (int64_t item = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; item < live;
+         item += stride) {
+      const int c = static_cast<int>(item & ((int64_t{1} << vshift) - 1));
+      const int64_t r = item >> vshift;
+      const int hk = static_cast<int>(r & ((int64_t{1} << hshift) - 1));
+      const int j = static_cast<int>(r >> hshift);
+      int64_t dblk, dtok;
+      if (!cache_row<DST_PAGED>(p.dst, b, j, dblk, dtok)) continue;
+      const int32_t pos = idxb[static_cast<int64_t>(hk) * p.idx_stride + j];
+      u32x4 val = u32x4{0u, 0u, 0u, 0u};
+      int64_t sblk, stok;
+      if (pos >= 0 && pos < src_len && cache_row<SRC_PAGED>(p.src, b, pos, sblk, stok)) {
+        const int64_t so =
+            (sblk * p.src.s_blk + stok * p.src.s_tok + hk * p.src.s_head) * p.esize + c * 16;
+        val = __builtin_nontemporal_load(
+            reinterpret_cast<const u32x4*>((is_v ? p.src.v : p.src.k) + so));
+      }
+      const int64_t dof =
+          (dblk * p.dst.s_blk + dtok * p.dst.s_tok + hk * p.dst.s_head) * p.esize + c * 16;
+      *reinterpret_cast<u32x4*>((is_v ? p.dst.v : p.dst.k) + dof) = val;
+    }
+  }
+}
+
 hipError_t launch_kv_gather(const GatherParams& p, bool src_paged, bool dst_paged, hipStream_t s) {
+  if (p.vec_shift >= 0 && p.head_shift >= 0) {
+    const int64_t per_seq = static_cast<int64_t>(p.idx_stride) << (p.vec_shift + p.head_shift);
+    const int64_t want = (per_seq + 255) / 256;
+    const dim3 g(static_cast<uint32_t>(want < 4096 ? want : 4096),
+                 static_cast<uint32_t>(p.B < 65535 ? p.B : 65535), 2),
+        blk(256);
+    if (src_paged && dst_paged)
+      hipLaunchKernelGGL((kv_gather_pow2_kernel<true, true>), g, blk, 0, s, p);
+    else if (src_paged)
+      hipLaunchKernelGGL((kv_gather_pow2_kernel<true, false>), g, blk, 0, s, p);
+    else if (dst_paged)
+      hipLaunchKernelGGL((kv_gather_pow2_kernel<false, true>), g, blk, 0, s, p);
+    else
+      hipLaunchKernelGGL((kv_gather_pow2_kernel<false, false>), g, blk, 0, s, p);
+    return hipGetLastError();
+  }
   const int64_t want = (p.n_items + 255) / 256;
   const uint32_t blocks = static_cast<uint32_t>(want < (1 << 20) ? want : (1 << 20));
   const dim3 g(blocks), blk(256);
