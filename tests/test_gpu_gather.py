@@ -60,6 +60,9 @@ GATHER = [
     ("contig_to_paged_f32_d64", 2, 4, 64, "f32", [90, 200], 0, 8, 50, [50, 17]),
     ("paged_to_paged_bf16", 3, 8, 128, "bf16", [1000, 64, 333], 16, 16, 257, [257, 64, 300]),
     ("paged1_to_paged4_f32", 2, 1, 64, "f32", [37, 20], 1, 4, 9, [9, 5]),
+    # shapes that are not powers of two (12 vectors per row, 3 or 6 kv heads)
+    ("contig_to_paged_bf16_h3_d96", 2, 3, 96, "bf16", [200, 150], 0, 8, 30, [30, 12]),
+    ("paged_to_contig_f32_h6", 2, 6, 64, "f32", [100, 64], 16, 0, 20, [20, 7]),
 ]
 
 
