@@ -451,8 +451,9 @@ __global__ void __launch_bounds__(kSelRegThreads) snapkv_select_reg_kernel(const
     }
     for (int j = 4 * n4 + tid; j < n; j += kSelRegThreads) buf[sk_pad(j)] = v[j];
     __syncthreads();
-    // Raw vote at segment offset o (-h <= o < 66 + h) of this thread's window,
-    // +0 outside the prefix; the word index stays inside the buffer.
+    // Raw vote at segment offset o (-POOL/2 <= o < 33 + POOL/2) of this
+    // thread's window, +0 outside the prefix; the word index stays inside the
+    // buffer.
     const int base = j0 + kSelPadW * tid;  // sk_pad(j0)
     auto raw = [&](int o) -> float {
       const int jj = j0 + o;
@@ -483,9 +484,9 @@ __global__ void __launch_bounds__(kSelRegThreads) snapkv_select_reg_kernel(const
   // compaction below look at the position).
   uint32_t tau = 0, above = 0;
   if (keep > 0)
-    sk_radix_select<kSelKpt, kSelRegThreads>([&](int e) { return key[e]; }, [](int) { return true; }, keep,
-                             reinterpret_cast<uint32_t*>(buf), wsum, &s_prefix, &s_above, tau,
-                             above);
+    sk_radix_select<kSelKpt, kSelRegThreads>(
+        [&](int e) { return key[e]; }, [](int) { return true; }, keep,
+        reinterpret_cast<uint32_t*>(buf), wsum, &s_prefix, &s_above, tau, above);
   const uint32_t need_eq = keep > 0 ? static_cast<uint32_t>(keep) - above : 0;
 
   if (keep > 0) {
