@@ -218,3 +218,48 @@ def test_config_counter_summary(tmp_path):
         extra = 10.0 if ci == 4 else 0.0
         assert float(r[3]) == pytest.approx((1000.0 * (ci + 1) + extra) * 1024 * 2, rel=1e-3)
         assert float(r[4]) == pytest.approx((1000.0 * (ci + 1) + extra) * 1024, rel=1e-3)
+
+
+def test_prefill_summary(tmp_path):
+    """--summarize prefill: trace times and counter bytes of the SnapKV and
+    gather kernels, the counters scaled by the run's 1 GiB copy, each read
+    compared with its algorithmic bytes from the bench line."""
+    import csv
+    import json
+    P0 = "void md::snapkv_pass_kernel<128, true, 2, true, 0, 64>(md::SnapkvParams)"
+    P1 = "void md::snapkv_pass_kernel<128, true, 2, true, 1, 64>(md::SnapkvParams)"
+    S, G, C = "void md::snapkv_select_reg_kernel<5>(x)", "void md::kv_gather_pow2_kernel<true, false>(x)", \
+        "md::bench_copy_kernel(x)"
+    seq = [(C, 0, 0), (P0, 10.0, 2.0), (P1, 10.0, 4.0), (S, 4.0, 1.0), (G, 6.0, 5.0)] * 2
+    tr, fe, wr = tmp_path / "t.csv", tmp_path / "f.csv", tmp_path / "w.csv"
+    with open(tr, "w", newline="") as f:
+        w = csv.writer(f)
+        w.writerow(["Dispatch_Id", "Kernel_Name", "Start_Timestamp", "End_Timestamp"])
+        for i, (n, _, _) in enumerate(seq):
+            w.writerow([i + 1, n, 1000 * i, 1000 * i + (2000 if n == P0 else 500)])
+    for path, ctr, col in ((fe, "FETCH_SIZE", 1), (wr, "WRITE_SIZE", 2)):
+        with open(path, "w", newline="") as f:
+            w = csv.writer(f)
+            w.writerow(["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
+            for i, row in enumerate(seq):
+                # the copy reads and writes 1 GiB: FETCH_SIZE reads half of it here
+                val = (512.0 * 1024 if col == 1 else 1024.0 * 1024) if row[0] == C else row[col] * 1024
+                w.writerow([i + 1, row[0], ctr, val])
+    line = {"metric": "m", "value": 1, "unit": "GB/s", "steps": 1, "warmup": 1,
+            "detail": {"snapkv_votes_k_bytes (two passes over K)": 2 * 10.0 * 2 ** 20 * 2,
+                       "kv_gather_bytes (read + write)": 2 * 6.0 * 2 ** 20 * 2,
+                       "t_snapkv_votes_us (prefill, 32 observation queries)": 1.0,
+                       "t_snapkv_select_us (pool 5, budget 2049)": 1.0,
+                       "t_kv_gather_us (the 2049 listed rows into a draft cache, once per prompt)": 1.0}}
+    bj = tmp_path / "b.json"
+    bj.write_text(json.dumps(line) + "\n")
+    text = bench.summarize_prefill(str(tr), str(fe), str(wr), str(bj), "cmd")
+    rows = {r.split("|")[2].strip(): r for r in text.splitlines() if r.startswith("| `")}
+    assert set(rows) == {"softmax statistics over K", "votes (K again, votes written)",
+                         "pool, radix select, compaction", "listed rows into a draft cache"}
+    # scale_fetch = 2: each pass reads 2 x 10 MiB = its algorithmic K bytes exactly
+    assert rows["softmax statistics over K"].rstrip(" |").endswith("1.0000")
+    assert "| 2.0 |" in rows["softmax statistics over K"]  # 2000 ns per dispatch
+    # the selection's algorithmic read is what the votes pass wrote (4 MiB); it reads 8 MiB
+    assert rows["pool, radix select, compaction"].rstrip(" |").endswith("2.0000")
+    assert "bench_copy" not in text
