@@ -1,11 +1,14 @@
 """Every tuning override the library reads from the environment, against the
 fp64 oracle: MD_PREFETCH_DEPTH (a second tile in flight: its own kernel
 instances), MD_OCCUPANCY (instances compiled for one or two waves per SIMD),
-MD_LPT (longest-first dispatch off, or on wherever a plan allows it) and
+MD_LPT (longest-first dispatch off, or on wherever a plan allows it),
 MD_HEADS_PER_WG (one head or a head pair per workgroup), MD_FUSED_MERGE
 (split ranges merged by each head group's last workgroup instead of a second
-launch) and MD_SLOTS_SCALE (plans for two or four workgroups per compute
-unit: more and shorter chunks).  The overrides are
+launch), MD_SLOTS_SCALE (plans for two or four workgroups per compute unit:
+more and shorter chunks), MD_BALANCED and MD_BAL_WG_PER_CU (the balanced
+verify off, or forced wherever allowed, with one or two workgroups per
+compute unit) and MD_WAVES (eight waves per workgroup wherever the wide
+instances exist).  The overrides are
 read on every call, so one process sweeps them all; each setting runs the
 same shapes: one to four 16-row tiles, both head dims, the streaming and
 listed drafts, a split range with its merge and a longest-first batch."""
