@@ -1054,6 +1054,101 @@ def summarize_prefill(trace_csv, fetch_csv, write_csv, bench_json, cmd):
     return "\n".join(out) + "\n"
 
 
+# The kernels around verification in the bench line, told apart by grid size
+# (work-items): the (gamma+1)-token append into the paged cache, the one-token
+# appends of the engine-shaped steps, both acceptance passes and the commit.
+def _grid(d):
+    return int(d.get("grid", 0))
+
+
+def summarize_steps(trace_csv, fetch_csv, write_csv, bench_json, cmd):
+    """Kernel times (trace) and HBM bytes per dispatch of the step kernels,
+    grouped by (kernel, grid size); counters scaled by the run's 1 GiB copy."""
+    rec = _bench_line(bench_json)
+    det = rec["detail"]
+
+    def load(path):
+        out = []
+        for r in _rows(path):
+            g = r.get("Grid_Size_X") or r.get("Grid_Size") or 0
+            out.append(dict(r, _grid=int(g)))
+        return out
+
+    def dispatches(rows):
+        ds = {}
+        for r in rows:
+            d = ds.setdefault(int(r["Dispatch_Id"]), {"name": r["Kernel_Name"], "grid": r["_grid"]})
+            if r.get("Start_Timestamp"):
+                d["start"], d["end"] = int(r["Start_Timestamp"]), int(r["End_Timestamp"])
+            if "Counter_Name" in r:
+                d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+        return [ds[k] for k in sorted(ds)]
+
+    trace = dispatches(load(trace_csv))
+    ctr, calib = {}, {}
+    for c, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        ds = dispatches(load(path))
+        calib[c] = [d for d in ds if "bench_copy_kernel" in d["name"]][-1][c]
+        ctr[c] = ds
+    gib = float(1 << 30)
+    scale = {c: gib / (calib[c] * 1024.0) for c in calib}
+    keys = ("kv_append_kernel", "argmax_partial_kernel", "accept_kernel", "kv_commit_kernel")
+    groups = {}
+    for d in trace:
+        if any(k in d["name"] for k in keys):
+            groups.setdefault((_short(d["name"]), _grid(d)), []).append((d["end"] - d["start"]) / 1000.0)
+    alg = {"argmax_partial_kernel": (det["greedy_accept_logits_bytes"], "the logits once"),
+           "kv_append_kernel": (det["kv_append_bytes (read + write)"] / 2, "the new K/V rows once")}
+    big_append = max((g for (n, g) in groups if "kv_append" in n), default=0)
+    am = [us for (n, g), us in groups.items() if "argmax_partial_kernel" in n]
+    argmax_gbs = (det["greedy_accept_logits_bytes"] / (sum(am[0]) / len(am[0])) / 1e3
+                  if am else float("nan"))
+    out = ["# Kernels around verification: KV append, greedy acceptance, commit (rocprofv3)",
+           "",
+           f"Workload: the verify step of {WORKLOAD} -- B = 64, gamma = 4 (5 tokens per",
+           "sequence), Hkv = 8, d = 128, bf16 K/V in 16-token pages; fp32 verifier logits over",
+           "the Llama-3 vocabulary (128256 entries) with seeded planted targets; commit into",
+           "2049-entry listed draft caches plus a 1024-slot rolling ring; the engine-shaped",
+           "steps append one token per draft.  Cold cache (1 GiB evicted before every timed",
+           "call).  One MI355X (gfx950).",
+           "",
+           "Commands (from /tmp with TMPDIR=/tmp; R = the repository root): the kernel trace and",
+           "the FETCH_SIZE and WRITE_SIZE passes of the attention profiles,",
+           ""]
+    out += [f"    {c}" for c in cmd.split(" ;; ")]
+    out += ["",
+            f"HBM bytes = KiB x 1024 x scale, calibrated on the run's 1 GiB copy (scale_fetch =",
+            f"{scale['FETCH_SIZE']:.5f}, scale_write = {scale['WRITE_SIZE']:.5f}); means over the "
+            "dispatches of each (kernel, grid size).",
+            "",
+            "| kernel | work-items | calls | avg us | min | max | HBM read bytes | HBM write bytes | "
+            "algorithmic read bytes | read / algorithmic |",
+            "|---|---|---|---|---|---|---|---|---|---|"]
+    for (name, grid), us in sorted(groups.items()):
+        def mean(c):
+            v = [d[c] * 1024 * scale[c] for d in ctr[c] if _short(d["name"]) == name and _grid(d) == grid]
+            return sum(v) / len(v) if v else float("nan")
+        r_b, w_b = mean("FETCH_SIZE"), mean("WRITE_SIZE")
+        a = next((alg[k] for k in alg if k in name), None)
+        if a is None or ("kv_append" in name and grid != big_append):
+            algs, ratio = "--", "--"
+        else:
+            algs, ratio = f"{a[0]:.4e} ({a[1]})", f"{r_b / a[0]:.4f}"
+        out.append(f"| `{name}` | {grid} | {len(us)} | {sum(us) / len(us):.2f} | {min(us):.2f} | "
+                   f"{max(us):.2f} | {r_b:.4e} | {w_b:.4e} | {algs} | {ratio} |")
+    out += ["",
+            "bench.py's HIP events around the whole calls of the same run (under the profiler): "
+            f"append {det['t_kv_append_us (gamma+1 tokens, paged)']:.2f} us, greedy accept "
+            f"{det['t_greedy_accept_us (fp32 logits, vocab 128256)']:.2f} us (both passes), "
+            f"commit {det['t_kv_commit_us (lengths + 1024-slot ring)']:.2f} us.",
+            "",
+            f"Reading: the argmax pass streams the logits at {argmax_gbs:.0f} GB/s by kernel "
+            "time; the appends,",
+            "the acceptance pass and the commit are launch-latency bound (a few us each from a",
+            "cold cache)."]
+    return "\n".join(out) + "\n"
+
+
 def summarize_lds(csv_path, bench_json, cmd):
     """LDS counters per kernel instance (means per dispatch over every dispatch
     of that instance in the run), the bench's timed verify and draft named."""
@@ -1107,7 +1202,7 @@ def main():
     ap.add_argument("--paged-ab", action="store_true",
                     help="only the paged / sequential-page / contiguous verify A/B (profiles/)")
     ap.add_argument("--summarize", choices=["trace", "counters", "mfma", "latency", "paged", "lds",
-                                            "configs", "config-counters", "prefill"])
+                                            "configs", "config-counters", "prefill", "steps"])
     ap.add_argument("--csv", nargs="+")
     ap.add_argument("--bench-json", nargs="+")
     ap.add_argument("--cmd", default="")
@@ -1124,7 +1219,9 @@ def main():
               "config-counters": lambda: summarize_config_counters(
                   args.csv[0], args.csv[1], args.bench_json[0], args.bench_json[-1], args.cmd),
               "prefill": lambda: summarize_prefill(args.csv[0], args.csv[1], args.csv[2],
-                                                   args.bench_json[0], args.cmd)}
+                                                   args.bench_json[0], args.cmd),
+              "steps": lambda: summarize_steps(args.csv[0], args.csv[1], args.csv[2],
+                                               args.bench_json[0], args.cmd)}
         sys.stdout.write(fn[args.summarize]())
         return
     if args.gpus != 1:

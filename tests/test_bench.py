@@ -263,3 +263,45 @@ def test_prefill_summary(tmp_path):
     # the selection's algorithmic read is what the votes pass wrote (4 MiB); it reads 8 MiB
     assert rows["pool, radix select, compaction"].rstrip(" |").endswith("2.0000")
     assert "bench_copy" not in text
+
+
+def test_steps_summary_groups_by_grid(tmp_path):
+    """--summarize steps: step kernels grouped by (kernel, grid size), so the
+    one-token appends of the engine-shaped steps do not mix with the timed
+    (gamma+1)-token append, whose read is compared with its algorithmic bytes."""
+    import csv
+    import json
+    A, M, C = "void md::kv_append_kernel<true>(x)", "void md::argmax_partial_kernel<false, true>(x)", \
+        "md::bench_copy_kernel(x)"
+    seq = [(C, 1, 0, 0), (A, 81920, 2.0, 1.0), (A, 16384, 0.5, 0.25), (M, 573440, 8.0, 0.0),
+           (A, 81920, 2.0, 1.0)]
+    tr, fe, wr = tmp_path / "t.csv", tmp_path / "f.csv", tmp_path / "w.csv"
+    with open(tr, "w", newline="") as f:
+        w = csv.writer(f)
+        w.writerow(["Dispatch_Id", "Kernel_Name", "Grid_Size_X", "Start_Timestamp", "End_Timestamp"])
+        for i, (n, g, _, _) in enumerate(seq):
+            w.writerow([i + 1, n, g, 10000 * i, 10000 * i + (4000 if n == M else 1000)])
+    for path, ctr, col in ((fe, "FETCH_SIZE", 2), (wr, "WRITE_SIZE", 3)):
+        with open(path, "w", newline="") as f:
+            w = csv.writer(f)
+            w.writerow(["Dispatch_Id", "Kernel_Name", "Grid_Size", "Counter_Name", "Counter_Value"])
+            for i, row in enumerate(seq):
+                val = (512.0 * 1024 if col == 2 else 1024.0 * 1024) if row[0] == C else row[col] * 1024
+                w.writerow([i + 1, row[0], row[1], ctr, val])
+    line = {"metric": "m", "value": 1, "unit": "GB/s", "steps": 1, "warmup": 1,
+            "detail": {"greedy_accept_logits_bytes": 16.0 * 2 ** 20,
+                       "kv_append_bytes (read + write)": 2 * 4.0 * 2 ** 20,
+                       "t_kv_append_us (gamma+1 tokens, paged)": 1.0,
+                       "t_greedy_accept_us (fp32 logits, vocab 128256)": 1.0,
+                       "t_kv_commit_us (lengths + 1024-slot ring)": 1.0}}
+    bj = tmp_path / "b.json"
+    bj.write_text(json.dumps(line) + "\n")
+    text = bench.summarize_steps(str(tr), str(fe), str(wr), str(bj), "cmd")
+    rows = [r for r in text.splitlines() if r.startswith("| `")]
+    big = next(r for r in rows if "| 81920 |" in r)
+    small = next(r for r in rows if "| 16384 |" in r)
+    arg = next(r for r in rows if "argmax" in r)
+    assert "| 2 |" in big and big.rstrip(" |").endswith("1.0000")  # 2 MiB x 2 = 4 MiB
+    assert small.rstrip(" |").endswith("--")
+    assert arg.rstrip(" |").endswith("1.0000") and "| 4.00 |" in arg
+    assert "bench_copy" not in text
