@@ -115,17 +115,28 @@ snapkv_pass_kernel(const SnapkvParams p) {
 
   // Cooperative tile load: thread -> key row (threadIdx / LPT) + n * ROWS_PER_WG_LOAD,
   // 16 B chunk threadIdx % LPT.  Keys past the range read element 0 and are masked.
-  auto load_tile = [&](sk_u32x4 (&x)[SH::NLD], int tile) {
+  // Page ids are read one tile ahead of the K loads that use them, so a
+  // tile's loads never wait on a page-table read.
+  auto load_pids = [&](int (&pid)[SH::NLD], int tile) {
+    if constexpr (PAGED) {
+      for (int n = 0; n < SH::NLD; ++n) {
+        const int tt = n * SH::ROWS_PER_WG_LOAD + threadIdx.x / SH::LPT;
+        const int j = v_begin + tile * KT + tt;
+        const bool ok = tile < n_tiles && j < v_end;
+        pid[n] = ptab[ok ? (j >> p.page_shift) : 0];
+      }
+    }
+  };
+  auto load_tile = [&](sk_u32x4 (&x)[SH::NLD], int tile, const int (&pid)[SH::NLD]) {
     for (int n = 0; n < SH::NLD; ++n) {
       const int tt = n * SH::ROWS_PER_WG_LOAD + threadIdx.x / SH::LPT;
       const int j = v_begin + tile * KT + tt;
       bool ok = tile < n_tiles && j < v_end;
       int64_t off = 0;
       if (PAGED) {
-        const int pid = ptab[ok ? (j >> p.page_shift) : 0];
-        ok = ok && pid >= 0 && pid < p.num_pages;
-        off = ok ? static_cast<int64_t>(pid) * p.s_blk + static_cast<int64_t>(j & pmask) * p.s_tok +
-                       head_off
+        ok = ok && pid[n] >= 0 && pid[n] < p.num_pages;
+        off = ok ? static_cast<int64_t>(pid[n]) * p.s_blk +
+                       static_cast<int64_t>(j & pmask) * p.s_tok + head_off
                  : 0;
       } else {
         off = ok ? static_cast<int64_t>(b) * p.s_blk + static_cast<int64_t>(j) * p.s_tok + head_off
@@ -150,12 +161,16 @@ snapkv_pass_kernel(const SnapkvParams p) {
     }
 
   sk_u32x4 xr[SH::NLD];
-  load_tile(xr, 0);
+  int pids[SH::NLD] = {};
+  load_pids(pids, 0);
+  load_tile(xr, 0, pids);
+  load_pids(pids, 1);
   for (int tile = 0; tile < n_tiles; ++tile) {
     const int buf = tile & 1;
     store_tile(xr, buf);
     __syncthreads();
-    load_tile(xr, tile + 1);  // next tile in flight while this one is used
+    load_tile(xr, tile + 1, pids);  // next tile in flight while this one is used
+    load_pids(pids, tile + 2);
     const int v0 = v_begin + tile * KT;
 
     // S = Q K^T for this wave's row tiles and the tile's NB 16-key blocks.
