@@ -963,9 +963,9 @@ LDS_COUNTERS = ["SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE", "SQ_LDS_ADDR_CONFLI
 # The prefill-time kernels of the bench line: the SnapKV passes and selection
 # and the gather of the selected rows into a draft cache of their own.
 PREFILL_KERNELS = [
-    ("snapkv_pass_kernel", ", 0, ", "softmax statistics over K", "k_once"),
+    ("snapkv_pass_kernel", ", 0, 64", "softmax statistics over K", "k_once"),
     ("snapkv_lse_kernel", "", "merge chunk statistics", None),
-    ("snapkv_pass_kernel", ", 1, ", "votes (K again, votes written)", "k_once"),
+    ("snapkv_pass_kernel", ", 1, 64", "votes (K again, votes written)", "k_once"),
     ("snapkv_select", "", "pool, radix select, compaction", "votes"),
     ("kv_gather", "", "listed rows into a draft cache", "gather"),
 ]
@@ -1003,7 +1003,7 @@ def summarize_prefill(trace_csv, fetch_csv, write_csv, bench_json, cmd):
         rd = [d["FETCH_SIZE"] * 1024 * scale["FETCH_SIZE"] for d in pick(ctr["FETCH_SIZE"], key, sub)]
         wr = [d["WRITE_SIZE"] * 1024 * scale["WRITE_SIZE"] for d in pick(ctr["WRITE_SIZE"], key, sub)]
         r_b, w_b = sum(rd) / len(rd), sum(wr) / len(wr)
-        if key == "snapkv_pass_kernel" and sub == ", 1, ":
+        if key == "snapkv_pass_kernel" and sub == ", 1, 64":
             votes_written = w_b
         rows.append((sorted({_short(d["name"]) for d in tr}), role, len(us), sum(us) / len(us),
                      min(us), max(us), r_b, w_b, a))

@@ -20,11 +20,12 @@
 //   snapkv_select_kernel        per unit: pooled votes, radix select of the
 //       top keep, ordered compaction, plus the window.
 // In the pass kernels all G*n_obs rows of a unit share each 64-key tile,
-// loaded once into LDS as whole 256 B rows; each wave owns a quarter of the
-// rows (16-row MFMA tiles) and computes S = Q K^T on v_mfma_f32_16x16x32_bf16,
+// loaded once into LDS as whole 256 B rows; each wave owns one or two 16-row
+// MFMA tiles of the rows and computes S = Q K^T on v_mfma_f32_16x16x32_bf16,
 // so each lane holds four rows of one key: a key's vote sums inside the lane
 // and across the wave's four lane groups, and the softmax statistics of a
-// row stay in its lanes until the chunk ends.
+// row stay in its lanes until the chunk ends.  A tile costs one barrier: the
+// staging buffers and the per-wave vote sums alternate between two slots.
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
@@ -38,15 +39,16 @@ typedef __bf16 sk_bf16x8 __attribute__((ext_vector_type(8)));
 typedef float sk_f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t sk_u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kSkWaves = 4;
+constexpr int kSkWaves = 4;      // up to 64 rows per unit: four waves of one row tile
+constexpr int kSkWavesWide = 8;  // statistics pass, 65-256 rows: eight waves of one or two row tiles
 constexpr int kSkTile = 64;  // keys per tile: measured 5% faster than 32 keys, 128 slower
 
-template <int D, bool BF16, int KT = kSkTile>
+template <int D, bool BF16, int KT = kSkTile, int WV = kSkWaves>
 struct SkShape {
   static constexpr int ES = BF16 ? 2 : 4;
   static constexpr int KCB = D * ES / 64;     // 16 B A-operand chunks per lane per 16-key block
   static constexpr int LPT = D * ES / 16;     // lanes per key row
-  static constexpr int ROWS_PER_WG_LOAD = kSkWaves * 64 / LPT;  // key rows one pass of all waves loads
+  static constexpr int ROWS_PER_WG_LOAD = WV * 64 / LPT;  // key rows one pass of all waves loads
   static constexpr int NLD = KT / ROWS_PER_WG_LOAD;             // loads per lane per tile
   static constexpr int NB = KT / 16;                             // 16-key MFMA blocks per tile
   static constexpr int KROW = D * ES + 16;    // padded LDS row (odd multiple of 16 B)
@@ -54,14 +56,21 @@ struct SkShape {
 
 }  // namespace
 
-// TW: 16-row tiles per wave (rows per workgroup = 64 * TW); KT: keys per tile.
-template <int D, bool BF16, int TW, bool PAGED, int PASS, int KT>
-__global__ void __launch_bounds__(kSkWaves * 64)
+// TW: 16-row tiles per wave, WV: waves (rows per workgroup = 16 * TW * WV); KT:
+// keys per tile.  The statistics pass runs 65-256 rows as eight waves of one
+// or two row tiles (at 128 rows 21% faster than four waves of two: twice the
+// waves to cover the MFMA, exponential and load latencies; the bf16
+// single-tile instance is held to 80 registers, six waves per SIMD).  The
+// votes pass keeps four waves (the whole call 10% faster than with eight:
+// half the LDS reads of each tile and of the per-wave vote sums).
+template <int D, bool BF16, int TW, bool PAGED, bool WA, int PASS, int KT, int WV>
+__global__ void __launch_bounds__(WV * 64)
+    __attribute__((amdgpu_waves_per_eu(BF16 && WV == 8 && TW == 1 ? 6 : 1)))
 snapkv_pass_kernel(const SnapkvParams p) {
-  using SH = SkShape<D, BF16, KT>;
+  using SH = SkShape<D, BF16, KT, WV>;
   constexpr int NB = SH::NB;
   __shared__ __attribute__((aligned(16))) unsigned char kt[2][KT * SH::KROW];
-  __shared__ float red[kSkWaves][KT];
+  __shared__ float red[2][WV][KT];  // PASS 1: per-wave key sums of two tiles
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -114,36 +123,81 @@ snapkv_pass_kernel(const SnapkvParams p) {
   const int pmask = (1 << p.page_shift) - 1;
 
   // Cooperative tile load: thread -> key row (threadIdx / LPT) + n * ROWS_PER_WG_LOAD,
-  // 16 B chunk threadIdx % LPT.  Keys past the range read element 0 and are masked.
-  // Page ids are read one tile ahead of the K loads that use them, so a
-  // tile's loads never wait on a page-table read.
+  // 16 B chunk threadIdx % LPT; a wave's lanes cover RPW consecutive rows of
+  // each load.  Page ids are read one tile ahead of the K loads that use
+  // them, so a tile's loads never wait on a page-table read.
+  //  WA (pages of at least RPW rows, or contiguous rows): a wave's RPW rows
+  //    lie in one page, so their base address is wave-uniform scalar
+  //    arithmetic and each lane adds a fixed 32-bit offset.  Rows past the
+  //    range read the range's last key (contiguous) or stay inside the page
+  //    of the group's first row; a group wholly past it reads element 0.
+  //  !WA: each lane computes its own row address; keys past the range read
+  //    element 0.  Keys past the range are masked either way.
+  constexpr int RPW = 64 / SH::LPT;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const uint32_t lane_chunk = static_cast<uint32_t>(lane % SH::LPT) * 16;
+  const uint32_t lane_row = static_cast<uint32_t>(lane / SH::LPT);
+  const uint32_t row_bytes = WA ? static_cast<uint32_t>(p.s_tok * SH::ES) : 0;
+  const uint32_t lane_off = lane_row * row_bytes + lane_chunk;
+
+  // Page ids of a tile's loads: per lane (pid[n], !WA), or, with WA, one
+  // vector read in which lane n < NLD fetches load n's id (pid[0]), taken
+  // out with readlane where the load is issued.
   auto load_pids = [&](int (&pid)[SH::NLD], int tile) {
     if constexpr (PAGED) {
-      for (int n = 0; n < SH::NLD; ++n) {
-        const int tt = n * SH::ROWS_PER_WG_LOAD + threadIdx.x / SH::LPT;
-        const int j = v_begin + tile * KT + tt;
-        const bool ok = tile < n_tiles && j < v_end;
-        pid[n] = ptab[ok ? (j >> p.page_shift) : 0];
+      if constexpr (WA) {
+        const int n = lane % SH::NLD;
+        const int jw = v_begin + tile * KT + n * SH::ROWS_PER_WG_LOAD + wave_u * RPW;
+        const bool ok = tile < n_tiles && jw < v_end;
+        const int pg = ptab[ok ? (jw >> p.page_shift) : 0];
+        pid[0] = ok ? pg : -1;
+      } else {
+        for (int n = 0; n < SH::NLD; ++n) {
+          const int tt = n * SH::ROWS_PER_WG_LOAD + threadIdx.x / SH::LPT;
+          const int j = v_begin + tile * KT + tt;
+          const bool ok = tile < n_tiles && j < v_end;
+          pid[n] = ptab[ok ? (j >> p.page_shift) : 0];
+        }
       }
     }
   };
   auto load_tile = [&](sk_u32x4 (&x)[SH::NLD], int tile, const int (&pid)[SH::NLD]) {
+    if (tile >= n_tiles) return;  // past the chunk: nothing to stage
     for (int n = 0; n < SH::NLD; ++n) {
-      const int tt = n * SH::ROWS_PER_WG_LOAD + threadIdx.x / SH::LPT;
-      const int j = v_begin + tile * KT + tt;
-      bool ok = tile < n_tiles && j < v_end;
       int64_t off = 0;
-      if (PAGED) {
-        ok = ok && pid[n] >= 0 && pid[n] < p.num_pages;
-        off = ok ? static_cast<int64_t>(pid[n]) * p.s_blk +
-                       static_cast<int64_t>(j & pmask) * p.s_tok + head_off
-                 : 0;
+      uint32_t voff = lane_chunk;
+      if constexpr (WA) {
+        const int jw = v_begin + tile * KT + n * SH::ROWS_PER_WG_LOAD + wave_u * RPW;
+        voff = lane_off;
+        if constexpr (PAGED) {
+          const int pg = __builtin_amdgcn_readlane(pid[0], n);
+          const bool ok = pg >= 0 && pg < p.num_pages;
+          off = ok ? static_cast<int64_t>(pg) * p.s_blk +
+                         static_cast<int64_t>(jw & pmask) * p.s_tok + head_off
+                   : 0;
+          if (!ok) voff = lane_chunk;
+        } else {
+          const int jc = min(jw, v_end - 1);
+          off = static_cast<int64_t>(b) * p.s_blk + static_cast<int64_t>(jc) * p.s_tok + head_off;
+          if (jw + RPW > v_end)  // a group that reaches past the range
+            voff = min(lane_row, static_cast<uint32_t>(v_end - 1 - jc)) * row_bytes + lane_chunk;
+        }
       } else {
-        off = ok ? static_cast<int64_t>(b) * p.s_blk + static_cast<int64_t>(j) * p.s_tok + head_off
-                 : 0;
+        const int tt = n * SH::ROWS_PER_WG_LOAD + threadIdx.x / SH::LPT;
+        const int j = v_begin + tile * KT + tt;
+        bool ok = j < v_end;
+        if (PAGED) {
+          ok = ok && pid[n] >= 0 && pid[n] < p.num_pages;
+          off = ok ? static_cast<int64_t>(pid[n]) * p.s_blk +
+                         static_cast<int64_t>(j & pmask) * p.s_tok + head_off
+                   : 0;
+        } else {
+          off = ok ? static_cast<int64_t>(b) * p.s_blk + static_cast<int64_t>(j) * p.s_tok + head_off
+                   : 0;
+        }
       }
-      x[n] = __builtin_nontemporal_load(reinterpret_cast<const sk_u32x4*>(
-          kbase + off * SH::ES + (threadIdx.x % SH::LPT) * 16));
+      x[n] = __builtin_nontemporal_load(
+          reinterpret_cast<const sk_u32x4*>(kbase + off * SH::ES + voff));
     }
   };
   auto store_tile = [&](const sk_u32x4 (&x)[SH::NLD], int buf) {
@@ -153,6 +207,9 @@ snapkv_pass_kernel(const SnapkvParams p) {
     }
   };
 
+  // Row statistics in units of the raw score s (the scale is folded into the
+  // exponent's fused multiply-add).
+  const float c2 = p.scale_log2;
   float m_run[TW][4], l_run[TW][4];
   for (int t = 0; t < TW; ++t)
     for (int e = 0; e < 4; ++e) {
@@ -165,10 +222,26 @@ snapkv_pass_kernel(const SnapkvParams p) {
   load_pids(pids, 0);
   load_tile(xr, 0, pids);
   load_pids(pids, 1);
-  for (int tile = 0; tile < n_tiles; ++tile) {
+  const int n_full = n_tiles > 0 ? (v_end - v_begin) / KT : 0;  // tiles with every key in range
+  // Tiles before n_plain hold only in-range keys that every observation
+  // query sees (j < S - n_obs <= its position): no mask.  PASS 1 covers only
+  // such keys, up to its partial last tile.
+  const int n_plain = PASS == 0 ? min(n_full, max(n_pre - v_begin, 0) / KT) : n_tiles;
+  auto reduce_votes = [&](int tile) {  // PASS 1: sum the waves' sums of tile `tile`
+    if (threadIdx.x < KT) {
+      const int j = v_begin + tile * KT + threadIdx.x;
+      if (j < v_end) {
+        float sum = 0.f;
+        for (int w = 0; w < WV; ++w) sum += red[tile & 1][w][threadIdx.x];
+        p.votes[(static_cast<int64_t>(b) * p.Hkv + hk) * p.votes_stride + j] = sum;
+      }
+    }
+  };
+  auto body = [&](int tile, auto masked) {
     const int buf = tile & 1;
     store_tile(xr, buf);
     __syncthreads();
+    if (PASS == 1 && tile > 0) reduce_votes(tile - 1);
     load_tile(xr, tile + 1, pids);  // next tile in flight while this one is used
     load_pids(pids, tile + 2);
     const int v0 = v_begin + tile * KT;
@@ -195,27 +268,27 @@ snapkv_pass_kernel(const SnapkvParams p) {
     }
 
     if constexpr (PASS == 0) {
-      // Online max and sum of 2^(s*scale*log2e) per row, over this lane's NB
-      // keys (one per block); the rescale runs only when the max moves.
-      // (Skipping the mask on tiles before every query and moving the max
-      // lazily, as the attention kernel does, measured slower here.)
+      // Online max and sum of 2^((s - m) * scale * log2e) per row, over this
+      // lane's NB keys (one per block); the rescale runs only when the max moves.
       for (int t = 0; t < TW; ++t)
         for (int e = 0; e < 4; ++e) {
-          const int pos = row_pos[t][e];
           float x[NB];
           float mx = -INFINITY;
           for (int tb = 0; tb < NB; ++tb) {
-            const int j = v0 + tb * 16 + l16;
-            x[tb] = (j < v_end && j <= pos) ? sacc[t][tb][e] * p.scale_log2 : -INFINITY;
+            x[tb] = sacc[t][tb][e];
+            if constexpr (decltype(masked)::value) {
+              const int j = v0 + tb * 16 + l16;
+              if (!(j < v_end && j <= row_pos[t][e])) x[tb] = -INFINITY;
+            }
             mx = fmaxf(mx, x[tb]);
           }
           if (mx > m_run[t][e]) {
-            l_run[t][e] *= __builtin_amdgcn_exp2f(m_run[t][e] - mx);
+            l_run[t][e] *= __builtin_amdgcn_exp2f((m_run[t][e] - mx) * c2);
             m_run[t][e] = mx;
           }
-          const float m_use = m_run[t][e] == -INFINITY ? 0.f : m_run[t][e];
+          const float mc = m_run[t][e] == -INFINITY ? 0.f : m_run[t][e] * c2;
           float s = 0.f;
-          for (int tb = 0; tb < NB; ++tb) s += __builtin_amdgcn_exp2f(x[tb] - m_use);
+          for (int tb = 0; tb < NB; ++tb) s += __builtin_amdgcn_exp2f(fmaf(x[tb], c2, -mc));
           l_run[t][e] += s;
         }
     } else {
@@ -231,19 +304,22 @@ snapkv_pass_kernel(const SnapkvParams p) {
         col[tb] += __shfl_xor(col[tb], 16);
         col[tb] += __shfl_xor(col[tb], 32);
       }
+      // Each wave's sums go to this tile's slots; the four waves' sums are
+      // added after the next tile's barrier (reduce_votes), so a tile needs
+      // one barrier.
       if (grp == 0)
-        for (int tb = 0; tb < NB; ++tb) red[wave][tb * 16 + l16] = col[tb];
-      __syncthreads();
-      if (threadIdx.x < KT) {
-        const int j = v0 + threadIdx.x;
-        if (j < v_end) {
-          float sum = 0.f;
-          for (int w = 0; w < kSkWaves; ++w) sum += red[w][threadIdx.x];
-          p.votes[(static_cast<int64_t>(b) * p.Hkv + hk) * p.votes_stride + j] = sum;
-        }
-      }
+        for (int tb = 0; tb < NB; ++tb) red[buf][wave][tb * 16 + l16] = col[tb];
     }
-    __syncthreads();  // the tile buffer and the reduction slots are reused
+    // No barrier here: the next tile stages into the other buffer, and this
+    // buffer and these sums are rewritten only after the next tile's barrier,
+    // which every wave reaches after finishing this tile.
+  };
+  int tile = 0;
+  for (; tile < n_plain; ++tile) body(tile, std::false_type{});
+  for (; tile < n_tiles; ++tile) body(tile, std::true_type{});
+  if (PASS == 1 && n_tiles > 0) {
+    __syncthreads();
+    reduce_votes(n_tiles - 1);
   }
 
   if constexpr (PASS == 0) {
@@ -251,7 +327,7 @@ snapkv_pass_kernel(const SnapkvParams p) {
     // for this chunk.
     for (int t = 0; t < TW; ++t)
       for (int e = 0; e < 4; ++e) {
-        float m = m_run[t][e], l = l_run[t][e];
+        float m = m_run[t][e] == -INFINITY ? -INFINITY : m_run[t][e] * c2, l = l_run[t][e];
         for (int off = 1; off < 16; off <<= 1) {
           const float mo = __shfl_xor(m, off), lo = __shfl_xor(l, off);
           const float mn = fmaxf(m, mo);
@@ -644,12 +720,28 @@ __global__ void __launch_bounds__(kSelThreads) snapkv_select_kernel(const Snapkv
 
 template <int D, bool BF16, int TW, int PASS>
 static hipError_t sk_launch_tw(const SnapkvParams& p, bool paged, int64_t blocks, hipStream_t s) {
-  if (paged)
-    hipLaunchKernelGGL((snapkv_pass_kernel<D, BF16, TW, true, PASS, kSkTile>), dim3(blocks),
-                       dim3(kSkWaves * 64), 0, s, p);
-  else
-    hipLaunchKernelGGL((snapkv_pass_kernel<D, BF16, TW, false, PASS, kSkTile>), dim3(blocks),
-                       dim3(kSkWaves * 64), 0, s, p);
+  // Wave-uniform row addresses where a wave's rows share a page and the
+  // lane offsets fit 32 bits.
+  using SH = SkShape<D, BF16>;
+  constexpr int RPW = 64 / SH::LPT;
+  const bool wa = (!paged || (int64_t{1} << p.page_shift) >= RPW) &&
+                  p.s_tok >= 0 && p.s_tok * SH::ES * RPW <= (int64_t{1} << 30);
+#define MD_SK_LAUNCH(PG, WAV)                                                                 \
+  do {                                                                                        \
+    if constexpr (TW == 1 || PASS == 1)                                                       \
+      hipLaunchKernelGGL((snapkv_pass_kernel<D, BF16, TW, PG, WAV, PASS, kSkTile, kSkWaves>), \
+                         dim3(blocks), dim3(kSkWaves * 64), 0, s, p);                         \
+    else                                                                                      \
+      hipLaunchKernelGGL((snapkv_pass_kernel<D, BF16, TW / 2, PG, WAV, PASS, kSkTile,         \
+                                             kSkWavesWide>),                                  \
+                         dim3(blocks), dim3(kSkWavesWide * 64), 0, s, p);                     \
+  } while (0)
+  if (paged) {
+    if (wa) MD_SK_LAUNCH(true, true); else MD_SK_LAUNCH(true, false);
+  } else {
+    if (wa) MD_SK_LAUNCH(false, true); else MD_SK_LAUNCH(false, false);
+  }
+#undef MD_SK_LAUNCH
   return hipGetLastError();
 }
 

@@ -30,6 +30,13 @@ VOTES = [
     ("f32_g2_obs8_d64", 2, 8, 4, 2, 64, [100, 45], "f32", 0),
     ("bf16_g1_obs32_long", 1, 32, 2, 2, 128, [6000], "bf16", 16),
     ("bf16_short_prompts", 3, 16, 4, 1, 64, [16, 17, 40], "bf16", 0),
+    # the eight-wave instances (65-256 rows) in each address form: rows of a
+    # wave in one page, pages smaller than a wave's rows, contiguous
+    ("f32_g4_obs32_d64_paged", 2, 32, 8, 2, 64, [1500, 700], "f32", 16),
+    ("bf16_g8_obs32_d64_paged4", 2, 32, 16, 2, 64, [1100, 2000], "bf16", 4),
+    ("f32_g8_obs32_d128", 1, 32, 8, 1, 128, [1300], "f32", 0),
+    ("bf16_g4_obs32_paged2", 1, 32, 8, 2, 128, [777], "bf16", 2),
+    ("bf16_g3_obs29_ragged", 3, 29, 6, 2, 128, [29, 95, 3001], "bf16", 16),
 ]
 
 
