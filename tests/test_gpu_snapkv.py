@@ -67,6 +67,30 @@ def test_votes_against_oracle(case):
     say(f"  {name}: max err / bound = {worst:.3f}")
 
 
+def _random_votes_case(seed):
+    """A seeded problem across the votes kernels' paths: 16-256 rows (four or
+    eight waves, one to four row tiles), both head dims and dtypes, pages
+    from 1 token (per-lane addresses) to 64 or a contiguous cache, prompts
+    from the bare window to a few thousand tokens (partial tiles, chunk
+    edges, the masked window tiles)."""
+    rng = np.random.default_rng(5000 + seed)
+    combos = [(1, 8), (2, 16), (2, 32), (4, 16), (4, 29), (4, 32), (8, 16), (8, 29), (8, 32),
+              (16, 16)]  # (G, n_obs): 8 to 256 rows
+    G, n_obs = combos[int(rng.integers(len(combos)))]
+    Hkv = int(rng.choice([1, 2]))
+    d = int(rng.choice([64, 128]))
+    dtype = str(rng.choice(["bf16", "bf16", "f32"]))
+    page = int(rng.choice([0, 1, 2, 4, 16, 64]))
+    B = int(rng.integers(1, 4))
+    lens = [int(x) for x in rng.integers(n_obs, n_obs + int(rng.choice([60, 900, 4000])), size=B)]
+    return (f"random{seed}", B, n_obs, G * Hkv, Hkv, d, lens, dtype, page)
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_votes_random(seed):
+    test_votes_against_oracle(_random_votes_case(seed))
+
+
 # rows, stride, n_obs, budget, pool, prompt lens (per sequence), Hkv
 SELECT = [
     (3, 500, 32, 64, 5, [532, 300, 40], 2),
