@@ -1189,6 +1189,61 @@ def summarize_lds(csv_path, bench_json, cmd):
     return "\n".join(out) + "\n"
 
 
+ISSUE_COUNTERS = ["SQ_WAVES", "SQ_WAVE_CYCLES", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY",
+                  "SQ_ACTIVE_INST_VALU", "SQ_INSTS_VALU", "SQ_INSTS_VALU_TRANS_F32",
+                  "SQ_BUSY_CYCLES", "GRBM_GUI_ACTIVE"]
+
+
+def summarize_issue(csv_path, bench_json, cmd, num_cus=256):
+    """Where the waves of the SnapKV passes (and, for reference, the bench's
+    verify and draft) spend their time: wave-cycles waiting for anything
+    (a dependency: memory, LDS, a barrier) against waiting to issue (a ready
+    instruction held back by a busy unit), the VALU busy fraction as
+    rocprofv3's VALUBusy defines it, and VALU and transcendental instructions
+    per wave, from one --pmc pass over a bench run."""
+    rec = _bench_line(bench_json)
+    W, K, S0 = rec["warmup"], rec["steps"], settle_count(rec)
+    ds = _dispatches(_rows(csv_path))
+    ver, dra = timed_calls(ds, W, K, S0)
+    role = {ver[0][0]["name"]: "verify (bench)", dra[0][0]["name"]: "draft (bench)"}
+    groups = {}
+    for d in ds:
+        if d["name"] in role or "snapkv_pass_kernel" in d["name"]:
+            groups.setdefault(d["name"], []).append(d)
+    out = ["# Issue and wait counters of the SnapKV passes (rocprofv3 --pmc)",
+           "",
+           f"Workload: the prompts of {WORKLOAD} (B = 64 prompts of 32768 tokens, Llama-3.1-8B",
+           "heads, 16-token pages, 32 observation queries: 128 rows per kv head); the bench's",
+           "verify and draft for reference.  One MI355X (gfx950).  Means per dispatch over every",
+           "dispatch of each kernel instance.",
+           "",
+           "Command (from /tmp with TMPDIR=/tmp; R = the repository root):",
+           "",
+           f"    {cmd}",
+           "",
+           "wait (any) = SQ_WAIT_ANY / SQ_WAVE_CYCLES: the share of wave time spent waiting on",
+           "a dependency (memory, LDS, a barrier); wait (issue) = SQ_WAIT_INST_ANY /",
+           "SQ_WAVE_CYCLES: the share spent with an instruction ready but not issued (a busy",
+           "unit); VALU busy = 100 x SQ_ACTIVE_INST_VALU / CUs / GRBM_GUI_ACTIVE (rocprofv3's",
+           "VALUBusy, quad-cycle units as it reports them).",
+           "",
+           "| kernel | dispatches | waves | wait (any) | wait (issue) | VALU busy % | VALU insts / wave | transcendental / wave |",
+           "|---|---|---|---|---|---|---|---|"]
+    for name, dl in sorted(groups.items(), key=lambda kv: -sum(d.get("SQ_WAVE_CYCLES", 0) for d in kv[1])):
+        m = {c: sum(d.get(c, 0.0) for d in dl) / len(dl) for c in ISSUE_COUNTERS}
+        wc = m["SQ_WAVE_CYCLES"] or 1.0
+        waves = m["SQ_WAVES"] or 1.0
+        busy = 100.0 * m["SQ_ACTIVE_INST_VALU"] / num_cus / (m["GRBM_GUI_ACTIVE"] or 1.0)
+        label = (role[name] + " " if name in role else "") + f"`{_short(name)}`"
+        out.append(f"| {label} | {len(dl)} | {m['SQ_WAVES']:.0f} | {m['SQ_WAIT_ANY'] / wc:.3f} | "
+                   f"{m['SQ_WAIT_INST_ANY'] / wc:.3f} | {busy:.1f} | {m['SQ_INSTS_VALU'] / waves:.0f} | "
+                   f"{m['SQ_INSTS_VALU_TRANS_F32'] / waves:.0f} |")
+    snap = os.path.join(ROOT, "paper_2408_11049_amd", "csrc", "snapkv.hip")
+    out += ["", f"kernel_source_sha256: {kernel_source_sha256()}",
+            f"snapkv_source_sha256: {kernel_source_sha256([snap])}"]
+    return "\n".join(out) + "\n"
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -1202,7 +1257,8 @@ def main():
     ap.add_argument("--paged-ab", action="store_true",
                     help="only the paged / sequential-page / contiguous verify A/B (profiles/)")
     ap.add_argument("--summarize", choices=["trace", "counters", "mfma", "latency", "paged", "lds",
-                                            "configs", "config-counters", "prefill", "steps"])
+                                            "configs", "config-counters", "prefill", "steps",
+                                            "issue"])
     ap.add_argument("--csv", nargs="+")
     ap.add_argument("--bench-json", nargs="+")
     ap.add_argument("--cmd", default="")
@@ -1215,6 +1271,7 @@ def main():
               "latency": lambda: summarize_latency(args.csv[0], args.bench_json[0], args.cmd),
               "paged": lambda: summarize_paged(args.csv[0], args.bench_json[0], args.cmd),
               "lds": lambda: summarize_lds(args.csv[0], args.bench_json[0], args.cmd),
+              "issue": lambda: summarize_issue(args.csv[0], args.bench_json[0], args.cmd),
               "configs": lambda: summarize_configs(args.csv[0], args.bench_json[0], args.cmd),
               "config-counters": lambda: summarize_config_counters(
                   args.csv[0], args.csv[1], args.bench_json[0], args.bench_json[-1], args.cmd),

@@ -33,10 +33,19 @@ def _flags():
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 
+# Per-source flags.  snapkv.hip: MFMA results in VGPRs rather than AGPRs.
+# The SnapKV passes fit their register budgets either way, and the vector
+# work that reads each score then needs no copy out of an AGPR (32 per
+# 64-key tile and wave in the votes pass; measured 1.6% on the votes call,
+# votes identical).
+EXTRA_FLAGS = {"snapkv.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+
 def _compile(src: str, verbose: bool) -> str:
     obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
     lang = ["-x", "hip"] if src.endswith(".hip") else []
-    cmd = [hipcc()] + _flags() + lang + ["-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = ([hipcc()] + _flags() + EXTRA_FLAGS.get(src, []) + lang +
+           ["-c", os.path.join(CSRC, src), "-o", obj])
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -207,13 +207,14 @@ snapkv_pass_kernel(const SnapkvParams p) {
     }
   };
 
-  // Row statistics in units of the raw score s (the scale is folded into the
-  // exponent's fused multiply-add).
+  // Row statistics: the running max in the exponent's units (score x scale
+  // x log2e, the scale folded into the exponent's fused multiply-add) and
+  // the running sum.
   const float c2 = p.scale_log2;
-  float m_run[TW][4], l_run[TW][4];
+  float mc_run[TW][4], l_run[TW][4];  // running max x scale x log2e, and sum
   for (int t = 0; t < TW; ++t)
     for (int e = 0; e < 4; ++e) {
-      m_run[t][e] = -INFINITY;
+      mc_run[t][e] = -INFINITY;
       l_run[t][e] = 0.f;
     }
 
@@ -268,8 +269,10 @@ snapkv_pass_kernel(const SnapkvParams p) {
     }
 
     if constexpr (PASS == 0) {
-      // Online max and sum of 2^((s - m) * scale * log2e) per row, over this
-      // lane's NB keys (one per block); the rescale runs only when the max moves.
+      // Online max and sum of 2^(s * scale * log2e - mc) per row, over this
+      // lane's NB keys (one per block), with mc the running max in the
+      // exponent's units; the sum is rescaled on every tile (a select on a
+      // moved max costs more than the multiply-add it saves).
       for (int t = 0; t < TW; ++t)
         for (int e = 0; e < 4; ++e) {
           float x[NB];
@@ -282,14 +285,16 @@ snapkv_pass_kernel(const SnapkvParams p) {
             }
             mx = fmaxf(mx, x[tb]);
           }
-          if (mx > m_run[t][e]) {
-            l_run[t][e] *= __builtin_amdgcn_exp2f((m_run[t][e] - mx) * c2);
-            m_run[t][e] = mx;
-          }
-          const float mc = m_run[t][e] == -INFINITY ? 0.f : m_run[t][e] * c2;
+          const float mcn = fmaxf(mc_run[t][e], mx * c2);
+          // Unmasked tiles come first and give every row a finite max on
+          // the first of them; only masked tiles can meet a row with none
+          // (then the sums use 0 as reference and the max stays -inf).
+          float mcu = mcn;
+          if constexpr (decltype(masked)::value) mcu = mcn == -INFINITY ? 0.f : mcn;
           float s = 0.f;
-          for (int tb = 0; tb < NB; ++tb) s += __builtin_amdgcn_exp2f(fmaf(x[tb], c2, -mc));
-          l_run[t][e] += s;
+          for (int tb = 0; tb < NB; ++tb) s += __builtin_amdgcn_exp2f(fmaf(x[tb], c2, -mcu));
+          l_run[t][e] = fmaf(l_run[t][e], __builtin_amdgcn_exp2f(mc_run[t][e] - mcu), s);
+          mc_run[t][e] = mcn;
         }
     } else {
       // p = 2^(s*scale*log2e - lse2) summed over every row, per key: inside
@@ -327,7 +332,7 @@ snapkv_pass_kernel(const SnapkvParams p) {
     // for this chunk.
     for (int t = 0; t < TW; ++t)
       for (int e = 0; e < 4; ++e) {
-        float m = m_run[t][e] == -INFINITY ? -INFINITY : m_run[t][e] * c2, l = l_run[t][e];
+        float m = mc_run[t][e], l = l_run[t][e];
         for (int off = 1; off < 16; off <<= 1) {
           const float mo = __shfl_xor(m, off), lo = __shfl_xor(l, off);
           const float mn = fmaxf(m, mo);
