@@ -39,7 +39,7 @@ typedef __bf16 sk_bf16x8 __attribute__((ext_vector_type(8)));
 typedef float sk_f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t sk_u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kSkWaves = 4;      // up to 64 rows per unit: four waves of one row tile
+constexpr int kSkWaves = 4;      // up to 64 rows, and the votes pass at any row count
 constexpr int kSkWavesWide = 8;  // statistics pass, 65-256 rows: eight waves of one or two row tiles
 constexpr int kSkTile = 64;  // keys per tile: measured 5% faster than 32 keys, 128 slower
 
@@ -58,11 +58,11 @@ struct SkShape {
 
 // TW: 16-row tiles per wave, WV: waves (rows per workgroup = 16 * TW * WV); KT:
 // keys per tile.  The statistics pass runs 65-256 rows as eight waves of one
-// or two row tiles (at 128 rows 21% faster than four waves of two: twice the
-// waves to cover the MFMA, exponential and load latencies; the bf16
-// single-tile instance is held to 80 registers, six waves per SIMD).  The
-// votes pass keeps four waves (the whole call 10% faster than with eight:
-// half the LDS reads of each tile and of the per-wave vote sums).
+// or two row tiles (more waves to cover the MFMA, exponential and load
+// latencies; the bf16 single-tile instance is held to 80 registers, six
+// waves per SIMD).  The votes pass keeps four waves (the whole call 10%
+// faster than with eight: half the LDS reads of each tile and of the
+// per-wave vote sums).
 template <int D, bool BF16, int TW, bool PAGED, bool WA, int PASS, int KT, int WV>
 __global__ void __launch_bounds__(WV * 64)
     __attribute__((amdgpu_waves_per_eu(BF16 && WV == 8 && TW == 1 ? 6 : 1)))
