@@ -305,3 +305,41 @@ def test_steps_summary_groups_by_grid(tmp_path):
     assert small.rstrip(" |").endswith("--")
     assert arg.rstrip(" |").endswith("1.0000") and "| 4.00 |" in arg
     assert "bench_copy" not in text
+
+
+def test_issue_summary(tmp_path):
+    """--summarize issue: per-instance means of the SQ issue and wait counters
+    for the SnapKV passes and the bench's timed verify and draft; the wait
+    shares are ratios to the wave-cycles, instructions are per wave."""
+    import csv
+    import json
+    V = "void md::attn_partial_kernel<128, true, 2, true, false, 1, 1, true, 4>(md::AttnParams)"
+    D = "void md::attn_partial_kernel<128, true, 2, true, false, 1, 2, false, 8>(md::AttnParams)"
+    P0 = "void md::snapkv_pass_kernel<128, true, 1, true, true, 0, 64, 8>(md::SnapkvParams)"
+    C = "md::bench_copy_kernel(x)"
+    # counters per kernel: waves, wave-cycles, wait any, wait issue, valu active, valu insts,
+    # transcendental, busy, gui active
+    ctr = {V: (4, 1000, 380, 80, 250, 4000, 200, 10, 1000),
+           D: (8, 1000, 330, 370, 300, 800, 40, 10, 1000),
+           P0: (100, 1000, 400, 350, 136, 5000, 700, 10, 1000),
+           C: (1, 10, 1, 1, 1, 1, 0, 1, 10)}
+    seq = [C, V, D, V, D, P0, P0]
+    path = tmp_path / "c.csv"
+    with open(path, "w", newline="") as f:
+        w = csv.writer(f)
+        w.writerow(["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
+        for i, n in enumerate(seq):
+            for c, v in zip(bench.ISSUE_COUNTERS, ctr[n]):
+                w.writerow([i + 1, n, c, v])
+    bj = tmp_path / "b.json"
+    bj.write_text(json.dumps({"metric": "m", "value": 1, "unit": "GB/s", "steps": 1, "warmup": 1,
+                              "detail": {}}) + "\n")
+    text = bench.summarize_issue(str(path), str(bj), "cmd")
+    rows = [r for r in text.splitlines() if r.startswith("| ") and not r.startswith("| kernel")]
+    assert len(rows) == 3 and "bench_copy" not in text
+    by = {("verify" if "verify (bench)" in r else "draft" if "draft (bench)" in r else "pass0"): r
+          for r in rows}
+    cells = [c.strip() for c in by["pass0"].split("|")[1:-1]]
+    assert cells[1:] == ["2", "100", "0.400", "0.350", "0.1", "50", "7"]  # busy: 100 x 136 / 256 / 1000
+    assert by["draft"].split("|")[5].strip() == "0.370"
+    assert "kernel_source_sha256:" in text and "snapkv_source_sha256:" in text
